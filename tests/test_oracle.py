@@ -1,0 +1,411 @@
+"""Pins for the CPU oracle: each check ties it to something other than itself.
+
+Sources of truth used here: values the paper prints (tests/golden/
+paper_numbers.json), hand-worked encodings (tests/golden/tiled_cbc_hand.json),
+brute force in exact arithmetic on tiny inputs, closed forms and invariants.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from conftest import GOLDEN
+
+
+def _hand_cases():
+    with open(os.path.join(GOLDEN, "tiled_cbc_hand.json")) as fh:
+        return json.load(fh)["cases"]
+
+
+def _paper():
+    with open(os.path.join(GOLDEN, "paper_numbers.json")) as fh:
+        return json.load(fh)
+
+
+def _hand_matrix(case):
+    w = np.zeros((case["rows"], case["cols"]), dtype=np.uint16)
+    for m, k, h in case["nonzeros"]:
+        w[m, k] = int(h, 16)
+    return w
+
+
+def _exact(h):
+    """Exact rational value of an fp16 bit pattern (finite only), no NumPy floats."""
+    h = int(h)
+    sign = -1 if h & 0x8000 else 1
+    e = (h >> 10) & 0x1F
+    f = h & 0x3FF
+    assert e != 0x1F
+    if e == 0:
+        return sign * Fraction(f, 1 << 24)
+    return sign * Fraction(1024 + f, 1024) * Fraction(2) ** (e - 15)
+
+
+# ---------------------------------------------------------------------------
+# Tiled-CBC encoding
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("case", _hand_cases(), ids=lambda c: c["name"])
+def test_encode_matches_hand_worked_case(case):
+    w = _hand_matrix(case)
+    for enc in (oracle.encode, oracle.encode_brute):
+        f = enc(w, case["tile_m"], case["tile_k"])
+        assert f.tile_offset.tolist() == case["tile_offset"]
+        assert f.col_info.tolist() == [int(v, 16) for v in case["col_info"]]
+        assert f.bitmap.tolist() == [int(v, 16) for v in case["bitmap"]]
+        assert f.values.tolist() == [int(v, 16) for v in case["values"]]
+
+
+@pytest.mark.parametrize("case", _hand_cases(), ids=lambda c: c["name"])
+def test_product_matches_hand_worked_case(case):
+    w = _hand_matrix(case).view(np.float16)
+    for prod in case["products"]:
+        x = np.array([prod["x"]], dtype=np.float16)
+        y64, s64, y16 = oracle.spmspv(w, x, prod["t"])
+        expect = np.zeros(case["rows"])
+        for m, v in prod["y_nonzero"]:
+            expect[m] = v
+        assert np.array_equal(y64[0], expect)
+        assert np.array_equal(y16[0].astype(np.float64), expect)
+
+
+def test_padding_example_from_paper():
+    pad = _paper()["column_padding"]
+    w = np.zeros((64, 1), dtype=np.float16)
+    w[:pad["nnz"], 0] = np.float16(1.5)
+    f = oracle.encode(w, 64, 1)
+    assert f.values.size * 2 == pad["padded_bytes"]
+    assert f.values.size * 2 - pad["nnz"] * 2 == pad["pad_bytes"]
+
+
+def test_bitmap_words_per_column_from_paper():
+    p = _paper()["bitmap_words_per_column"]
+    w = synth.weights(p["tile_m"], 3, 7)
+    f = oracle.encode(w, p["tile_m"], 1)
+    assert f.bitmap.size == 3 * p["words"]
+
+
+@pytest.mark.parametrize("rows,cols,tm,tk,sw,seed", [
+    (64, 1, 64, 1, 0.0, 1), (64, 16, 64, 16, 0.5, 2), (130, 37, 64, 4, 0.6, 3),
+    (200, 33, 128, 8, 0.3, 4), (256, 40, 256, 16, 0.7, 5), (70, 9, 192, 2, 0.9, 6),
+    (65, 65, 64, 64, 0.5, 7), (129, 5, 1024, 1, 0.2, 8), (1, 1, 64, 1, 0.0, 9),
+])
+def test_encode_equals_scalar_brute_force(rows, cols, tm, tk, sw, seed):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, seed), sw)
+    a = oracle.encode(w, tm, tk)
+    b = oracle.encode_brute(w, tm, tk)
+    for name in ("tile_offset", "col_info", "bitmap", "values"):
+        assert np.array_equal(getattr(a, name), getattr(b, name)), name
+
+
+@pytest.mark.parametrize("rows,cols,tm,tk,sw,seed", [
+    (300, 70, 128, 16, 0.6, 11), (256, 256, 256, 16, 0.5, 12), (97, 130, 64, 32, 0.8, 13),
+    (512, 64, 512, 8, 0.0, 14), (1024, 48, 1024, 16, 0.95, 15),
+])
+def test_encode_round_trip_and_invariants(rows, cols, tm, tk, sw, seed):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, seed), sw)
+    f = oracle.encode(w, tm, tk)
+    # round trip: decoding gives back W_sp bit for bit (pruned entries are +0)
+    assert np.array_equal(oracle.decode(f).view(np.uint16), w.view(np.uint16))
+    wb = w.view(np.uint16)
+    nnz = int(((wb & 0x7FFF) != 0).sum())
+    # popcount of every bitmap equals the number of stored nonzeros
+    pop = sum(bin(int(v)).count("1") for v in f.bitmap)
+    assert pop == nnz == int(sum(int(c) & 0xFFFF for c in f.col_info))
+    wpc = tm // 64
+    for idx, ci in enumerate(f.col_info):
+        words = f.bitmap[idx * wpc:(idx + 1) * wpc]
+        assert sum(bin(int(v)).count("1") for v in words) == (int(ci) & 0xFFFF)
+        assert (int(ci) >> 16) % 8 == 0
+    # TileOffset: starts at 0, nondecreasing, multiples of 8, ends at len(values)
+    to = f.tile_offset.astype(np.int64)
+    assert to[0] == 0 and np.all(np.diff(to) >= 0) and np.all(to % 8 == 0)
+    assert to[-1] == f.values.size
+    # padding entries are +0; stored entries are nonzero
+    used = np.zeros(f.values.size, dtype=bool)
+    for r in range(f.n_stripes):
+        for k in range(f.n_colblocks * tk):
+            g = r * f.n_colblocks + k // tk
+            ci = int(f.col_info[g * tk + k % tk])
+            base = int(f.tile_offset[g]) + (ci >> 16)
+            used[base:base + (ci & 0xFFFF)] = True
+    assert np.all(f.values[~used] == 0)
+    assert np.all((f.values[used] & 0x7FFF) != 0)
+    # Sec. 4.1 storage formula equals the byte count of the arrays without padding
+    assert oracle.unpadded_bytes(f) == oracle.storage_bytes(rows, cols, tm, tk, nnz)
+
+
+def test_storage_formula_worked_numbers():
+    p = _paper()["storage_llama7b_attn_50"]
+    total = oracle.storage_bytes(p["rows"], p["cols"], p["tile_m"], p["tile_k"], p["nnz"])
+    assert total == p["total_bytes"]
+    assert total == p["tile_offset_bytes"] + p["col_info_bytes"] + p["bitmap_bytes"] + p["values_bytes"]
+
+
+def test_negative_zero_is_not_stored():
+    w = np.zeros((64, 2), dtype=np.uint16)
+    w[:, 0] = 0x8000
+    w[7, 1] = 0x8001  # smallest negative subnormal: nonzero
+    f = oracle.encode(w, 64, 2)
+    assert f.bitmap.tolist() == [0, 1 << 7]
+    assert f.values.tolist()[:1] == [0x8001]
+    assert np.array_equal(oracle.decode(f).view(np.uint16)[:, 1], w[:, 1])
+    assert np.all(oracle.decode(f).view(np.uint16)[:, 0] == 0)
+
+
+@pytest.mark.parametrize("tm,tk", [(32, 1), (100, 1), (1088, 1), (64, 3), (64, 512), (1024, 65)])
+def test_encode_rejects_bad_tiles(tm, tk):
+    with pytest.raises(ValueError):
+        oracle.encode(np.zeros((4, 4), dtype=np.float16), tm, tk)
+
+
+# ---------------------------------------------------------------------------
+# Magnitude pruning
+# ---------------------------------------------------------------------------
+
+def _prune_brute(w, sparsity):
+    flat = [int(v) for v in w.view(np.uint16).reshape(-1)]
+    n = math.floor(sparsity * len(flat))
+    keyed = sorted(range(len(flat)), key=lambda i: (abs(_exact(flat[i])), i))
+    out = list(flat)
+    for i in keyed[:n]:
+        out[i] = 0
+    return np.array(out, dtype=np.uint16).reshape(w.shape)
+
+
+@pytest.mark.parametrize("shape,sw,seed", [((8, 8), 0.5, 1), ((13, 7), 0.3, 2), ((5, 40), 0.77, 3),
+                                           ((16, 16), 0.0, 4), ((9, 9), 1.0, 5)])
+def test_prune_equals_brute_force(shape, sw, seed):
+    w = synth.weights(*shape, seed)
+    got = oracle.magnitude_prune(w, sw).view(np.uint16)
+    assert np.array_equal(got, _prune_brute(w, sw))
+
+
+def test_prune_tie_break_and_signed_zero():
+    # equal magnitudes of both signs plus -0: the cut falls inside the tie
+    w = np.array([[0.5, -0.5, 0.25, -0.0], [0.5, 1.0, -0.25, 0.5]], dtype=np.float16)
+    got = oracle.magnitude_prune(w, 0.5).view(np.uint16)
+    # order by (|w|, index): idx3 (-0), idx2 (0.25), idx6 (-0.25), idx0 (0.5) are the four smallest
+    expect = w.view(np.uint16).copy().reshape(-1)
+    expect[[3, 2, 6, 0]] = 0
+    assert np.array_equal(got.reshape(-1), expect)
+
+
+def test_prune_invariants_medium():
+    w = synth.weights(256, 192, 21)
+    w[3, :40] = np.float16(0.0)  # some entries already zero
+    sw = 0.6
+    p = oracle.magnitude_prune(w, sw)
+    wb, pb = w.view(np.uint16).reshape(-1), p.view(np.uint16).reshape(-1)
+    mag = np.abs(w.astype(np.float64)).reshape(-1)
+    n = math.floor(sw * w.size)
+    z = int(((wb & 0x7FFF) == 0).sum())
+    # the output differs from the input only where it became +0
+    assert np.all((pb == wb) | (pb == 0))
+    # exactly max(n, #already-zero) entries have zero magnitude afterwards
+    out_zero = (pb & 0x7FFF) == 0
+    assert out_zero.sum() == max(n, z)
+    # every kept magnitude is at least every pruned magnitude
+    assert mag[~out_zero].min() >= mag[out_zero].max()
+
+
+def test_prune_rejects_nan():
+    with pytest.raises(ValueError):
+        oracle.magnitude_prune(np.array([[np.nan, 1]], dtype=np.float16), 0.5)
+
+
+# ---------------------------------------------------------------------------
+# Threshold and activity
+# ---------------------------------------------------------------------------
+
+def _threshold_brute(x, p):
+    if p == 0:
+        return -1.0
+    mags = [abs(_exact(h)) for h in x.view(np.uint16).reshape(-1)]
+    need = math.ceil(p * len(mags))
+    # smallest candidate magnitude v with #{|x| <= v} >= need
+    return float(min(v for v in set(mags) if sum(1 for m in mags if m <= v) >= need))
+
+
+@pytest.mark.parametrize("p", [0.0, 0.1, 0.25, 0.5, 0.7, 0.99, 1.0])
+def test_threshold_equals_counting_definition(p):
+    x = synth.laplace_activations(3, 50, 31)
+    assert float(oracle.threshold_for(x, p)) == _threshold_brute(x, p)
+
+
+def test_threshold_with_ties():
+    x = np.array([[1.0, -1.0, 1.0, 2.0, 0.0, -0.0, 3.0, 1.0]], dtype=np.float16)
+    t = oracle.threshold_for(x, 0.5)  # 4th smallest of 0,0,1,1,1,1,2,3 is 1
+    assert t == np.float32(1.0)
+    act = oracle.active_mask(x, t)
+    assert act.tolist() == [[False, False, False, True, False, False, True, False]]
+
+
+def test_active_mask_elementwise_definition():
+    bits = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16).reshape(1, -1)
+    for t in (-1.0, 0.0, 6e-8, 0.5, 0.50006, 1.0, 65504.0, 70000.0, float("inf")):
+        t32 = float(np.float32(t))
+        act = oracle.active_mask(x, t)[0]
+        for h in list(range(0, 1 << 16, 97)) + [0x7C00, 0xFC00, 0x7C01, 0xFE00, 0x7BFF, 0x0001, 0x8000]:
+            e, f = (h >> 10) & 0x1F, h & 0x3FF
+            if e == 0x1F:
+                expect = (f == 0) and (math.inf > t32)  # +-inf vs t; NaN is never active
+            else:
+                expect = abs(float(_exact(h))) > t32  # both sides exact in a Python float
+            assert bool(act[h]) == expect, (h, t)
+
+
+def test_masked_activations_keep_bits():
+    x = synth.laplace_activations(2, 64, 5)
+    t = oracle.threshold_for(x, 0.5)
+    xm = oracle.masked_activations(x, t)
+    act = oracle.active_mask(x, t)
+    assert np.array_equal(xm.view(np.uint16)[act], x.view(np.uint16)[act])
+    assert np.all(xm.view(np.uint16)[~act] == 0)
+
+
+# ---------------------------------------------------------------------------
+# The masked product
+# ---------------------------------------------------------------------------
+
+def _product_exact(w, x, t):
+    M, K = w.shape
+    B = x.shape[0]
+    tt = Fraction(float(np.float32(t)))
+    out = [[Fraction(0)] * M for _ in range(B)]
+    wb, xb = w.view(np.uint16), x.view(np.uint16)
+    for b in range(B):
+        for k in range(K):
+            xv = _exact(xb[b, k])
+            if not abs(xv) > tt:
+                continue
+            for m in range(M):
+                out[b][m] += _exact(wb[m, k]) * xv
+    return out
+
+
+@pytest.mark.parametrize("M,K,B,sw,p,seed", [(7, 9, 1, 0.5, 0.5, 1), (16, 20, 3, 0.3, 0.25, 2),
+                                             (5, 33, 2, 0.0, 0.0, 3), (12, 12, 4, 0.9, 0.7, 4)])
+def test_product_equals_exact_brute_force(M, K, B, sw, p, seed):
+    w = oracle.magnitude_prune(synth.weights(M, K, seed), sw)
+    x = synth.laplace_activations(B, K, seed + 100)
+    t = oracle.threshold_for(x, p)
+    y64, s64, y16 = oracle.spmspv(w, x, t)
+    ex = _product_exact(w, x, t)
+    for b in range(B):
+        for m in range(M):
+            assert abs(Fraction(float(y64[b, m])) - ex[b][m]) <= Fraction(1, 10**12) * (1 + abs(ex[b][m]))
+            # y16 is the fp16 nearest to the exact value (ties far from likely)
+            assert abs(float(y16[b, m]) - float(ex[b][m])) <= abs(float(np.float16(float(ex[b][m]))) - float(ex[b][m])) + 1e-30
+
+
+def test_dense_no_threshold_is_plain_gemv():
+    w = synth.weights(40, 30, 9)
+    x = synth.laplace_activations(1, 30, 10)
+    y64, _, _ = oracle.spmspv(w, x, -1.0)
+    ex = _product_exact(w, x, -1.0)
+    assert np.allclose(y64[0], [float(v) for v in ex[0]], rtol=1e-13, atol=0)
+
+
+def test_all_inactive_gives_zero():
+    w = synth.weights(33, 17, 3)
+    x = synth.laplace_activations(2, 17, 4)
+    t = float(np.abs(x.astype(np.float64)).max())
+    y64, s64, y16 = oracle.spmspv(w, x, t)
+    assert np.all(y64 == 0) and np.all(s64 == 0) and np.all(y16.astype(np.float64) == 0)
+
+
+def test_single_active_column_is_scaled_column():
+    w = synth.weights(50, 12, 5)
+    x = np.full((1, 12), 0.25, dtype=np.float16)
+    x[0, 7] = np.float16(-3.0)
+    y64, _, _ = oracle.spmspv(w, x, 1.0)
+    assert np.array_equal(y64[0], -3.0 * w[:, 7].astype(np.float64))
+
+
+def test_rows_subset_agrees():
+    w = oracle.magnitude_prune(synth.weights(64, 48, 8), 0.5)
+    x = synth.laplace_activations(3, 48, 9)
+    t = oracle.threshold_for(x, 0.4)
+    y64, s64, _ = oracle.spmspv(w, x, t)
+    rows = [0, 5, 63, 17]
+    ex = _product_exact(w, x, t)
+    yr, sr = oracle.spmspv_rows(w, x, t, rows)
+    for b in range(3):
+        for i, m in enumerate(rows):
+            assert abs(yr[b, i] - float(ex[b][m])) <= 1e-12 * (1 + abs(float(ex[b][m])))
+    assert np.allclose(sr, s64[:, rows])
+
+
+# ---------------------------------------------------------------------------
+# Sec. 3 arithmetic and the byte model
+# ---------------------------------------------------------------------------
+
+def test_combined_sparsity_paper_numbers():
+    for c in _paper()["combined_sparsity"]:
+        ov, tot = oracle.combined_sparsity(c["sp"], c["dp"])
+        assert tot == pytest.approx(c["total"], abs=1e-12)
+        if "overlap" in c:
+            assert ov == pytest.approx(c["overlap"], abs=1e-12)
+        assert tot == pytest.approx(1 - (1 - c["sp"]) * (1 - c["dp"]), abs=1e-12)
+
+
+def test_intensity_formulas_from_flops_and_bytes():
+    # Eq. 2 is FLOPs / bytes with FLOPs = 2 M K N and bytes = 2 M K / CR + 2 K N
+    for M, K, N, cr in [(4096, 4096, 1, 1.0), (8192, 1024, 8, 2.7), (11008, 4096, 32, 1.3)]:
+        flops, byts = 2 * M * K * N, 2 * M * K / cr + 2 * K * N
+        assert oracle.compute_intensity(M, N, cr) == pytest.approx(flops / byts, rel=1e-12)
+        # Eq. 3 with s = 0 is Eq. 2; with s, only the weight bytes shrink
+        assert oracle.compute_intensity_spdp(M, N, cr, 0.0) == pytest.approx(flops / byts, rel=1e-12)
+        s = 0.5
+        byts_s = 2 * M * K / cr * (1 - s) + 2 * K * N
+        assert oracle.compute_intensity_spdp(M, N, cr, s) == pytest.approx(flops / byts_s, rel=1e-12)
+    assert oracle.compression_ratio(4096, 4096, 19152900) == pytest.approx(2 * 4096 * 4096 / 19152900)
+    assert oracle.attainable(100.0, 2.0, 8.0) == 16.0 and oracle.attainable(10.0, 2.0, 8.0) == 10.0
+
+
+def test_algorithmic_bytes_dense_closed_form():
+    # a fully dense 512 x 64 matrix at tile 256 x 16 with every column active:
+    # R = 2 stripes, K = 64 columns, each (stripe, column) moves 4 + 32 + 512 bytes,
+    # 2 x 4 = 8 GTiles touched, plus x (2 * 64 B) and y (2 * 512 B) for one token
+    w = np.ones((512, 64), dtype=np.float16)
+    f = oracle.encode(w, 256, 16)
+    x = np.ones((1, 64), dtype=np.float16)
+    expect = 2 * 64 * (4 + 32 + 512) + 4 * 8 + 2 * 64 + 2 * 512
+    assert oracle.algorithmic_bytes(f, x, -1.0) == expect
+    # only column 5 active: 2 stripes x (4 + 32 + 512) + 2 GTiles x 4 + x + y
+    x2 = np.zeros((1, 64), dtype=np.float16)
+    x2[0, 5] = 1
+    assert oracle.algorithmic_bytes(f, x2, 0.5) == 2 * (4 + 32 + 512) + 8 + 2 * 64 + 2 * 512
+
+
+def test_algorithmic_bytes_hand_case():
+    case = _hand_cases()[1]
+    f = oracle.encode(_hand_matrix(case), case["tile_m"], case["tile_k"])
+    x = np.array([[1.0, 4.0, -2.0]], dtype=np.float16)
+    # 2 stripes x 3 real columns x (4 + 8) metadata + padded values:
+    # stripe 0: cols 0,1,2 each 8 values; stripe 1: col 0 -> 8, col 1 -> 0, col 2 -> 8
+    vals = 2 * (8 + 8 + 8 + 8 + 0 + 8)
+    expect = 6 * (4 + 8) + vals + 4 * 4 + 2 * 3 + 2 * 70
+    assert oracle.algorithmic_bytes(f, x, -1.0) == expect
+
+
+def test_useful_flops_counts_products():
+    w = oracle.magnitude_prune(synth.weights(20, 10, 2), 0.5)
+    x = synth.laplace_activations(2, 10, 3)
+    t = oracle.threshold_for(x, 0.5)
+    cnt = 0
+    wb, act = w.view(np.uint16), oracle.active_mask(x, t)
+    for b in range(2):
+        for k in range(10):
+            for m in range(20):
+                if act[b, k] and (wb[m, k] & 0x7FFF):
+                    cnt += 1
+    assert oracle.useful_flops(w, x, t) == 2 * cnt
