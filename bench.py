@@ -1,0 +1,331 @@
+"""Benchmark of the decode-time Tiled-CBC spMspV on one MI355X.
+
+Default workload: the four Llama-7B attention projections (q, k, v, o; each
+4096 x 4096 fp16) swept over weight sparsity {50, 60, 70}% and activation
+sparsity {0, 25, 50}% at batch 1. One "step" is the whole sweep: 36 spMspV
+calls (3 x 3 points x 4 projections), each on its own encoded copy; copies
+rotate between steps so that every call streams from HBM rather than from
+the 256 MB Infinity Cache.
+
+Prints one JSON line. ``value`` is the whole step's algorithmic bytes over its
+time (GB/s). Algorithmic bytes per call = for every row stripe and every
+column active for some token: ColInfo (4 B) + bitmap (tile_m/8 B) + padded
+values (2 B x pad8(nnz)); + 4 B per touched GTile (TileOffset); + x and y.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import platform
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama7b-attn")
+    ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
+    ap.add_argument("--rotation-mb", type=float, default=600.0,
+                    help="minimum distinct encoded bytes between two uses of one copy")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--profile-only", action="store_true",
+                    help="run warmup + timed steps only (for rocprofv3 runs)")
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------------------
+# byte model (measurement code: computed from the handle's format arrays)
+
+def call_bytes(fmt: dict, x16: np.ndarray, code: int) -> tuple[int, float]:
+    """Algorithmic bytes of one call and the fraction of columns it reads."""
+    R, C, tk, tm = fmt["n_stripes"], fmt["n_colblocks"], fmt["tile_k"], fmt["tile_m"]
+    K, M = fmt["cols"], fmt["rows"]
+    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
+    act = ((mag > code) & (mag <= 0x7C00)).any(axis=0)            # [K]
+    actp = np.zeros(C * tk, dtype=bool)
+    actp[:K] = act
+    nnz = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64)
+    padded = (nnz + 7) // 8 * 8
+    per_col = 4 + tm // 8 + 2 * padded                           # [R, C*tk]
+    total = int((per_col * actp[None, :]).sum())
+    touched = actp.reshape(C, tk).any(axis=1).sum()
+    total += 4 * int(touched) * R
+    b = x16.shape[0]
+    total += 2 * b * K + 2 * b * M
+    return total, float(act.mean())
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in ("spdp.hip",):
+        with open(os.path.join(ROOT, "paper_2607_21985_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch from committed rocprofv3 counter summaries, if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_spmspv_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m_sha = re.search(r"kernel_sha:\s*(\w+)", text)
+    m_b = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_sha or not m_b or m_sha.group(1) != kernel_source_sha():
+        return None
+    return float(m_b.group(1))
+
+
+# ---------------------------------------------------------------------------
+
+def cpu_baseline(points, budget_s=20.0):
+    """Time the CPU oracle on a bounded sample of the same calls."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        blas = [(i.get("internal_api"), i.get("num_threads")) for i in threadpool_info()
+                if i.get("user_api") == "blas"]
+    except Exception:
+        blas = []
+    cores = max((n for _, n in blas if n), default=len(os.sched_getaffinity(0)))
+    sample = []
+    t_total, b_total = 0.0, 0
+    t_start = time.perf_counter()
+    for pt in points:
+        oracle.spmspv(pt["w"], pt["x"], pt["t"])  # warm-up
+        reps = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            oracle.spmspv(pt["w"], pt["x"], pt["t"])
+            reps.append(time.perf_counter() - t0)
+        t_total += float(np.median(reps))
+        b_total += pt["bytes"]
+        sample.append(pt["label"])
+        if time.perf_counter() - t_start > budget_s:
+            break
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    cpu = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {
+        "value": b_total / t_total / 1e9, "unit": "GB/s", "cores": int(cores), "kind": "oracle",
+        "sample": f"{len(sample)} of the step's calls ({', '.join(sample[:4])}{', ...' if len(sample) > 4 else ''}), "
+                  f"median of 3 after 1 warm-up, float64 NumPy masked product; cpu={cpu}; blas={blas}",
+        "us_per_call": t_total / len(sample) * 1e6,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        sys.exit(2)
+    import torch
+
+    import paper_2607_21985_amd as spdp
+    import synth
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no ROCm GPU visible"}))
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    wl = synth.workload(args.workload)
+    tile = wl["tile"]
+    batch = args.batch if args.batch is not None else wl["batch"][0]
+
+    # ---- inputs: prune (library host C++), calibrate, encode rotated copies
+    t_prep = time.perf_counter()
+    pruned = {}
+    for sw in wl["weight_sparsity"]:
+        for proj in wl["projections"]:
+            pruned[(sw, proj.name)] = spdp.prune_magnitude(proj.weight(), sw)
+    xs = {proj.name: proj.activations(batch) for proj in wl["projections"]}
+    points = []
+    for sw in wl["weight_sparsity"]:
+        for p in wl["act_sparsity"]:
+            for proj in wl["projections"]:
+                x = xs[proj.name]
+                t = spdp.calibrate_threshold(x, p)
+                points.append({"sw": sw, "p": p, "proj": proj, "x": x, "t": t,
+                               "w": pruned[(sw, proj.name)],
+                               "label": f"{proj.name}@sw{sw:g}/p{p:g}"})
+    t_enc = time.perf_counter()
+    copy0 = [spdp.encode(pt["w"], tile) for pt in points]
+    enc_s = (time.perf_counter() - t_enc) / len(points)
+    dev_bytes = sum(len(m.format()["values"]) * 2 for m in copy0)
+    n_copies = max(2, int(np.ceil(args.rotation_mb * 1e6 / max(dev_bytes, 1))) + 1)
+    copies = [copy0] + [[spdp.encode(pt["w"], tile) for pt in points] for _ in range(n_copies - 1)]
+    for pt, m in zip(points, copy0):
+        f = m.format()
+        pt["bytes"], pt["active_frac"] = call_bytes(f, pt["x"], spdp.threshold_code(pt["t"]))
+        pt["rows"], pt["cols"] = f["rows"], f["cols"]
+        del f
+    X = [[torch.from_numpy(pt["x"].view(np.int16)).view(torch.float16).to(dev) for pt in points]
+         for _ in range(n_copies)]
+    Y = [[torch.empty((batch, pt["rows"]), dtype=torch.float16, device=dev) for pt in points]
+         for _ in range(n_copies)]
+    for cp in copies:
+        for m in cp:
+            m.reserve(batch)
+    prep_s = time.perf_counter() - t_prep
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        c = i % n_copies
+        for j, pt in enumerate(points):
+            copies[c][j].spmspv_into(X[c][j], pt["t"], Y[c][j], stream)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize(dev)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(args.warmup + i)
+    ev1.record(stream)
+    torch.cuda.synchronize(dev)
+    total_ms = ev0.elapsed_time(ev1)
+    if args.profile_only:
+        print(json.dumps({"profile_only": True, "ms_per_step": total_ms / args.steps}), flush=True)
+        return
+    ms_per_step = total_ms / args.steps
+    step_bytes = sum(pt["bytes"] for pt in points)
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---- per-launch durations (HIP events around each launch, same stream)
+    per_call = np.zeros(len(points))
+    reps = max(2, min(10, args.steps))
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in points]
+    for i in range(reps):
+        c = (args.warmup + args.steps + i) % n_copies
+        for j, pt in enumerate(points):
+            evs[j][0].record(stream)
+            copies[c][j].spmspv_into(X[c][j], pt["t"], Y[c][j], stream)
+            evs[j][1].record(stream)
+        torch.cuda.synchronize(dev)
+        per_call += np.array([a.elapsed_time(b) for a, b in evs]) / reps
+    kern_ms = float(per_call.sum())
+    achieved = step_bytes / (kern_ms * 1e-3) / 1e9
+
+    # ---- dense fp16 GEMV baseline (torch F.linear), rotated the same way
+    dense = None
+    if not args.no_dense:
+        import torch.nn.functional as F
+        dW = {}
+        names = [proj.name for proj in wl["projections"]]
+        w_bytes = sum(proj.rows * proj.cols * 2 for proj in wl["projections"])
+        n_dc = max(2, int(np.ceil(args.rotation_mb * 1e6 / w_bytes)) + 1)
+        for proj in wl["projections"]:
+            w16 = proj.weight()
+            for c in range(n_dc):
+                dW[(c, proj.name)] = torch.from_numpy(w16.view(np.int16)).view(torch.float16).to(dev)
+        dX = {n: torch.from_numpy(xs[n].view(np.int16)).view(torch.float16).to(dev) for n in names}
+
+        def dstep(i):
+            c = i % n_dc
+            for n in names:
+                F.linear(dX[n], dW[(c, n)])
+
+        for i in range(args.warmup):
+            dstep(i)
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(args.steps):
+            dstep(i)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        d_us = e0.elapsed_time(e1) * 1e3 / (args.steps * len(names))
+        dense = {"us_per_call": d_us,
+                 "gbs": (w_bytes / len(names) + 2 * batch * (wl["projections"][0].rows + wl["projections"][0].cols)) / (d_us * 1e-6) / 1e9}
+        del dW
+
+    # ---- per-point summary
+    pts_out = []
+    n_proj = len(wl["projections"])
+    for k in range(0, len(points), n_proj):
+        grp = points[k:k + n_proj]
+        us = float(per_call[k:k + n_proj].sum() * 1e3 / n_proj)
+        byts = sum(pt["bytes"] for pt in grp)
+        d = {"sw": grp[0]["sw"], "p": grp[0]["p"], "us_per_call": round(us, 3),
+             "gbs": round(byts / (us * n_proj * 1e-6) / 1e9, 1),
+             "active_frac": round(float(np.mean([pt["active_frac"] for pt in grp])), 4),
+             "bytes_per_call": int(byts / n_proj)}
+        if dense:
+            d["speedup_vs_dense"] = round(dense["us_per_call"] / us, 3)
+        pts_out.append(d)
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(points)
+
+    traffic = read_traffic(args.workload)
+    us_per_call = ms_per_step * 1e3 / len(points)
+    out = {
+        "metric": "spMspV us/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic (seeded N(0,0.02) x per-column log-normal weights, Laplace+outlier activations)",
+        "config": {
+            "workload": args.workload,
+            "shapes": sorted({f"{pt['rows']}x{pt['cols']}" for pt in points}),
+            "projections": [proj.name for proj in wl["projections"]],
+            "weight_sparsity": wl["weight_sparsity"], "act_sparsity": wl["act_sparsity"],
+            "batch": batch, "tile": list(tile), "calls_per_step": len(points),
+            "rotation_copies": n_copies, "accumulate": "f32",
+        },
+        "us_per_call": round(us_per_call, 3),
+        "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "roofline": {
+            "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": traffic,
+            "kernel": "spmspv_kernel",
+            "kernel_us_per_launch": round(kern_ms * 1e3 / len(points), 3),
+            "algorithmic_bytes_per_launch": int(step_bytes / len(points)),
+        },
+        "cpu_baseline": cpu,
+        "dense_gemv": dense,
+        "speedup_vs_dense": round(dense["us_per_call"] / (kern_ms * 1e3 / len(points)), 3) if dense else None,
+        "points": pts_out,
+        "prep_s": round(prep_s, 2),
+        "encode_s_per_matrix": round(enc_s, 4),
+        "host": platform.node(),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,177 @@
+/*
+ * spdp.h -- C ABI of the MI355X (gfx950) Tiled-CBC spMspV library.
+ *
+ * The library implements the decode-time hot path of SPDP ("Unified
+ * Static-Dynamic Pruning for Efficient LLM Inference"): an fp16 weight matrix
+ * that has been statically pruned (unstructured) is stored in the Tiled-CBC
+ * format (Sec. 4.1), and each decode call multiplies it by activations whose
+ * small-magnitude entries are dropped at run time (dynamic pruning, Sec. 2.2),
+ * fetching only the active columns' metadata and values (Sec. 4.2).
+ *
+ * Conventions for every entry point:
+ *   - Matrices are row-major. W is rows x cols = out-features x in-features,
+ *     so y = W x with x of length cols.
+ *   - fp16 data travels as raw IEEE binary16 bit patterns (uint16_t).
+ *   - Every function returns an spdp_status; on error nothing is launched,
+ *     output handles are left NULL and spdp_last_error() holds a message for
+ *     the calling thread. No C++ exception crosses this ABI.
+ *   - Host pointers are read during the call only and never retained.
+ */
+#ifndef SPDP_H
+#define SPDP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum spdp_status {
+  SPDP_OK = 0,
+  SPDP_ERR_INVALID_ARG = -1, /* a null pointer, a bad size, NaN, ... */
+  SPDP_ERR_UNSUPPORTED = -2, /* valid input this build does not handle */
+  SPDP_ERR_OOM = -3,         /* host or device allocation failed */
+  SPDP_ERR_HIP = -4          /* a HIP runtime call failed (text in spdp_last_error) */
+} spdp_status;
+
+/* Opaque handle to one encoded matrix (host arrays + optional device copy). */
+typedef struct spdp_matrix* spdp_handle_t;
+
+/*
+ * spdp_encode -- Tiled-CBC encode of W (Sec. 4.1) and upload to the current
+ * HIP device.
+ *
+ *   W        host, rows*cols fp16 bit patterns, row-major, already pruned:
+ *            the library stores whatever zeros it is given. An element is
+ *            treated as zero iff its magnitude bits are zero (-0 is zero).
+ *   rows     M >= 1; cols: K >= 1. Ragged sizes are zero-padded to whole
+ *            tiles inside the format.
+ *   tile_m   rows of a GTile, a multiple of 64 in [64, 256] (the paper uses
+ *            256); each column tile carries tile_m/64 uint64 bitmap words.
+ *   tile_k   columns of a GTile, a power of two in [1, 256] (the paper uses 16).
+ *   out      receives the handle.
+ *
+ * Layout produced (byte-exact, inspect with spdp_format):
+ *   GTile g = r*C + c for row stripe r < R = ceil(M/tile_m) and column block
+ *   c < C = ceil(K/tile_k) (row-major GTile order).
+ *   tile_offset[g]  uint32, start of GTile g in values (fp16 elements);
+ *                   NGT+1 entries, the last one = number of values.
+ *   col_info[g*tile_k+j] uint32 = (offset << 16) | nnz: offset in fp16
+ *                   elements from tile_offset[g] (includes earlier columns'
+ *                   padding), nnz = nonzeros of column j of the GTile.
+ *   bitmap[(g*tile_k+j)*(tile_m/64) + w] uint64: bit i <-> row 64w+i of the
+ *                   stripe; 1 iff that element is nonzero.
+ *   values          nonzeros GTile by GTile, column by column, rows ascending,
+ *                   each column padded with +0 to a multiple of 8 elements
+ *                   (16 bytes, Sec. 4.2.3).
+ *
+ * Device memory for the four arrays plus a small split-K workspace is
+ * allocated on the current device and owned by the handle. Returns
+ * SPDP_ERR_UNSUPPORTED if the format would hold 2^32 or more values.
+ */
+int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
+                int32_t tile_k, spdp_handle_t* out);
+
+/*
+ * spdp_encode_host -- the same encoding without any device work: the handle
+ * holds host arrays only (usable on machines without a GPU, e.g. to inspect
+ * the format). spdp_spmspv on such a handle returns SPDP_ERR_INVALID_ARG.
+ */
+int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
+                     int32_t tile_m, int32_t tile_k, spdp_handle_t* out);
+
+/*
+ * spdp_spmspv -- Y = W_sp . mask(X) for a batch of decode tokens (Sec. 4.2).
+ *
+ *   h          handle from spdp_encode (device copy on the current device).
+ *   X          device, batch x cols fp16, row-major, 16-byte aligned.
+ *   batch      number of tokens, 1 <= batch <= 32.
+ *   threshold  dynamic-pruning threshold (Sec. 5.1 per-layer ECDF quantile):
+ *              column k takes part for token b iff |X[b,k]| > threshold
+ *              (strict). A negative threshold keeps every column; NaN is
+ *              SPDP_ERR_INVALID_ARG. NaN activations are never active.
+ *              Columns inactive for every token of the batch are not read.
+ *   Y          device, batch x rows fp16, row-major, fully overwritten with
+ *              the fp32-accumulated result rounded once to nearest even.
+ *              Must not overlap X.
+ *   stream     hipStream_t to enqueue on (NULL = the null stream).
+ *
+ * Asynchronous: the call validates, enqueues one kernel and returns; X and Y
+ * must stay valid until the stream passes the work. The handle's workspace
+ * is reused by every call, so one handle must not run on two streams at
+ * once. The first call with a larger batch than before grows the workspace
+ * (a device allocation); spdp_reserve does that ahead of time.
+ */
+int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
+                float threshold, uint16_t* Y, void* stream);
+
+/* spdp_reserve -- size the handle's workspace for batches up to max_batch. */
+int spdp_reserve(spdp_handle_t h, int32_t max_batch);
+
+/*
+ * spdp_free -- release a handle. Waits for the device to finish work that
+ * may still use it. spdp_free(NULL) does nothing. Using h afterwards is
+ * undefined.
+ */
+void spdp_free(spdp_handle_t h);
+
+/* Read-only view of an encoded matrix. Host arrays are owned by the handle
+ * and live until spdp_free; device pointers are NULL for host-only handles. */
+typedef struct spdp_format {
+  int64_t rows, cols;
+  int32_t tile_m, tile_k;
+  int64_t n_stripes;   /* R */
+  int64_t n_colblocks; /* C */
+  int64_t n_gtiles;    /* R*C */
+  int64_t n_values;    /* length of values (= tile_offset[n_gtiles]) */
+  const uint32_t* tile_offset; /* host, n_gtiles + 1 */
+  const uint32_t* col_info;    /* host, n_gtiles * tile_k */
+  const uint64_t* bitmap;      /* host, n_gtiles * tile_k * tile_m / 64 */
+  const uint16_t* values;      /* host, n_values */
+  const void* d_tile_offset;   /* device copies (or NULL) */
+  const void* d_col_info;
+  const void* d_bitmap;
+  const void* d_values;
+  int32_t device; /* HIP device ordinal of the copies, -1 if host-only */
+} spdp_format_t;
+
+int spdp_format(spdp_handle_t h, spdp_format_t* out);
+
+/*
+ * Offline preparation helpers (host only, no device work).
+ *
+ * spdp_prune_magnitude -- global unstructured magnitude pruning (Sec. 2.2,
+ * static pruning by magnitude): out = W with the floor(sparsity*n) entries of
+ * smallest |W| set to +0. Ties in magnitude go by index, lowest first. W and
+ * out may alias. NaN entries are SPDP_ERR_INVALID_ARG; sparsity in [0, 1].
+ */
+int spdp_prune_magnitude(const uint16_t* W, int64_t n, double sparsity,
+                         uint16_t* out);
+
+/*
+ * spdp_calibrate_threshold -- TEAL-style threshold (Sec. 5.1: a quantile of
+ * the empirical distribution of |x| over calibration activations): *t is
+ * the ceil(p*n)-th smallest |X| over all n entries, so the strict rule
+ * |x| > t drops at least that many; p == 0 (or n == 0) gives -1, which keeps
+ * everything. NaN entries are SPDP_ERR_INVALID_ARG; p in [0, 1].
+ */
+int spdp_calibrate_threshold(const uint16_t* X, int64_t n, double p, float* t);
+
+/*
+ * spdp_threshold_code -- the integer form of a threshold that the kernels
+ * use: for finite-or-infinite, non-NaN fp16 x, |x| > threshold holds iff
+ * code < (x & 0x7FFF) <= 0x7C00. code = -1 for a negative threshold, else the
+ * bit pattern of the largest fp16 magnitude not above the threshold.
+ */
+int spdp_threshold_code(float threshold, int32_t* code);
+
+/* Static text for a status code, and the calling thread's last error detail. */
+const char* spdp_strerror(int status);
+const char* spdp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPDP_H */

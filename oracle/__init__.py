@@ -93,8 +93,12 @@ def magnitude_prune(w: np.ndarray, sparsity: float) -> np.ndarray:
 
     The ``n = floor(sparsity * W.size)`` entries of smallest magnitude are set
     to +0 (bits 0x0000); all other entries keep their bits. Ties in magnitude
-    are broken by row-major linear index, ascending (a stable sort), so the
-    result is unique. NaN entries are rejected (their magnitude has no order).
+    are broken by row-major linear index, lowest first, so the result is
+    unique. NaN entries are rejected (their magnitude has no order).
+
+    Steps: the n-th smallest magnitude is the cut; every entry below the cut
+    is pruned, and the entries equal to the cut are pruned in index order
+    until n entries are pruned in total.
     """
     if not 0.0 <= sparsity <= 1.0:
         raise ValueError("sparsity must lie in [0, 1]")
@@ -103,10 +107,16 @@ def magnitude_prune(w: np.ndarray, sparsity: float) -> np.ndarray:
         raise ValueError("NaN weights cannot be magnitude-pruned")
     flat = w.reshape(-1)
     n = int(math.floor(sparsity * flat.size))
-    mag = np.abs(flat.astype(np.float64))
-    order = np.argsort(mag, kind="stable")
     out = flat.copy()
-    out[order[:n]] = np.float16(0.0)  # +0
+    if n == 0:
+        return out.reshape(w.shape)
+    mag = np.abs(flat.astype(np.float64))
+    cut = np.partition(mag, n - 1)[n - 1]
+    below = mag < cut
+    quota = n - int(below.sum())
+    tied = np.flatnonzero(mag == cut)[:quota]
+    out[below] = np.float16(0.0)  # +0
+    out[tied] = np.float16(0.0)
     return out.reshape(w.shape)
 
 

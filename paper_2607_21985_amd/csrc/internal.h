@@ -1,0 +1,45 @@
+// Internal declarations shared by the host-side C++ (host.cpp) and the HIP
+// side (spdp.hip) of libspdp. Not part of the public ABI (include/spdp.h).
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "spdp.h"
+
+// One encoded matrix: the Tiled-CBC arrays on the host, their device copies,
+// and the split-K workspace of the spMspV kernel.
+struct spdp_matrix {
+  int64_t rows = 0, cols = 0;
+  int32_t tile_m = 0, tile_k = 0;
+  int64_t n_stripes = 0, n_colblocks = 0, n_gtiles = 0;
+  std::vector<uint32_t> tile_offset;
+  std::vector<uint32_t> col_info;
+  std::vector<uint64_t> bitmap;
+  std::vector<uint16_t> values;
+
+  int device = -1;  // -1: host-only handle
+  void* d_tile_offset = nullptr;
+  void* d_col_info = nullptr;
+  void* d_bitmap = nullptr;
+  void* d_values = nullptr;
+
+  // Split-K workspace: fp32 partial sums [segments][batch][n_stripes*tile_m]
+  // and one arrival counter per row stripe (zero between calls).
+  float* d_partials = nullptr;
+  size_t partial_floats = 0;
+  uint32_t* d_counters = nullptr;
+};
+
+namespace spdp {
+
+// Records the detail text for the calling thread and returns `status`.
+int fail(int status, const std::string& detail);
+void clear_error();
+
+// Validates shape/tile arguments and fills the host arrays of `m`.
+int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
+                       int32_t tile_m, int32_t tile_k, spdp_matrix* m);
+
+}  // namespace spdp

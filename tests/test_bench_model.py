@@ -1,0 +1,24 @@
+"""bench.py's byte model agrees with the oracle's (CPU only)."""
+
+import numpy as np
+import pytest
+
+import bench
+import oracle
+import paper_2607_21985_amd as spdp
+import synth
+
+
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch", [
+    (1024, 1024, (64, 64), 0.5, 0.5, 1), (700, 900, (256, 16), 0.6, 0.25, 1),
+    (300, 1000, (128, 8), 0.5, 0.0, 3), (333, 517, (192, 4), 0.7, 0.5, 8),
+])
+def test_call_bytes_matches_oracle(rows, cols, tile, sw, p, batch):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows + cols), sw)
+    x = synth.laplace_activations(batch, cols, 5)
+    t = float(oracle.threshold_for(x, p))
+    f = spdp.encode_host(w, tile).format()
+    got, frac = bench.call_bytes(f, x, spdp.threshold_code(t))
+    ref = oracle.encode(w, *tile)
+    assert got == oracle.algorithmic_bytes(ref, x, t)
+    assert frac == pytest.approx(oracle.active_mask(x, t).any(axis=0).mean())

@@ -1,0 +1,290 @@
+"""GPU parity: the HIP spMspV path (through the C ABI) against the CPU oracle.
+
+Every case builds its inputs from ``synth`` (seeded), runs the oracle's own
+pipeline (oracle.magnitude_prune -> oracle.threshold_for -> oracle.spmspv) on
+the CPU and the library's pipeline (spdp.encode -> spdp_spmspv on the GPU),
+and compares element by element:
+
+    |Y_gpu - y64| <= 2e-3 * S + 1e-5,   S = sum_k |W_sp[m,k]| |xm[b,k]|,
+
+with Y finite, and exactly 0 where no active term exists (S == 0). Small cases
+are checked in full; full-size shapes (in the same launch configuration as
+bench.py) are checked on sampled rows plus whole-output properties.
+"""
+
+import ctypes
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from conftest import GOLDEN
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2607_21985_amd as spdp  # noqa: E402
+
+RTOL, ATOL = 2e-3, 1e-5
+
+
+def _dev():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm GPU (torch.cuda.is_available() is False)")
+    return torch.device("cuda:0")
+
+
+def _to_dev(x16: np.ndarray):
+    t = torch.from_numpy(np.ascontiguousarray(x16).view(np.int16)).view(torch.float16)
+    return t.to(_dev())
+
+
+def _run_gpu(m, x16, t, y_init=None):
+    X = _to_dev(x16)
+    if y_init is None:
+        Y = torch.full((x16.shape[0], m.rows), float("nan"), dtype=torch.float16, device=X.device)
+    else:
+        Y = y_init
+    m.spmspv_into(X, t, Y)
+    torch.cuda.synchronize()
+    return Y.cpu().numpy().astype(np.float64)
+
+
+def _assert_close(y, y64, s64, label=""):
+    assert np.all(np.isfinite(y)), f"{label}: non-finite output"
+    err = np.abs(y - y64)
+    bound = RTOL * s64 + ATOL
+    bad = err > bound
+    if bad.any():
+        b, m = np.argwhere(bad)[0]
+        raise AssertionError(f"{label}: {bad.sum()} elements out of tolerance; first at "
+                             f"(b={b}, m={m}): gpu={y[b, m]} ref={y64[b, m]} S={s64[b, m]}")
+    zero = s64 == 0
+    assert np.all(y[zero] == 0), f"{label}: rows with no active term are not exactly 0"
+
+
+def _case(rows, cols, tile, sw, p, batch, wseed, xseed, xkind="laplace"):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, wseed), sw)
+    x = (synth.laplace_activations if xkind == "laplace" else synth.swiglu_activations)(batch, cols, xseed)
+    t = float(oracle.threshold_for(x, p))
+    return w, x, t
+
+
+def _check_full(w, x, t, tile, label):
+    print(f"[gpu] {label}", flush=True)
+    m = spdp.encode(w, tile)
+    y = _run_gpu(m, x, t)
+    y64, s64, _ = oracle.spmspv(w, x, t)
+    _assert_close(y, y64, s64, label)
+    m.close()
+    return y
+
+
+# ---------------------------------------------------------------------------
+
+def _hand_cases():
+    with open(os.path.join(GOLDEN, "tiled_cbc_hand.json")) as fh:
+        return json.load(fh)["cases"]
+
+
+@pytest.mark.parametrize("case", _hand_cases(), ids=lambda c: c["name"])
+def test_hand_worked_cases_exact(case):
+    w = np.zeros((case["rows"], case["cols"]), dtype=np.uint16)
+    for mm, k, h in case["nonzeros"]:
+        w[mm, k] = int(h, 16)
+    w = w.view(np.float16)
+    m = spdp.encode(w, (case["tile_m"], case["tile_k"]))
+    for prod in case["products"]:
+        x = np.array([prod["x"]], dtype=np.float16)
+        y = _run_gpu(m, x, prod["t"])
+        expect = np.zeros(case["rows"])
+        for mm, v in prod["y_nonzero"]:
+            expect[mm] = v
+        assert np.array_equal(y[0], expect)
+    m.close()
+
+
+SMALL = [
+    # rows, cols, tile, sw, p, batch
+    (64, 64, (64, 64), 0.5, 0.5, 1),
+    (1024, 1024, (64, 64), 0.5, 0.5, 1),      # the 1024x1024 single-layer workload
+    (1, 1, (64, 1), 0.0, 0.0, 1),
+    (70, 3, (64, 2), 0.3, 0.0, 1),
+    (333, 517, (256, 16), 0.5, 0.5, 1),
+    (513, 1000, (256, 16), 0.6, 0.25, 2),
+    (256, 4096, (256, 16), 0.7, 0.5, 3),
+    (700, 900, (128, 8), 0.5, 0.3, 4),
+    (450, 640, (192, 32), 0.4, 0.5, 5),
+    (300, 2048, (64, 1), 0.5, 0.5, 8),
+    (1000, 1536, (256, 256), 0.5, 0.6, 13),
+    (257, 777, (256, 4), 0.8, 0.2, 16),
+    (129, 300, (128, 64), 0.5, 0.5, 17),
+    (512, 1111, (256, 16), 0.6, 0.4, 32),
+    (96, 5000, (64, 16), 0.9, 0.7, 7),
+]
+
+
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch", SMALL)
+def test_small_against_oracle(rows, cols, tile, sw, p, batch):
+    w, x, t = _case(rows, cols, tile, sw, p, batch, rows * 7 + cols, cols * 3 + batch)
+    _check_full(w, x, t, tile, f"small {rows}x{cols} tile={tile} sw={sw} p={p} B={batch}")
+
+
+def test_dense_no_threshold_is_gemv():
+    w, x, _ = _case(300, 700, (256, 16), 0.0, 0.0, 2, 5, 6)
+    _check_full(w, x, -1.0, (256, 16), "dense")
+
+
+def test_everything_inactive_gives_exact_zero():
+    w, x, _ = _case(300, 700, (256, 16), 0.5, 0.0, 3, 7, 8)
+    t = float(np.abs(x.astype(np.float64)).max())
+    y = _check_full(w, x, t, (256, 16), "all inactive")
+    assert np.all(y == 0)
+
+
+def test_all_zero_weights():
+    w = np.zeros((200, 300), dtype=np.float16)
+    x = synth.laplace_activations(2, 300, 1)
+    y = _check_full(w, x, -1.0, (128, 16), "zero W")
+    assert np.all(y == 0)
+
+
+def test_single_active_column():
+    w, _, _ = _case(500, 333, (256, 16), 0.5, 0.0, 1, 11, 12)
+    x = np.full((1, 333), 0.25, dtype=np.float16)
+    x[0, 200] = np.float16(-3.0)
+    y = _check_full(w, x, 1.0, (256, 16), "one column")
+    assert np.array_equal(y[0], (np.float16(-3.0) * w[:, 200].astype(np.float64)).astype(np.float16).astype(np.float64))
+
+
+def test_nan_activations_are_never_active():
+    w, x, t = _case(256, 512, (256, 16), 0.5, 0.5, 2, 13, 14)
+    x = x.copy()
+    x[0, ::5] = np.float16(np.nan)
+    _check_full(w, x, t, (256, 16), "NaN in x")
+
+
+def test_negative_zero_threshold_and_ties():
+    w, _, _ = _case(256, 256, (256, 16), 0.5, 0.0, 1, 15, 16)
+    x = np.tile(np.array([1.0, -1.0, 0.5, 0.0, -0.0, 2.0, -2.0, 1.0], dtype=np.float16), (2, 32))
+    for t in (1.0, 0.5, 0.0, -0.0, -1.0, 1.9999, 2.0):
+        _check_full(w, x, t, (256, 16), f"ties t={t}")
+
+
+def test_output_fully_overwritten_and_repeatable():
+    w, x, t = _case(600, 1500, (256, 16), 0.5, 0.5, 4, 17, 18)
+    m = spdp.encode(w, (256, 16))
+    y1 = _run_gpu(m, x, t)
+    y2 = _run_gpu(m, x, t)  # second call: split-K counters were re-armed by the first
+    assert np.array_equal(y1, y2), "two identical calls differ"
+    y64, s64, _ = oracle.spmspv(w, x, t)
+    _assert_close(y1, y64, s64, "repeat")
+    # growing then shrinking the batch reuses / grows the workspace
+    for b in (1, 9, 32, 2):
+        xb = synth.laplace_activations(b, 1500, 100 + b)
+        tb = float(oracle.threshold_for(xb, 0.5))
+        yb = _run_gpu(m, xb, tb)
+        y64, s64, _ = oracle.spmspv(w, xb, tb)
+        _assert_close(yb, y64, s64, f"batch {b}")
+    m.close()
+
+
+@pytest.mark.parametrize("splitk", ["1", "2", "3", "7", "64", "1000"])
+def test_split_k_settings(splitk, monkeypatch):
+    monkeypatch.setenv("SPDP_SPLITK", splitk)
+    w, x, t = _case(777, 3000, (256, 16), 0.5, 0.5, 3, 19, 20)
+    _check_full(w, x, t, (256, 16), f"splitk={splitk}")
+
+
+def test_streams_and_interleaved_handles():
+    dev = _dev()
+    cases = [_case(400 + 64 * i, 900 + 100 * i, (256, 16), 0.5, 0.5, 1 + i, 30 + i, 40 + i) for i in range(3)]
+    mats = [spdp.encode(w, (256, 16)) for w, _, _ in cases]
+    s = torch.cuda.Stream(device=dev)
+    outs = []
+    with torch.cuda.stream(s):
+        for (w, x, t), m in zip(cases, mats):
+            X = _to_dev(x)
+            Y = torch.empty((x.shape[0], m.rows), dtype=torch.float16, device=dev)
+            m.spmspv_into(X, t, Y, stream=s)
+            outs.append(Y)
+    s.synchronize()
+    for (w, x, t), Y in zip(cases, outs):
+        y64, s64, _ = oracle.spmspv(w, x, t)
+        _assert_close(Y.cpu().numpy().astype(np.float64), y64, s64, "stream")
+    for m in mats:
+        m.close()
+
+
+def test_device_copy_matches_host_format():
+    w, _, _ = _case(700, 900, (256, 16), 0.6, 0.0, 1, 21, 22)
+    m = spdp.encode(w, (256, 16))
+    f = m.format()
+    ref = oracle.encode(w, 256, 16)
+    for name in ("tile_offset", "col_info", "bitmap", "values"):
+        assert np.array_equal(f[name], getattr(ref, name)), name
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+    torch.cuda.synchronize()
+    for name, ptr in m.device_pointers().items():
+        host = np.empty_like(f[name])
+        assert hip.hipMemcpy(host.ctypes.data, ptr, host.nbytes, 2) == 0
+        assert np.array_equal(host, f[name]), name
+    m.close()
+
+
+def test_argument_errors_on_device():
+    w, x, t = _case(128, 256, (128, 16), 0.5, 0.5, 2, 23, 24)
+    m = spdp.encode(w, (128, 16))
+    X = _to_dev(x)
+    Y = torch.empty((2, 128), dtype=torch.float16, device=X.device)
+    with pytest.raises(spdp.SpdpError):
+        m.spmspv_into(X, float("nan"), Y)
+    L = spdp.lib()
+    for b in (0, 33, -1):
+        assert L.spdp_spmspv(m._h, ctypes.c_void_p(X.data_ptr()), b, ctypes.c_float(0.1),
+                             ctypes.c_void_p(Y.data_ptr()), None) == -1
+    # misaligned and overlapping buffers
+    assert L.spdp_spmspv(m._h, ctypes.c_void_p(X.data_ptr() + 2), 1, ctypes.c_float(0.1),
+                         ctypes.c_void_p(Y.data_ptr()), None) == -1
+    assert L.spdp_spmspv(m._h, ctypes.c_void_p(X.data_ptr()), 1, ctypes.c_float(0.1),
+                         ctypes.c_void_p(X.data_ptr()), None) == -1
+    m.close()
+
+
+# ---------------------------------------------------------------------------
+# Full-size workloads, same launch configuration as bench.py, sampled rows.
+
+def _check_sampled(w, x, t, tile, label, n_rows=192, seed=0):
+    print(f"[gpu] {label}", flush=True)
+    m = spdp.encode(w, tile)
+    y = _run_gpu(m, x, t)
+    m.close()
+    assert np.all(np.isfinite(y)), label
+    rng = np.random.default_rng(seed)
+    rows = np.unique(np.concatenate([[0, w.shape[0] - 1], rng.choice(w.shape[0], n_rows, replace=False)]))
+    y64, s64 = oracle.spmspv_rows(w, x, t, rows)
+    _assert_close(y[:, rows], y64, s64, label)
+
+
+FULL = []
+for name in ("llama7b-attn", "llama7b-mlp", "llama13b-layer", "llama70b-layer"):
+    wl = synth.workload(name)
+    for proj in wl["projections"]:
+        FULL.append((name, proj))
+
+
+@pytest.mark.parametrize("name,proj", FULL, ids=[f"{n}-{p.name}" for n, p in FULL])
+def test_full_size_sampled(name, proj):
+    wl = synth.workload(name)
+    sw = max(wl["weight_sparsity"])
+    p = max(wl["act_sparsity"])
+    batch = max(wl["batch"]) if name != "llama70b-layer" else 32
+    w = oracle.magnitude_prune(proj.weight(), sw)
+    for b in sorted({1, batch}):
+        x = proj.activations(b)
+        t = float(oracle.threshold_for(x, p))
+        _check_sampled(w, x, t, wl["tile"], f"{name}/{proj.name} {proj.rows}x{proj.cols} sw={sw} p={p} B={b}")

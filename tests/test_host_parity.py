@@ -1,0 +1,99 @@
+"""Bit-exact parity of the library's host C++ (Tiled-CBC encoder, magnitude
+pruning, threshold calibration, threshold code) against the CPU oracle, on
+the same seeded inputs. No GPU involved."""
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2607_21985_amd as spdp
+import synth
+
+
+def _same_format(lib_fmt, ref):
+    for name in ("tile_offset", "col_info", "bitmap", "values"):
+        a, b = lib_fmt[name], getattr(ref, name)
+        assert a.dtype == b.dtype and a.shape == b.shape, name
+        assert np.array_equal(a, b), name
+
+
+@pytest.mark.parametrize("rows,cols,tm,tk,sw,seed", [
+    (1, 1, 64, 1, 0.0, 1), (64, 16, 64, 16, 0.5, 2), (130, 37, 64, 4, 0.6, 3),
+    (200, 33, 128, 8, 0.3, 4), (256, 40, 256, 16, 0.7, 5), (70, 9, 192, 2, 0.9, 6),
+    (65, 65, 64, 64, 0.5, 7), (300, 70, 256, 256, 0.2, 8), (513, 1000, 256, 16, 0.5, 9),
+    (1024, 1024, 64, 64, 0.5, 101), (777, 300, 128, 1, 0.95, 10), (257, 129, 256, 128, 1.0, 11),
+])
+def test_encoder_bit_exact_small(rows, cols, tm, tk, sw, seed):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, seed), sw)
+    _same_format(spdp.encode_host(w, (tm, tk)).format(), oracle.encode(w, tm, tk))
+
+
+def test_encoder_keeps_signed_zero_and_subnormals_exact():
+    w = synth.weights(256, 64, 77)
+    wb = w.view(np.uint16).copy()
+    wb[::7, ::3] = 0x8000          # -0: not stored
+    wb[1::11, 1::5] = 0x0001       # smallest subnormal: stored
+    wb[2::13, 2::7] = 0x83FF       # largest negative subnormal: stored
+    w2 = wb.view(np.float16)
+    _same_format(spdp.encode_host(w2, (256, 16)).format(), oracle.encode(w2, 256, 16))
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("rows,cols,sw,seed", [(4096, 4096, 0.5, 201), (11008, 4096, 0.6, 301),
+                                               (4096, 11008, 0.6, 303)])
+def test_encoder_bit_exact_full_size(rows, cols, sw, seed):
+    w = spdp.prune_magnitude(synth.weights(rows, cols, seed), sw)
+    _same_format(spdp.encode_host(w, (256, 16)).format(), oracle.encode(w, 256, 16))
+
+
+@pytest.mark.parametrize("shape,sw,seed", [((8, 8), 0.5, 1), ((13, 7), 0.3, 2), ((300, 70), 0.6, 3),
+                                           ((64, 64), 0.0, 4), ((9, 9), 1.0, 5), ((1000, 333), 0.77, 6)])
+def test_prune_bit_exact(shape, sw, seed):
+    w = synth.weights(*shape, seed)
+    assert np.array_equal(spdp.prune_magnitude(w, sw).view(np.uint16),
+                          oracle.magnitude_prune(w, sw).view(np.uint16))
+
+
+def test_prune_ties_cross_chunks():
+    # many equal magnitudes of both signs, far more than one worker chunk
+    rng = np.random.default_rng(5)
+    vals = np.array([0.5, -0.5, 0.25, -0.25, 1.0, 0.0, -0.0], dtype=np.float16)
+    w = vals[rng.integers(0, vals.size, size=(3000, 3000))]
+    for sw in (0.1, 0.37, 0.5, 0.93):
+        assert np.array_equal(spdp.prune_magnitude(w, sw).view(np.uint16),
+                              oracle.magnitude_prune(w, sw).view(np.uint16))
+
+
+@pytest.mark.slow
+def test_prune_bit_exact_full_size():
+    w = synth.weights(4096, 4096, 201)
+    assert np.array_equal(spdp.prune_magnitude(w, 0.5).view(np.uint16),
+                          oracle.magnitude_prune(w, 0.5).view(np.uint16))
+
+
+@pytest.mark.parametrize("p", [0.0, 0.1, 0.25, 0.5, 0.7, 0.999, 1.0])
+@pytest.mark.parametrize("kind,b,k,seed", [("laplace", 1, 4096, 211), ("laplace", 8, 5120, 411),
+                                           ("swiglu", 4, 11008, 313), ("laplace", 1, 7, 3)])
+def test_calibrate_matches_oracle(p, kind, b, k, seed):
+    x = (synth.laplace_activations if kind == "laplace" else synth.swiglu_activations)(b, k, seed)
+    assert np.float32(spdp.calibrate_threshold(x, p)) == oracle.threshold_for(x, p)
+
+
+def test_calibrate_empty_and_ties():
+    assert spdp.calibrate_threshold(np.zeros(0, dtype=np.float16), 0.5) == -1.0
+    x = np.array([[1.0, -1.0, 1.0, 2.0, 0.0, -0.0, 3.0, 1.0]], dtype=np.float16)
+    assert spdp.calibrate_threshold(x, 0.5) == float(oracle.threshold_for(x, 0.5))
+
+
+def test_threshold_code_decides_like_oracle_for_every_fp16():
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16).reshape(1, -1)
+    mag = (bits & 0x7FFF).astype(np.int64)
+    ts = [-1.0, -0.0, 0.0, 5.96e-8, 6e-8, 1e-7, 6.1e-5, 0.1, 0.5, 0.50006, 1.0, 1.0009765625,
+          3.14159, 1000.0, 65504.0, 65519.0, 65520.0, 1e30, float("inf"), float("-inf")]
+    rng = np.random.default_rng(0)
+    ts += list(rng.uniform(0, 10, 30)) + list(np.float16(rng.uniform(0, 10, 10)).astype(float))
+    for t in ts:
+        code = spdp.threshold_code(t)
+        lib_act = (mag > code) & (mag <= 0x7C00)
+        assert np.array_equal(lib_act, oracle.active_mask(x, t)[0]), t
