@@ -40,28 +40,46 @@ namespace {
 
 constexpr int kWaves = 4;                 // waves per workgroup
 constexpr int kThreads = 64 * kWaves;
-constexpr int kMaxWords = 4;              // tile_m <= 256
-constexpr int kBatchCols = 4;             // active columns staged per wave per round
-constexpr int kSlotBytes = 64 * kMaxWords * 2;  // one column of one stripe, fp16
-constexpr int kStageBytes = kWaves * kBatchCols * kSlotBytes;  // 16 KiB
+constexpr int kMaxWords = 4;              // tile_m <= 256: at most 4 bitmap words per column
+constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one stripe (fp16)
+constexpr int kBatch = 16;                // active columns per pipeline stage of a wave
+constexpr int kMaxWaveCols = 128;         // columns of one wave's K range
+constexpr int kLoadsPerBatch = kBatch / 2 + 1;  // 16-byte-per-lane loads issued per stage
 constexpr int kMaxBatch = 32;
 
 struct KernelArgs {
-  const uint32_t* __restrict__ tile_offset;
-  const uint32_t* __restrict__ col_info;
-  const uint64_t* __restrict__ bitmap;
-  const uint16_t* __restrict__ values;
-  const uint16_t* __restrict__ x;
-  uint16_t* __restrict__ y;
-  float* __restrict__ partials;  // [segments][batch][n_stripes * tile_m]
-  uint32_t* __restrict__ counters;  // [n_stripes]
+  const uint32_t* tile_offset;
+  const uint32_t* col_info;
+  const uint64_t* bitmap;
+  const uint16_t* values;
+  const uint16_t* x;
+  uint16_t* y;
+  float* partials;     // [segments][batch][n_stripes * tile_m]
+  uint32_t* counters;  // [n_stripes], zero between calls
   int rows, cols;
   int tile_m, wpc, tk_log2, n_colblocks, n_stripes;
   int batch;
   int code;       // threshold code: active iff code < (x & 0x7fff) <= 0x7c00
-  int wave_cols;  // columns per wave (multiple of 16)
+  int wave_cols;  // columns per wave (multiple of 16, <= kMaxWaveCols)
   int segments;   // workgroups per row stripe
 };
+
+// LDS use. The two pipeline buffers are separate __shared__ arrays so that
+// the compiler can tell reads of one from LDS-DMA writes into the other (it
+// then waits only for the DMA a read depends on).
+constexpr int kValBufBytes = kWaves * kBatch * kSlotBytes;  // one stage, all waves
+constexpr int kBmBufBytes = kWaves * 32 * 16;              // one stage, all waves
+
+template <int NB>
+struct Smem {
+  static constexpr int kSlice = NB < 8 ? NB : 8;  // tokens per cross-wave reduction pass
+  static constexpr int kRed = kWaves * kSlice * 256 * 4;
+  static_assert(kRed <= kValBufBytes, "reduction reuses the first value buffer");
+};
+
+// s_waitcnt immediate for gfx9: wait until at most n vector-memory operations
+// are outstanding, leaving the LDS/scalar and export counters unconstrained.
+constexpr int vmcnt_imm(int n) { return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8); }
 
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -72,38 +90,31 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return __half2float(__ushort_as_half((unsigned short)h));
 }
 
-struct Words4 {
-  uint64_t w[kMaxWords];
-};
-
-template <int NB>
-struct Smem {
-  static constexpr int kXBytes = kWaves * 64 * NB * 2;   // masked x, fp16 bits
-  static constexpr int kSlice = NB < 8 ? NB : 8;          // tokens per reduction pass
-  static constexpr int kRedBytes = kWaves * kSlice * 256 * 4;
-  static constexpr int kMain = kStageBytes + kXBytes;
-  static constexpr int kBytes = kMain > kRedBytes ? kMain : kRedBytes;
-};
-
-// Read-only metadata is reached through constant-address-space pointers so
-// that uniform (per-column) accesses compile to scalar loads.
-template <class T>
-using const_ptr = const __attribute__((address_space(4))) T*;
-
-template <class T>
-__device__ __forceinline__ const_ptr<T> as_const(const T* p) {
-  return reinterpret_cast<const_ptr<T>>(reinterpret_cast<uintptr_t>(p));
-}
-
+// 16 bytes per lane from global memory straight into LDS: lane i's bytes land
+// at lds_base + 16 * i (gfx950 LDS DMA).
 __device__ __forceinline__ void lds_dma16(const void* src, void* lds_base) {
   __builtin_amdgcn_global_load_lds(src, reinterpret_cast<__attribute__((address_space(3))) void*>(
                                             reinterpret_cast<uintptr_t>(lds_base)),
                                    16, 0, 0);
 }
 
+// Wave-uniform 64-bit value from two VGPR halves (readfirstlane yields int:
+// go through uint32_t so that bit 31 of the low half is not sign-extended).
+__device__ __forceinline__ uint64_t uniform64(uint32_t lo, uint32_t hi) {
+  return (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(lo) |
+         ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(hi) << 32);
+}
+
 template <int NB>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char smem[Smem<NB>::kBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char val0[kValBufBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char val1[kValBufBytes];
+  __shared__ __attribute__((aligned(512))) unsigned char bm0[kBmBufBytes];
+  __shared__ __attribute__((aligned(512))) unsigned char bm1[kBmBufBytes];
+  // one entry per active column, in activity order: {value base, column
+  // index into ColInfo/bitmap, 16-byte chunks of values, unused}
+  __shared__ uint4 ent_s[kWaves][kMaxWaveCols];
+  __shared__ uint16_t xs_s[kWaves][kMaxWaveCols * NB];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
@@ -112,12 +123,14 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int r = blockIdx.y;
   const int tk_mask = (1 << a.tk_log2) - 1;
   const int wpc = a.wpc;
-  const_ptr<uint32_t> col_info = as_const(a.col_info);
-  const_ptr<uint32_t> tile_offset = as_const(a.tile_offset);
-  const_ptr<uint64_t> bitmap = as_const(a.bitmap);
+  const int g_row = r * a.n_colblocks;
 
-  unsigned char* stage = smem + wave * (kBatchCols * kSlotBytes);
-  uint16_t* xs = reinterpret_cast<uint16_t*>(smem + kStageBytes) + wave * 64 * NB;
+  uint4* ent_l = ent_s[wave];
+  uint16_t* xs_l = xs_s[wave];
+  unsigned char* my_val0 = val0 + wave * (kBatch * kSlotBytes);
+  unsigned char* my_val1 = val1 + wave * (kBatch * kSlotBytes);
+  unsigned char* my_bm0 = bm0 + wave * (32 * 16);
+  unsigned char* my_bm1 = bm1 + wave * (32 * 16);
 
   float acc[kMaxWords][NB];
 #pragma unroll
@@ -126,114 +139,160 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
 
   const int k_begin = (seg * kWaves + wave) * a.wave_cols;
-  const int k_end = min(k_begin + a.wave_cols, a.cols);
-  const int g_row = r * a.n_colblocks;
+  const int range = max(0, min(a.wave_cols, a.cols - k_begin));
 
-  for (int k0 = k_begin; k0 < k_end; k0 += 64) {
-    // ---- 1. activity of 64 columns, union over the batch ----
-    const int k = k0 + lane;
-    const bool in_range = k < k_end;
+  // ---- 1. the wave's K range: activations and column metadata in one round
+  // trip (ColInfo/TileOffset are fetched for every column of the range, which
+  // removes a dependent memory round trip; their cache lines are shared by
+  // neighbouring columns, so little extra traffic results).
+  constexpr int kChunks = kMaxWaveCols / 64;
+  uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
+  // every load of the range first (one memory round trip), then the logic
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int off = 64 * c + lane;
+    const bool in = off < range;
+    const int k = k_begin + (in ? off : 0);
+    const int g = g_row + (k >> a.tk_log2);
+    colx[c] = ((uint32_t)g << a.tk_log2) + (uint32_t)(k & tk_mask);
+    ci[c] = 0u;
+    to[c] = 0u;
+    if (64 * c < range) {
+      ci[c] = a.col_info[colx[c]];
+      to[c] = a.tile_offset[g];
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) xb[c][b] = (in && b < a.batch) ? a.x[(size_t)b * a.cols + k] : 0u;
+  }
+  int n_act = 0;
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    const int off = 64 * c + lane;
+    const bool in = off < range;
     uint64_t act = 0;
+    bool on[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
-      uint32_t xb = 0;
-      if (in_range && b < a.batch) xb = a.x[(size_t)b * a.cols + k];
-      const int mag = (int)(xb & 0x7FFFu);
-      const bool on = in_range && b < a.batch && mag > a.code && mag <= 0x7C00;
-      act |= __builtin_amdgcn_ballot_w64(on);
-      xs[lane * NB + b] = on ? (uint16_t)xb : (uint16_t)0;
+      const int mag = (int)(xb[c][b] & 0x7FFFu);
+      on[b] = in && b < a.batch && mag > a.code && mag <= 0x7C00;
+      act |= __builtin_amdgcn_ballot_w64(on[b]);
     }
+    if ((act >> lane) & 1) {
+      const int pos = n_act + (int)mbcnt64(act);
+      ent_l[pos] = make_uint4(to[c] + (ci[c] >> 16), colx[c], ((ci[c] & 0xFFFFu) + 7u) >> 3, 0u);
+#pragma unroll
+      for (int b = 0; b < NB; ++b) xs_l[pos * NB + b] = on[b] ? (uint16_t)xb[c][b] : (uint16_t)0;
+    }
+    n_act += __builtin_popcountll(act);
+  }
+  // pad the last batch with harmless entries (value 0, column 0, no chunks)
+  if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1)))
+    ent_l[n_act + lane] = make_uint4(0u, 0u, 0u, 0u);
 
-    while (act) {
-      // ---- 2. pop up to kBatchCols active columns (scalar), fetch metadata ----
-      int kc[kBatchCols];
-      bool live[kBatchCols];
-#pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        live[u] = act != 0;
-        kc[u] = live[u] ? (int)__builtin_ctzll(act) : 0;  // dead slots alias column k0
-        act &= act - 1;
-      }
-      // Issue every scalar load of the batch before using any result: scalar
-      // loads return out of order, so each first use waits for all of them.
-      uint32_t ci[kBatchCols], to[kBatchCols];
-      Words4 bw[kBatchCols];
-#pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        const int kk = k0 + kc[u];
-        const int g = g_row + (kk >> a.tk_log2);
-        const size_t col = ((size_t)g << a.tk_log2) + (kk & tk_mask);
-        ci[u] = col_info[col];
-        to[u] = tile_offset[g];
-        const_ptr<uint64_t> bm = bitmap + col * wpc;  // arrays carry tail padding
-#pragma unroll
-        for (int w = 0; w < kMaxWords; ++w) bw[u].w[w] = bm[w];
-      }
-      int base[kBatchCols], nch[kBatchCols];
-#pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        base[u] = (int)(to[u] + (ci[u] >> 16));
-        nch[u] = (int)(((ci[u] & 0xFFFFu) + 7u) >> 3) & -(int)live[u];
-      }
-      // ---- values: two columns per 16-byte-per-lane load, straight into LDS ----
-      const int hsel = lane >> 5;
-      const int q = lane & 31;
-#pragma unroll
-      for (int pr = 0; pr < kBatchCols / 2; ++pr) {
-        // Lanes past the column's last chunk re-read its first chunk (same
-        // cache line, no extra HBM traffic); what they leave in the slot is
-        // never read, because only rows whose bitmap bit is set use a value.
-        const int my_base = hsel ? base[2 * pr + 1] : base[2 * pr];
-        const int my_nch = hsel ? nch[2 * pr + 1] : nch[2 * pr];
-        const int chunk = q < my_nch ? q : 0;
-        lds_dma16(a.values + (size_t)my_base + 8 * chunk, stage + 2 * pr * kSlotBytes);
-      }
-      uint64_t words[kBatchCols][kMaxWords];
-#pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        const uint64_t keep = 0ull - (uint64_t)live[u];
-#pragma unroll
-        for (int w = 0; w < kMaxWords; ++w)
-          words[u][w] = bw[u].w[w] & keep & (0ull - (uint64_t)(w < wpc));
-      }
-      __builtin_amdgcn_s_waitcnt(0);  // LDS DMA of this batch has landed
-      __builtin_amdgcn_wave_barrier();
+  // ---- 2. pipeline over batches of kBatch active columns: while batch i is
+  // decoded, batch i+1's values and bitmaps are already streaming into LDS.
+  const int n_batches = (n_act + kBatch - 1) / kBatch;
+  const int hsel = lane >> 5;
+  const int q = lane & 31;
+  const unsigned char* bitmap_bytes = reinterpret_cast<const unsigned char*>(a.bitmap);
 
-      // ---- 3. bitmap decode: rank by masked popcount, read the value ----
-      uint32_t vbits[kBatchCols][kMaxWords];
+  auto issue = [&](int i, unsigned char* val_buf, unsigned char* bm_buf) {
+    uint4 e[kBatch / 2];
 #pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        const uint16_t* slot = reinterpret_cast<const uint16_t*>(stage + u * kSlotBytes);
+    for (int pr = 0; pr < kBatch / 2; ++pr) e[pr] = ent_l[i * kBatch + 2 * pr + hsel];
+    const uint4 eb = ent_l[i * kBatch + (q >> 1)];
+    // values: lanes 0-31 fetch column 2pr, lanes 32-63 column 2pr+1, 16 B per
+    // lane; lanes past the column's end re-read its first chunk (same cache
+    // line) and what they leave in the slot is never read
+#pragma unroll
+    for (int pr = 0; pr < kBatch / 2; ++pr) {
+      const int chunk = q < (int)e[pr].z ? q : 0;
+      lds_dma16(a.values + (size_t)e[pr].x + 8 * chunk, val_buf + 2 * pr * kSlotBytes);
+    }
+    // bitmaps: lanes 2u and 2u+1 fetch the first and second 16 B of column u
+    // (columns with fewer than 4 words read into the arrays' tail padding)
+    if (lane < 32) lds_dma16(bitmap_bytes + (size_t)eb.y * wpc * 8 + 16 * (lane & 1), bm_buf);
+  };
+
+  // Columns are decoded four at a time so that each LDS round trip (bitmap
+  // words, then values) is shared by four columns.
+  constexpr int kQuad = 4;
+  auto decode = [&](int i, const unsigned char* val_buf, const unsigned char* bm_buf) {
+    const int n_here = min(kBatch, n_act - i * kBatch);
+    for (int u0 = 0; u0 < n_here; u0 += kQuad) {
+      uint4 braw[kQuad][2];
+#pragma unroll
+      for (int c = 0; c < kQuad; ++c) {
+        braw[c][0] = *reinterpret_cast<const uint4*>(bm_buf + 32 * (u0 + c));
+        braw[c][1] = *reinterpret_cast<const uint4*>(bm_buf + 32 * (u0 + c) + 16);
+      }
+      float xv[kQuad][NB];
+#pragma unroll
+      for (int c = 0; c < kQuad; ++c)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) xv[c][b] = half_bits_to_float(xs_l[(i * kBatch + u0 + c) * NB + b]);
+      uint64_t words[kQuad][kMaxWords];
+#pragma unroll
+      for (int c = 0; c < kQuad; ++c) {
+        // columns past the batch's end (padding entries) get empty bitmaps
+        const uint64_t keep = (u0 + c < n_here) ? ~0ull : 0ull;
+        words[c][0] = uniform64(braw[c][0].x, braw[c][0].y) & keep;
+        words[c][1] = wpc > 1 ? uniform64(braw[c][0].z, braw[c][0].w) & keep : 0ull;
+        words[c][2] = wpc > 2 ? uniform64(braw[c][1].x, braw[c][1].y) & keep : 0ull;
+        words[c][3] = wpc > 3 ? uniform64(braw[c][1].z, braw[c][1].w) & keep : 0ull;
+      }
+      // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
+      // below the lane, plus the popcounts of the column's earlier words
+      uint32_t vb[kQuad][kMaxWords];
+#pragma unroll
+      for (int c = 0; c < kQuad; ++c) {
+        const uint16_t* slot = reinterpret_cast<const uint16_t*>(val_buf + (u0 + c) * kSlotBytes);
         uint32_t prefix = 0;
 #pragma unroll
         for (int w = 0; w < kMaxWords; ++w) {
-          const uint32_t rank = min(prefix + mbcnt64(words[u][w]), 255u);
-          vbits[u][w] = slot[rank];
-          prefix += (uint32_t)__builtin_popcountll(words[u][w]);
+          vb[c][w] = slot[prefix + mbcnt64(words[c][w])];
+          prefix += (uint32_t)__builtin_popcountll(words[c][w]);
         }
       }
-      // ---- 4. accumulate where the bitmap bit is set ----
+      // 4. accumulate where the bitmap bit is set (the word is the EXEC mask)
 #pragma unroll
-      for (int u = 0; u < kBatchCols; ++u) {
-        float xv[NB];
-#pragma unroll
-        for (int b = 0; b < NB; ++b) xv[b] = half_bits_to_float(xs[kc[u] * NB + b]);
+      for (int c = 0; c < kQuad; ++c)
 #pragma unroll
         for (int w = 0; w < kMaxWords; ++w) {
-          if (__builtin_amdgcn_inverse_ballot_w64(words[u][w])) {
-            const float v = half_bits_to_float(vbits[u][w]);
+          if (__builtin_amdgcn_inverse_ballot_w64(words[c][w])) {
+            const float v = half_bits_to_float(vb[c][w]);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[b], acc[w][b]);
+            for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[c][b], acc[w][b]);
           }
         }
-      }
-      __builtin_amdgcn_wave_barrier();
     }
+  };
+
+  // Two-stage ping-pong: buffer 0 holds even batches, buffer 1 odd ones.
+  if (n_batches > 0) issue(0, my_val0, my_bm0);
+  for (int i = 0; i < n_batches; i += 2) {
+    if (i + 1 < n_batches) {
+      issue(i + 1, my_val1, my_bm1);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kLoadsPerBatch));
+    } else {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    }
+    __builtin_amdgcn_wave_barrier();
+    decode(i, my_val0, my_bm0);
+    if (i + 1 >= n_batches) break;
+    if (i + 2 < n_batches) {
+      issue(i + 2, my_val0, my_bm0);
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kLoadsPerBatch));
+    } else {
+      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    }
+    __builtin_amdgcn_wave_barrier();
+    decode(i + 1, my_val1, my_bm1);
   }
 
-  // ---- 5. reduce the 4 waves in LDS, write this segment's partial sums ----
+  // ---- 5. reduce the 4 waves in LDS, write this segment's partial sums
   const int mpad = a.n_stripes * a.tile_m;
-  float* red = reinterpret_cast<float*>(smem);
+  float* red = reinterpret_cast<float*>(val0);
   constexpr int kSlice = Smem<NB>::kSlice;
 #pragma unroll
   for (int b0 = 0; b0 < NB; b0 += kSlice) {
@@ -253,34 +312,55 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
           float s = 0.0f;
 #pragma unroll
           for (int wv = 0; wv < kWaves; ++wv) s += red[(wv * kSlice + bb) * 256 + row];
-          a.partials[((size_t)seg * a.batch + b) * mpad + (size_t)r * a.tile_m + row] = s;
+          // device-coherent store: read back below by whichever workgroup
+          // of this stripe arrives last, possibly on another XCD
+          __hip_atomic_store(&a.partials[((size_t)seg * a.batch + b) * mpad + (size_t)r * a.tile_m + row],
+                             s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
       }
     }
   }
 
-  // ---- split-K completion: the last workgroup of the stripe finishes Y ----
-  __threadfence();
+  // ---- split-K completion. The partial stores above bypass the per-XCD L2
+  // (device-scope atomics), so waiting for their completion before counting
+  // in publishes them without an L2-wide write-back; the last workgroup reads
+  // them with device-scope loads.
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0);
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
   __syncthreads();
   if (threadIdx.x == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(&a.counters[r], 1u, __ATOMIC_ACQ_REL,
+    const uint32_t prev = __hip_atomic_fetch_add(&a.counters[r], 1u, __ATOMIC_RELAXED,
                                                  __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == (uint32_t)(a.segments - 1));
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
   const int row = threadIdx.x;
   const int m = r * a.tile_m + row;
   if (row < a.tile_m && m < a.rows) {
+    // All segments' partials of a token are requested before any is added, so
+    // the reduction costs one memory round trip per kFinal segments, and the
+    // sum runs in segment order (deterministic).
+    constexpr int kFinal = 16;
     for (int b = 0; b < a.batch; ++b) {
       float s = 0.0f;
-      for (int sg = 0; sg < a.segments; ++sg)
-        s += a.partials[((size_t)sg * a.batch + b) * mpad + m];
+      for (int sg0 = 0; sg0 < a.segments; sg0 += kFinal) {
+        float v[kFinal];
+#pragma unroll
+        for (int j = 0; j < kFinal; ++j) {
+          const int sg = min(sg0 + j, a.segments - 1);
+          v[j] = __hip_atomic_load(&a.partials[((size_t)sg * a.batch + b) * mpad + m], __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        }
+#pragma unroll
+        for (int j = 0; j < kFinal; ++j)
+          if (sg0 + j < a.segments) s += v[j];
+      }
       a.y[(size_t)b * a.rows + m] = __half_as_ushort(__float2half_rn(s));
     }
   }
-  if (threadIdx.x == 0) a.counters[r] = 0u;
+  if (threadIdx.x == 0) __hip_atomic_store(&a.counters[r], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 using spdp::fail;
@@ -289,20 +369,22 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(SPDP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Split-K heuristic: aim for about 1024 workgroups (4 per CU on 256 CUs)
-// while giving every wave at least 16 columns; SPDP_SPLITK overrides the
-// number of segments for tuning.
+// Split-K heuristic: about 2048 waves (8 per CU on 256 CUs), every wave
+// covering a multiple of 16 columns and at most kMaxWaveCols of them.
+// SPDP_SPLITK overrides the number of segments (for tuning).
 void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   const int64_t cols = m->cols;
-  int64_t want = std::max<int64_t>(1, 1024 / std::max<int64_t>(1, m->n_stripes));
+  const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
+  int64_t want = std::max<int64_t>(1, 2048 / (kWaves * stripes));
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1) want = v;
   }
+  const int64_t min_seg = (cols + kWaves * kMaxWaveCols - 1) / (kWaves * kMaxWaveCols);
   const int64_t max_seg = std::max<int64_t>(1, (cols + kWaves * 16 - 1) / (kWaves * 16));
-  const int64_t s = std::min(want, max_seg);
+  const int64_t s = std::max(min_seg, std::min(want, max_seg));
   int64_t wc = (cols + s * kWaves - 1) / (s * kWaves);
-  wc = (wc + 15) / 16 * 16;
+  wc = std::min<int64_t>(kMaxWaveCols, (wc + 15) / 16 * 16);
   *wave_cols = (int)wc;
   *segments = (int)((cols + wc * kWaves - 1) / (wc * kWaves));
 }
