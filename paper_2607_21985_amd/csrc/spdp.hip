@@ -42,7 +42,8 @@ constexpr int kWaves = 4;                 // waves per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxWords = 4;              // tile_m <= 256: at most 4 bitmap words per column
 constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one stripe (fp16)
-constexpr int kBatch = 16;                // active columns per pipeline stage of a wave
+constexpr int kBatch = 8;                 // active columns per pipeline stage of a wave
+constexpr int kQuad = 4;                  // columns decoded together
 constexpr int kMaxWaveCols = 128;         // columns of one wave's K range
 constexpr int kLoadsPerBatch = kBatch / 2 + 1;  // 16-byte-per-lane loads issued per stage
 constexpr int kMaxBatch = 32;
@@ -57,22 +58,23 @@ struct KernelArgs {
   float* partials;     // [segments][batch][n_stripes * tile_m]
   uint32_t* counters;  // [n_stripes], zero between calls
   int rows, cols;
-  int tile_m, wpc, tk_log2, n_colblocks, n_stripes;
+  int tile_m, tk_log2, n_colblocks, n_stripes;
   int batch;
   int code;       // threshold code: active iff code < (x & 0x7fff) <= 0x7c00
   int wave_cols;  // columns per wave (multiple of 16, <= kMaxWaveCols)
   int segments;   // workgroups per row stripe
+  uint32_t zero_col;  // column index whose bitmap lies in the zeroed tail padding
 };
 
 // LDS use. The two pipeline buffers are separate __shared__ arrays so that
 // the compiler can tell reads of one from LDS-DMA writes into the other (it
 // then waits only for the DMA a read depends on).
 constexpr int kValBufBytes = kWaves * kBatch * kSlotBytes;  // one stage, all waves
-constexpr int kBmBufBytes = kWaves * 32 * 16;              // one stage, all waves
+constexpr int kBmBufBytes = kWaves * kBatch * 32;          // one stage, all waves
 
 template <int NB>
 struct Smem {
-  static constexpr int kSlice = NB < 8 ? NB : 8;  // tokens per cross-wave reduction pass
+  static constexpr int kSlice = NB < 4 ? NB : 4;  // tokens per cross-wave reduction pass
   static constexpr int kRed = kWaves * kSlice * 256 * 4;
   static_assert(kRed <= kValBufBytes, "reduction reuses the first value buffer");
 };
@@ -98,6 +100,16 @@ __device__ __forceinline__ void lds_dma16(const void* src, void* lds_base) {
                                    16, 0, 0);
 }
 
+// Read-only arrays reached through the constant address space: uniform
+// (per-column) reads of them compile to scalar loads.
+template <class T>
+using const_ptr = const __attribute__((address_space(4))) T*;
+
+template <class T>
+__device__ __forceinline__ const_ptr<T> as_const(const T* p) {
+  return reinterpret_cast<const_ptr<T>>(reinterpret_cast<uintptr_t>(p));
+}
+
 // Wave-uniform 64-bit value from two VGPR halves (readfirstlane yields int:
 // go through uint32_t so that bit 31 of the low half is not sign-extended).
 __device__ __forceinline__ uint64_t uniform64(uint32_t lo, uint32_t hi) {
@@ -105,16 +117,19 @@ __device__ __forceinline__ uint64_t uniform64(uint32_t lo, uint32_t hi) {
          ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(hi) << 32);
 }
 
-template <int NB>
+// NB: tokens per call rounded up to a power of two; WPC: bitmap words per
+// column (tile_m / 64).
+template <int NB, int WPC>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char val0[kValBufBytes];
   __shared__ __attribute__((aligned(1024))) unsigned char val1[kValBufBytes];
-  __shared__ __attribute__((aligned(512))) unsigned char bm0[kBmBufBytes];
-  __shared__ __attribute__((aligned(512))) unsigned char bm1[kBmBufBytes];
+  __shared__ __attribute__((aligned(256))) unsigned char bm0[kBmBufBytes];
+  __shared__ __attribute__((aligned(256))) unsigned char bm1[kBmBufBytes];
   // one entry per active column, in activity order: {value base, column
   // index into ColInfo/bitmap, 16-byte chunks of values, unused}
   __shared__ uint4 ent_s[kWaves][kMaxWaveCols];
   __shared__ uint16_t xs_s[kWaves][kMaxWaveCols * NB];
+  __shared__ __attribute__((aligned(16))) uint32_t col_s[kWaves][kMaxWaveCols];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
@@ -122,19 +137,19 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int seg = blockIdx.x;
   const int r = blockIdx.y;
   const int tk_mask = (1 << a.tk_log2) - 1;
-  const int wpc = a.wpc;
   const int g_row = r * a.n_colblocks;
 
   uint4* ent_l = ent_s[wave];
   uint16_t* xs_l = xs_s[wave];
+  uint32_t* col_l = col_s[wave];
   unsigned char* my_val0 = val0 + wave * (kBatch * kSlotBytes);
   unsigned char* my_val1 = val1 + wave * (kBatch * kSlotBytes);
-  unsigned char* my_bm0 = bm0 + wave * (32 * 16);
-  unsigned char* my_bm1 = bm1 + wave * (32 * 16);
+  unsigned char* my_bm0 = bm0 + wave * (kBatch * 32);
+  unsigned char* my_bm1 = bm1 + wave * (kBatch * 32);
 
-  float acc[kMaxWords][NB];
+  float acc[WPC][NB];
 #pragma unroll
-  for (int w = 0; w < kMaxWords; ++w)
+  for (int w = 0; w < WPC; ++w)
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
 
@@ -147,7 +162,6 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   // neighbouring columns, so little extra traffic results).
   constexpr int kChunks = kMaxWaveCols / 64;
   uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
-  // every load of the range first (one memory round trip), then the logic
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int off = 64 * c + lane;
@@ -180,14 +194,19 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     if ((act >> lane) & 1) {
       const int pos = n_act + (int)mbcnt64(act);
       ent_l[pos] = make_uint4(to[c] + (ci[c] >> 16), colx[c], ((ci[c] & 0xFFFFu) + 7u) >> 3, 0u);
+      col_l[pos] = colx[c];
 #pragma unroll
       for (int b = 0; b < NB; ++b) xs_l[pos * NB + b] = on[b] ? (uint16_t)xb[c][b] : (uint16_t)0;
     }
     n_act += __builtin_popcountll(act);
   }
-  // pad the last batch with harmless entries (value 0, column 0, no chunks)
+  // Pad the last batch with entries that read an all-zero bitmap (in the
+  // bitmap array's zeroed tail) and no values: they decode to nothing.
   if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1)))
-    ent_l[n_act + lane] = make_uint4(0u, 0u, 0u, 0u);
+  {
+    ent_l[n_act + lane] = make_uint4(0u, a.zero_col, 0u, 0u);
+    col_l[n_act + lane] = a.zero_col;
+  }
 
   // ---- 2. pipeline over batches of kBatch active columns: while batch i is
   // decoded, batch i+1's values and bitmaps are already streaming into LDS.
@@ -200,7 +219,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     uint4 e[kBatch / 2];
 #pragma unroll
     for (int pr = 0; pr < kBatch / 2; ++pr) e[pr] = ent_l[i * kBatch + 2 * pr + hsel];
-    const uint4 eb = ent_l[i * kBatch + (q >> 1)];
+    const uint4 eb = ent_l[i * kBatch + ((lane >> 1) & (kBatch - 1))];
     // values: lanes 0-31 fetch column 2pr, lanes 32-63 column 2pr+1, 16 B per
     // lane; lanes past the column's end re-read its first chunk (same cache
     // line) and what they leave in the slot is never read
@@ -210,55 +229,58 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       lds_dma16(a.values + (size_t)e[pr].x + 8 * chunk, val_buf + 2 * pr * kSlotBytes);
     }
     // bitmaps: lanes 2u and 2u+1 fetch the first and second 16 B of column u
-    // (columns with fewer than 4 words read into the arrays' tail padding)
-    if (lane < 32) lds_dma16(bitmap_bytes + (size_t)eb.y * wpc * 8 + 16 * (lane & 1), bm_buf);
+    // (columns with fewer than 4 words read into the next column or the
+    // arrays' tail padding; those words are never used)
+    if (lane < 2 * kBatch) lds_dma16(bitmap_bytes + (size_t)eb.y * WPC * 8 + 16 * (lane & 1), bm_buf);
   };
 
-  // Columns are decoded four at a time so that each LDS round trip (bitmap
-  // words, then values) is shared by four columns.
-  constexpr int kQuad = 4;
-  auto decode = [&](int i, const unsigned char* val_buf, const unsigned char* bm_buf) {
+  // The decode reads each quad's column indices from LDS, moves them to
+  // scalar registers and loads the columns' bitmap words with scalar loads:
+  // the words then serve directly as MaskedPopcount masks and EXEC masks.
+  // (The LDS-DMA of the bitmaps above only pulls their lines into L2 ahead of
+  // these loads.)
+  const_ptr<uint64_t> bitmap_c = as_const(a.bitmap);
+
+  auto decode = [&](int i, const unsigned char* val_buf) {
     const int n_here = min(kBatch, n_act - i * kBatch);
     for (int u0 = 0; u0 < n_here; u0 += kQuad) {
-      uint4 braw[kQuad][2];
+      const uint4 cq = *reinterpret_cast<const uint4*>(&col_l[i * kBatch + u0]);
+      const uint32_t cols[kQuad] = {(uint32_t)__builtin_amdgcn_readfirstlane(cq.x),
+                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.y),
+                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.z),
+                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.w)};
+      uint64_t words[kQuad][WPC];
 #pragma unroll
       for (int c = 0; c < kQuad; ++c) {
-        braw[c][0] = *reinterpret_cast<const uint4*>(bm_buf + 32 * (u0 + c));
-        braw[c][1] = *reinterpret_cast<const uint4*>(bm_buf + 32 * (u0 + c) + 16);
+        const_ptr<uint64_t> bm = bitmap_c + (size_t)cols[c] * WPC;
+#pragma unroll
+        for (int w = 0; w < WPC; ++w) words[c][w] = bm[w];
       }
       float xv[kQuad][NB];
 #pragma unroll
       for (int c = 0; c < kQuad; ++c)
 #pragma unroll
         for (int b = 0; b < NB; ++b) xv[c][b] = half_bits_to_float(xs_l[(i * kBatch + u0 + c) * NB + b]);
-      uint64_t words[kQuad][kMaxWords];
-#pragma unroll
-      for (int c = 0; c < kQuad; ++c) {
-        // columns past the batch's end (padding entries) get empty bitmaps
-        const uint64_t keep = (u0 + c < n_here) ? ~0ull : 0ull;
-        words[c][0] = uniform64(braw[c][0].x, braw[c][0].y) & keep;
-        words[c][1] = wpc > 1 ? uniform64(braw[c][0].z, braw[c][0].w) & keep : 0ull;
-        words[c][2] = wpc > 2 ? uniform64(braw[c][1].x, braw[c][1].y) & keep : 0ull;
-        words[c][3] = wpc > 3 ? uniform64(braw[c][1].z, braw[c][1].w) & keep : 0ull;
-      }
       // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
       // below the lane, plus the popcounts of the column's earlier words
-      uint32_t vb[kQuad][kMaxWords];
+      uint32_t vb[kQuad][WPC];
 #pragma unroll
       for (int c = 0; c < kQuad; ++c) {
         const uint16_t* slot = reinterpret_cast<const uint16_t*>(val_buf + (u0 + c) * kSlotBytes);
         uint32_t prefix = 0;
 #pragma unroll
-        for (int w = 0; w < kMaxWords; ++w) {
+        for (int w = 0; w < WPC; ++w) {
           vb[c][w] = slot[prefix + mbcnt64(words[c][w])];
           prefix += (uint32_t)__builtin_popcountll(words[c][w]);
         }
       }
-      // 4. accumulate where the bitmap bit is set (the word is the EXEC mask)
+      // 4. accumulate where the bitmap bit is set (the word is the lane mask;
+      // the compiler turns this into an FMA plus a select on it, which
+      // measures faster than branching on EXEC)
 #pragma unroll
       for (int c = 0; c < kQuad; ++c)
 #pragma unroll
-        for (int w = 0; w < kMaxWords; ++w) {
+        for (int w = 0; w < WPC; ++w) {
           if (__builtin_amdgcn_inverse_ballot_w64(words[c][w])) {
             const float v = half_bits_to_float(vb[c][w]);
 #pragma unroll
@@ -278,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     }
     __builtin_amdgcn_wave_barrier();
-    decode(i, my_val0, my_bm0);
+    decode(i, my_val0);
     if (i + 1 >= n_batches) break;
     if (i + 2 < n_batches) {
       issue(i + 2, my_val0, my_bm0);
@@ -287,7 +309,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
     }
     __builtin_amdgcn_wave_barrier();
-    decode(i + 1, my_val1, my_bm1);
+    decode(i + 1, my_val1);
   }
 
   // ---- 5. reduce the 4 waves in LDS, write this segment's partial sums
@@ -298,13 +320,12 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   for (int b0 = 0; b0 < NB; b0 += kSlice) {
     __syncthreads();
 #pragma unroll
-    for (int w = 0; w < kMaxWords; ++w)
+    for (int w = 0; w < WPC; ++w)
 #pragma unroll
-      for (int bb = 0; bb < kSlice; ++bb)
-        if (w < wpc) red[(wave * kSlice + bb) * 256 + 64 * w + lane] = acc[w][b0 + bb];
+      for (int bb = 0; bb < kSlice; ++bb) red[(wave * kSlice + bb) * 256 + 64 * w + lane] = acc[w][b0 + bb];
     __syncthreads();
     const int row = threadIdx.x;
-    if (row < a.tile_m) {
+    if (row < 64 * WPC) {
 #pragma unroll
       for (int bb = 0; bb < kSlice; ++bb) {
         const int b = b0 + bb;
@@ -338,11 +359,11 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   if (!s_last) return;
   const int row = threadIdx.x;
   const int m = r * a.tile_m + row;
-  if (row < a.tile_m && m < a.rows) {
+  if (row < 64 * WPC && m < a.rows) {
     // All segments' partials of a token are requested before any is added, so
     // the reduction costs one memory round trip per kFinal segments, and the
     // sum runs in segment order (deterministic).
-    constexpr int kFinal = 16;
+    constexpr int kFinal = 32;
     for (int b = 0; b < a.batch; ++b) {
       float s = 0.0f;
       for (int sg0 = 0; sg0 < a.segments; sg0 += kFinal) {
@@ -449,10 +470,20 @@ int upload(const std::vector<T>& v, void** dst) {
   return SPDP_OK;
 }
 
-template <int NB>
-hipError_t launch(const KernelArgs& args, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL(spmspv_kernel<NB>, grid, dim3(kThreads), 0, stream, args);
+template <int NB, int WPC>
+hipError_t launch_one(const KernelArgs& args, dim3 grid, hipStream_t stream) {
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
+}
+
+template <int NB>
+hipError_t launch(const KernelArgs& args, int wpc, dim3 grid, hipStream_t stream) {
+  switch (wpc) {
+    case 1: return launch_one<NB, 1>(args, grid, stream);
+    case 2: return launch_one<NB, 2>(args, grid, stream);
+    case 3: return launch_one<NB, 3>(args, grid, stream);
+    default: return launch_one<NB, 4>(args, grid, stream);
+  }
 }
 
 }  // namespace
@@ -558,7 +589,8 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float thresho
   args.rows = (int)h->rows;
   args.cols = (int)h->cols;
   args.tile_m = h->tile_m;
-  args.wpc = h->tile_m / 64;
+  const int wpc = h->tile_m / 64;
+  args.zero_col = (uint32_t)(h->n_gtiles * h->tile_k);
   args.tk_log2 = __builtin_ctz((unsigned)h->tile_k);
   args.n_colblocks = (int)h->n_colblocks;
   args.n_stripes = (int)h->n_stripes;
@@ -570,17 +602,17 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float thresho
   const dim3 grid((unsigned)segments, (unsigned)h->n_stripes);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (batch <= 1)
-    e = launch<1>(args, grid, s);
+    e = launch<1>(args, wpc, grid, s);
   else if (batch <= 2)
-    e = launch<2>(args, grid, s);
+    e = launch<2>(args, wpc, grid, s);
   else if (batch <= 4)
-    e = launch<4>(args, grid, s);
+    e = launch<4>(args, wpc, grid, s);
   else if (batch <= 8)
-    e = launch<8>(args, grid, s);
+    e = launch<8>(args, wpc, grid, s);
   else if (batch <= 16)
-    e = launch<16>(args, grid, s);
+    e = launch<16>(args, wpc, grid, s);
   else
-    e = launch<32>(args, grid, s);
+    e = launch<32>(args, wpc, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }
