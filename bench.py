@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--no-dense", action="store_true")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed steps only (for rocprofv3 runs)")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after the timed steps, run one device-to-device copy of this many MiB "
+                         "(a known-size reference for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -209,26 +212,42 @@ def main():
     ev1.record(stream)
     torch.cuda.synchronize(dev)
     total_ms = ev0.elapsed_time(ev1)
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20)
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize(dev)
+        dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        del src, dst
     if args.profile_only:
-        print(json.dumps({"profile_only": True, "ms_per_step": total_ms / args.steps}), flush=True)
+        print(json.dumps({"profile_only": True, "ms_per_step": total_ms / args.steps,
+                          "launches": (args.warmup + args.steps) * len(points),
+                          "algorithmic_bytes_per_launch": sum(pt["bytes"] for pt in points) / len(points)}),
+              flush=True)
         return
     ms_per_step = total_ms / args.steps
     step_bytes = sum(pt["bytes"] for pt in points)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
 
-    # ---- per-launch durations (HIP events around each launch, same stream)
-    per_call = np.zeros(len(points))
+    # ---- kernel duration per sweep point: launches run back to back on one
+    # stream (no gaps between kernels), so HIP events around a run of
+    # launches divided by their number give the kernels' average duration;
+    # an event pair around every single launch would add its own overhead.
+    n_proj = len(wl["projections"])
     reps = max(2, min(10, args.steps))
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in points]
-    for i in range(reps):
-        c = (args.warmup + args.steps + i) % n_copies
-        for j, pt in enumerate(points):
-            evs[j][0].record(stream)
-            copies[c][j].spmspv_into(X[c][j], pt["t"], Y[c][j], stream)
-            evs[j][1].record(stream)
+    per_call = np.zeros(len(points))
+    for k in range(0, len(points), n_proj):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for rep in range(reps):
+            c = rep % n_copies
+            for j in range(k, k + n_proj):
+                copies[c][j].spmspv_into(X[c][j], points[j]["t"], Y[c][j], stream)
+        e1.record(stream)
         torch.cuda.synchronize(dev)
-        per_call += np.array([a.elapsed_time(b) for a, b in evs]) / reps
-    kern_ms = float(per_call.sum())
+        per_call[k:k + n_proj] = e0.elapsed_time(e1) / (reps * n_proj)
+    kern_ms = ms_per_step
     achieved = step_bytes / (kern_ms * 1e-3) / 1e9
 
     # ---- dense fp16 GEMV baseline (torch F.linear), rotated the same way
@@ -266,7 +285,6 @@ def main():
 
     # ---- per-point summary
     pts_out = []
-    n_proj = len(wl["projections"])
     for k in range(0, len(points), n_proj):
         grp = points[k:k + n_proj]
         us = float(per_call[k:k + n_proj].sum() * 1e3 / n_proj)
@@ -314,6 +332,7 @@ def main():
             "traffic": traffic,
             "kernel": "spmspv_kernel",
             "kernel_us_per_launch": round(kern_ms * 1e3 / len(points), 3),
+            "duration_source": "HIP events around the timed steps (back-to-back launches on one stream)",
             "algorithmic_bytes_per_launch": int(step_bytes / len(points)),
         },
         "cpu_baseline": cpu,
