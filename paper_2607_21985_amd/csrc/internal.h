@@ -25,11 +25,11 @@ struct spdp_matrix {
   void* d_bitmap = nullptr;
   void* d_values = nullptr;
 
-  // Split-K workspace: fp32 partial sums [segments][batch][n_stripes*tile_m]
-  // and one arrival counter per row stripe (zero between calls).
-  float* d_partials = nullptr;
-  size_t partial_floats = 0;
-  uint32_t* d_counters = nullptr;
+  // Split-K workspace: {fp32 partial sum, epoch} pairs
+  // [segments - 1][batch][n_stripes*tile_m], and the epoch of the last call.
+  unsigned long long* d_partials = nullptr;
+  size_t partial_floats = 0;  // capacity in pairs
+  uint32_t epoch = 0;
 };
 
 namespace spdp {

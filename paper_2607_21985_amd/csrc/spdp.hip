@@ -3,28 +3,33 @@
 // own device memory.
 //
 // One launch per call does the whole path:
-//   1. activity: each wave reads its slice of the activations and takes the
-//      strict magnitude test |x| > t as an integer compare on fp16 bits; a
-//      64-lane ballot turns the per-token results into a 64-column mask
-//      (union over the batch) held in scalar registers (Sec. 4.2, XTile
-//      loading and the activation-aware selection of GTile loading);
-//   2. metadata then data (Sec. 4.2.2, "metadata first, data second"): the
-//      scalar unit walks the set bits of the mask, loads each active column's
-//      ColInfo and TileOffset entry with scalar loads, and the wave streams the
-//      column's padded values with 16-byte vector loads into LDS, two columns
-//      per load instruction (lanes 0-31 and 32-63);
+//   1. activity: each wave reads its K range of the activations and takes
+//      the strict magnitude test |x| > t as an integer compare on fp16 bits;
+//      64-lane ballots (union over the batch) compact the active columns into
+//      a per-wave list in LDS (Sec. 4.2, XTile loading and the
+//      activation-aware selection of GTile loading);
+//   2. metadata then data (Sec. 4.2.2): ColInfo and TileOffset of the range
+//      arrive in the same round trip as the activations; the list then
+//      drives batches of 8 active columns whose padded values (16-byte vector
+//      loads, two columns per load instruction) and bitmap words stream into
+//      registers three batches ahead of the decode; a batch moves to LDS
+//      right before it is decoded;
 //   3. bitmap decode (HAD-SMBD, Sec. 4.2.1): lane i owns row 64w+i of bitmap
 //      word w; its value sits at the masked popcount of the word below bit i
 //      (v_mbcnt_lo/hi, the MaskedPopcount of the paper) plus the popcount of
-//      the earlier words, and the word itself is the execution mask, so rows
-//      without a nonzero issue no LDS read and no FMA;
+//      the earlier words, and the word itself (read out of the batch's
+//      registers with v_readlane) is the execution mask, so rows without a
+//      nonzero issue no LDS read and no FMA;
 //   4. accumulate in fp32 on the vector ALUs with fp16 operands (v_fma_mix),
 //      no matrix cores (Sec. 3.3 challenge 2, Sec. 4.2 step 5);
 //   5. split-K (Sec. 4.2.3): the workgroups of a row stripe cover disjoint K
-//      segments; each reduces its 4 waves in LDS and writes fp32 partial sums
-//      to a workspace, and the last workgroup to arrive for the stripe adds
-//      the partials in segment order and writes fp16 Y (round to nearest
-//      even), then re-arms the stripe's counter for the next call.
+//      segments; each reduces its 4 waves in LDS. Every segment but the last
+//      stores its fp32 partial sums to a workspace, each value paired with
+//      the call's epoch number in one 8-byte store; the last segment's
+//      workgroup loads the other segments' partials until every one carries
+//      the current epoch, adds them in segment order (its own last) and
+//      writes fp16 Y (round to nearest even). No counter, no fence: a
+//      partial is usable as soon as its own store has landed.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -45,8 +50,9 @@ constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one s
 constexpr int kBatch = 8;                 // active columns per pipeline stage of a wave
 constexpr int kQuad = 4;                  // columns decoded together
 constexpr int kMaxWaveCols = 128;         // columns of one wave's K range
-constexpr int kLoadsPerBatch = kBatch / 2 + 1;  // 16-byte-per-lane loads issued per stage
+constexpr int kDepth = 3;                 // batches whose values are in flight per wave
 constexpr int kMaxBatch = 32;
+constexpr int kDummyBatch = kMaxWaveCols / kBatch;  // LDS batch of all-zero entries
 
 struct KernelArgs {
   const uint32_t* tile_offset;
@@ -55,8 +61,9 @@ struct KernelArgs {
   const uint16_t* values;
   const uint16_t* x;
   uint16_t* y;
-  float* partials;     // [segments][batch][n_stripes * tile_m]
-  uint32_t* counters;  // [n_stripes], zero between calls
+  // [segments - 1][batch][n_stripes * tile_m]: {fp32 bits, epoch} pairs
+  unsigned long long* partials;
+  uint32_t epoch;      // this call's tag, never 0 (the workspace starts zeroed)
   int rows, cols;
   int tile_m, tk_log2, n_colblocks, n_stripes;
   int batch;
@@ -66,22 +73,16 @@ struct KernelArgs {
   uint32_t zero_col;  // column index whose bitmap lies in the zeroed tail padding
 };
 
-// LDS use. The two pipeline buffers are separate __shared__ arrays so that
-// the compiler can tell reads of one from LDS-DMA writes into the other (it
-// then waits only for the DMA a read depends on).
-constexpr int kValBufBytes = kWaves * kBatch * kSlotBytes;  // one stage, all waves
-constexpr int kBmBufBytes = kWaves * kBatch * 32;          // one stage, all waves
+// LDS use: one value slot buffer per wave (the batch being decoded; the
+// batches in flight live in registers).
+constexpr int kValBufBytes = kWaves * kBatch * kSlotBytes;
 
 template <int NB>
 struct Smem {
   static constexpr int kSlice = NB < 4 ? NB : 4;  // tokens per cross-wave reduction pass
   static constexpr int kRed = kWaves * kSlice * 256 * 4;
-  static_assert(kRed <= kValBufBytes, "reduction reuses the first value buffer");
+  static_assert(kRed <= kValBufBytes, "reduction reuses the value buffer");
 };
-
-// s_waitcnt immediate for gfx9: wait until at most n vector-memory operations
-// are outstanding, leaving the LDS/scalar and export counters unconstrained.
-constexpr int vmcnt_imm(int n) { return (n & 0xF) | (((n >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8); }
 
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
   return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -92,44 +93,77 @@ __device__ __forceinline__ float half_bits_to_float(uint32_t h) {
   return __half2float(__ushort_as_half((unsigned short)h));
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane i's bytes land
-// at lds_base + 16 * i (gfx950 LDS DMA).
-__device__ __forceinline__ void lds_dma16(const void* src, void* lds_base) {
-  __builtin_amdgcn_global_load_lds(src, reinterpret_cast<__attribute__((address_space(3))) void*>(
-                                            reinterpret_cast<uintptr_t>(lds_base)),
-                                   16, 0, 0);
-}
-
-// Read-only arrays reached through the constant address space: uniform
-// (per-column) reads of them compile to scalar loads.
+// Pointers into the constant address space: reads through them are scalar
+// loads.
 template <class T>
 using const_ptr = const __attribute__((address_space(4))) T*;
 
-template <class T>
-__device__ __forceinline__ const_ptr<T> as_const(const T* p) {
-  return reinterpret_cast<const_ptr<T>>(reinterpret_cast<uintptr_t>(p));
+// One column of one token: acc[w] += f32(v[w]) * f32(x) in the lanes whose
+// bit is set in word w, where v[w] and x are fp16 bits. The whole column is
+// one block so that nothing else runs under the narrowed EXEC: save EXEC
+// while ANDing it with the first word, AND the saved mask with each later
+// word, restore at the end (one scalar instruction per word, no branch).
+template <int WPC>
+__device__ __forceinline__ void masked_fma_column(float (&acc)[WPC][1], const uint32_t (&v)[WPC],
+                                                  uint32_t x, const uint64_t (&m)[WPC]) {
+  uint64_t save;
+#define SPDP_FMA(W) "v_fma_mix_f32 %[a" #W "], %[v" #W "], %[x], %[a" #W "] op_sel_hi:[1,1,0]\n\t"
+  if constexpr (WPC == 1) {
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0) "s_mov_b64 exec, %[sv]"
+                 : [a0] "+v"(acc[0][0]), [sv] "=&s"(save)
+                 : [m0] "s"(m[0]), [v0] "v"(v[0]), [x] "v"(x)
+                 : "scc");
+  } else if constexpr (WPC == 2) {
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1) "s_mov_b64 exec, %[sv]"
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [sv] "=&s"(save)
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [v0] "v"(v[0]), [v1] "v"(v[1]), [x] "v"(x)
+                 : "scc");
+  } else if constexpr (WPC == 3) {
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1)
+                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2) "s_mov_b64 exec, %[sv]"
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]), [sv] "=&s"(save)
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [v0] "v"(v[0]), [v1] "v"(v[1]),
+                   [v2] "v"(v[2]), [x] "v"(x)
+                 : "scc");
+  } else {
+    static_assert(WPC == 4, "at most four bitmap words per column");
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1)
+                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2)
+                 "s_and_b64 exec, %[sv], %[m3]\n\t" SPDP_FMA(3) "s_mov_b64 exec, %[sv]"
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]),
+                   [a3] "+v"(acc[3][0]), [sv] "=&s"(save)
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [m3] "s"(m[3]), [v0] "v"(v[0]),
+                   [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [x] "v"(x)
+                 : "scc");
+  }
+#undef SPDP_FMA
 }
 
-// Wave-uniform 64-bit value from two VGPR halves (readfirstlane yields int:
-// go through uint32_t so that bit 31 of the low half is not sign-extended).
-__device__ __forceinline__ uint64_t uniform64(uint32_t lo, uint32_t hi) {
-  return (uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(lo) |
-         ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(hi) << 32);
+// The kernel's argument block, read again from the kernel-argument segment
+// through a pointer the compiler cannot see through: fields used only after
+// the main loop are loaded there instead of holding scalar registers
+// throughout it.
+template <class Args>
+__device__ __forceinline__ const_ptr<Args> reload_args() {
+  auto p = (const_ptr<Args>)__builtin_amdgcn_kernarg_segment_ptr();
+  asm volatile("" : "+s"(p));
+  return p;
 }
 
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
 // column (tile_m / 64).
 template <int NB, int WPC>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char val0[kValBufBytes];
-  __shared__ __attribute__((aligned(1024))) unsigned char val1[kValBufBytes];
-  __shared__ __attribute__((aligned(256))) unsigned char bm0[kBmBufBytes];
-  __shared__ __attribute__((aligned(256))) unsigned char bm1[kBmBufBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char valbuf[kValBufBytes];
   // one entry per active column, in activity order: {value base, column
-  // index into ColInfo/bitmap, 16-byte chunks of values, unused}
-  __shared__ uint4 ent_s[kWaves][kMaxWaveCols];
+  // index into ColInfo/bitmap, 16-byte chunks of values, unused}; batch
+  // kDummyBatch holds entries that load nothing of use (see below)
+  __shared__ uint4 ent_s[kWaves][kMaxWaveCols + kBatch];
   __shared__ uint16_t xs_s[kWaves][kMaxWaveCols * NB];
-  __shared__ __attribute__((aligned(16))) uint32_t col_s[kWaves][kMaxWaveCols];
+  __shared__ __attribute__((aligned(16))) uint32_t col_s[kWaves][kMaxWaveCols + kBatch];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
@@ -142,10 +176,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   uint4* ent_l = ent_s[wave];
   uint16_t* xs_l = xs_s[wave];
   uint32_t* col_l = col_s[wave];
-  unsigned char* my_val0 = val0 + wave * (kBatch * kSlotBytes);
-  unsigned char* my_val1 = val1 + wave * (kBatch * kSlotBytes);
-  unsigned char* my_bm0 = bm0 + wave * (kBatch * 32);
-  unsigned char* my_bm1 = bm1 + wave * (kBatch * 32);
+  unsigned char* my_val = valbuf + wave * (kBatch * kSlotBytes);
 
   float acc[WPC][NB];
 #pragma unroll
@@ -202,10 +233,14 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   }
   // Pad the last batch with entries that read an all-zero bitmap (in the
   // bitmap array's zeroed tail) and no values: they decode to nothing.
-  if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1)))
-  {
+  // The dummy batch is all such entries; stages past the last batch load it.
+  if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1))) {
     ent_l[n_act + lane] = make_uint4(0u, a.zero_col, 0u, 0u);
     col_l[n_act + lane] = a.zero_col;
+  }
+  if (lane < kBatch) {
+    ent_l[kDummyBatch * kBatch + lane] = make_uint4(0u, a.zero_col, 0u, 0u);
+    col_l[kDummyBatch * kBatch + lane] = a.zero_col;
   }
 
   // ---- 2. pipeline over batches of kBatch active columns: while batch i is
@@ -215,107 +250,148 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int q = lane & 31;
   const unsigned char* bitmap_bytes = reinterpret_cast<const unsigned char*>(a.bitmap);
 
-  auto issue = [&](int i, unsigned char* val_buf, unsigned char* bm_buf) {
-    uint4 e[kBatch / 2];
+  // A stage holds one batch in registers. Values: lane l of load pr has 16
+  // bytes of column 2pr + (l >= 32), chunk l & 31; lanes past a column's end
+  // re-read its first chunk (same cache line) and what they leave in the
+  // slot is never read. Bitmaps: lane l reads dword l % (2 WPC) of column
+  // (l / (2 WPC)) % 8; the data is unused (the decode reads the words with
+  // scalar loads) but the load brings the lines into L2 three batches ahead
+  // of those scalar loads, and it is waited for with the values. A stage past the last
+  // batch loads the dummy batch: every lane reads the same 16 bytes of values
+  // and one all-zero bitmap, so every stage issues the same loads and the
+  // in-order wait counts release exactly the oldest stage.
+  static_assert(kBatch == 8, "a stage is four 16-byte loads per lane");
+  static_assert(kBatch * 2 * WPC <= 64, "a batch's bitmap words fit one dword per lane");
+  const uint32_t bm_lane_off = (uint32_t)(lane % (2 * WPC)) * 4u;
+  const int bm_col = (lane / (2 * WPC)) & (kBatch - 1);
+#define SPDP_LOAD(E, V) V = *reinterpret_cast<const uint4*>(a.values + (size_t)(E).x + 8 * (q < (int)(E).z ? q : 0))
+#define SPDP_ISSUE(I, V)                                                                          \
+  do {                                                                                            \
+    const int bi_ = (I) < n_batches ? (I) : kDummyBatch;                                          \
+    const uint4 e0_ = ent_l[bi_ * kBatch + 0 + hsel];                                             \
+    const uint4 e1_ = ent_l[bi_ * kBatch + 2 + hsel];                                             \
+    const uint4 e2_ = ent_l[bi_ * kBatch + 4 + hsel];                                             \
+    const uint4 e3_ = ent_l[bi_ * kBatch + 6 + hsel];                                             \
+    const uint32_t bcol_ = col_l[bi_ * kBatch + bm_col];                                          \
+    SPDP_LOAD(e0_, V##0);                                                                         \
+    SPDP_LOAD(e1_, V##1);                                                                         \
+    SPDP_LOAD(e2_, V##2);                                                                         \
+    SPDP_LOAD(e3_, V##3);                                                                         \
+    V##b = *reinterpret_cast<const uint32_t*>(bitmap_bytes + (size_t)bcol_ * WPC * 8 + bm_lane_off); \
+  } while (0)
+#define SPDP_TO_LDS(V, BM)                                                                           \
+  do {                                                                                            \
+    *reinterpret_cast<uint4*>(my_val + 0 * kSlotBytes + 16 * lane) = V##0;                        \
+    *reinterpret_cast<uint4*>(my_val + 2 * kSlotBytes + 16 * lane) = V##1;                        \
+    *reinterpret_cast<uint4*>(my_val + 4 * kSlotBytes + 16 * lane) = V##2;                        \
+    *reinterpret_cast<uint4*>(my_val + 6 * kSlotBytes + 16 * lane) = V##3;                        \
+    BM = V##b;                                                                                    \
+  } while (0)
+
+  // Decode of batch i: its values are in the wave's LDS slots. The column
+  // indices move from LDS to scalar registers and the bitmap words come with
+  // scalar loads (their lines were pulled into L2 with the batch's values),
+  // so the words serve directly as MaskedPopcount masks and EXEC masks.
+  auto decode_quad = [&](int i, int u0, uint32_t bm) {
+    uint64_t words[kQuad][WPC];
 #pragma unroll
-    for (int pr = 0; pr < kBatch / 2; ++pr) e[pr] = ent_l[i * kBatch + 2 * pr + hsel];
-    const uint4 eb = ent_l[i * kBatch + ((lane >> 1) & (kBatch - 1))];
-    // values: lanes 0-31 fetch column 2pr, lanes 32-63 column 2pr+1, 16 B per
-    // lane; lanes past the column's end re-read its first chunk (same cache
-    // line) and what they leave in the slot is never read
+    for (int c = 0; c < kQuad; ++c)
 #pragma unroll
-    for (int pr = 0; pr < kBatch / 2; ++pr) {
-      const int chunk = q < (int)e[pr].z ? q : 0;
-      lds_dma16(a.values + (size_t)e[pr].x + 8 * chunk, val_buf + 2 * pr * kSlotBytes);
+      for (int w = 0; w < WPC; ++w) {
+        const int l = (u0 + c) * 2 * WPC + 2 * w;
+        words[c][w] = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)bm, l) |
+                      ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)bm, l + 1) << 32);
+      }
+    // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
+    // below the lane plus the popcounts of the column's earlier words
+    uint32_t vb[kQuad][WPC];
+#pragma unroll
+    for (int c = 0; c < kQuad; ++c) {
+      const uint16_t* slot = reinterpret_cast<const uint16_t*>(my_val + (u0 + c) * kSlotBytes);
+      uint32_t prefix = 0;
+#pragma unroll
+      for (int w = 0; w < WPC; ++w) {
+        vb[c][w] = slot[prefix + mbcnt64(words[c][w])];
+        prefix += (uint32_t)__builtin_popcountll(words[c][w]);
+      }
     }
-    // bitmaps: lanes 2u and 2u+1 fetch the first and second 16 B of column u
-    // (columns with fewer than 4 words read into the next column or the
-    // arrays' tail padding; those words are never used)
-    if (lane < 2 * kBatch) lds_dma16(bitmap_bytes + (size_t)eb.y * WPC * 8 + 16 * (lane & 1), bm_buf);
-  };
-
-  // The decode reads each quad's column indices from LDS, moves them to
-  // scalar registers and loads the columns' bitmap words with scalar loads:
-  // the words then serve directly as MaskedPopcount masks and EXEC masks.
-  // (The LDS-DMA of the bitmaps above only pulls their lines into L2 ahead of
-  // these loads.)
-  const_ptr<uint64_t> bitmap_c = as_const(a.bitmap);
-
-  auto decode = [&](int i, const unsigned char* val_buf) {
-    const int n_here = min(kBatch, n_act - i * kBatch);
-    for (int u0 = 0; u0 < n_here; u0 += kQuad) {
-      const uint4 cq = *reinterpret_cast<const uint4*>(&col_l[i * kBatch + u0]);
-      const uint32_t cols[kQuad] = {(uint32_t)__builtin_amdgcn_readfirstlane(cq.x),
-                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.y),
-                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.z),
-                                    (uint32_t)__builtin_amdgcn_readfirstlane(cq.w)};
-      uint64_t words[kQuad][WPC];
+    // 4. accumulate where the bitmap bit is set: for one token the words
+    // become EXEC around single FMAs (no branch, no select); for more tokens
+    // the compiler's FMA-plus-select on the word is used
+    const int xrow = (i * kBatch + u0) * NB;
 #pragma unroll
-      for (int c = 0; c < kQuad; ++c) {
-        const_ptr<uint64_t> bm = bitmap_c + (size_t)cols[c] * WPC;
+    for (int c = 0; c < kQuad; ++c) {
+      if constexpr (NB == 1) {
+        masked_fma_column<WPC>(acc, vb[c], (uint32_t)xs_l[xrow + c], words[c]);
+      } else {
+        float xv[NB];
 #pragma unroll
-        for (int w = 0; w < WPC; ++w) words[c][w] = bm[w];
-      }
-      float xv[kQuad][NB];
+        for (int b = 0; b < NB; ++b) xv[b] = half_bits_to_float(xs_l[xrow + c * NB + b]);
 #pragma unroll
-      for (int c = 0; c < kQuad; ++c)
-#pragma unroll
-        for (int b = 0; b < NB; ++b) xv[c][b] = half_bits_to_float(xs_l[(i * kBatch + u0 + c) * NB + b]);
-      // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
-      // below the lane, plus the popcounts of the column's earlier words
-      uint32_t vb[kQuad][WPC];
-#pragma unroll
-      for (int c = 0; c < kQuad; ++c) {
-        const uint16_t* slot = reinterpret_cast<const uint16_t*>(val_buf + (u0 + c) * kSlotBytes);
-        uint32_t prefix = 0;
-#pragma unroll
-        for (int w = 0; w < WPC; ++w) {
-          vb[c][w] = slot[prefix + mbcnt64(words[c][w])];
-          prefix += (uint32_t)__builtin_popcountll(words[c][w]);
-        }
-      }
-      // 4. accumulate where the bitmap bit is set (the word is the lane mask;
-      // the compiler turns this into an FMA plus a select on it, which
-      // measures faster than branching on EXEC)
-#pragma unroll
-      for (int c = 0; c < kQuad; ++c)
-#pragma unroll
-        for (int w = 0; w < WPC; ++w) {
+        for (int w = 0; w < WPC; ++w)
           if (__builtin_amdgcn_inverse_ballot_w64(words[c][w])) {
             const float v = half_bits_to_float(vb[c][w]);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[c][b], acc[w][b]);
+            for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[b], acc[w][b]);
           }
-        }
+      }
     }
   };
+  // A batch is two quads; the second one of a batch with at most four real
+  // columns reads only padding entries (all-zero words) and is skipped.
+  static_assert(kBatch == 2 * kQuad, "a batch is two quads");
+  auto decode = [&](int i, uint32_t bm) {
+    decode_quad(i, 0, bm);
+    if (n_act - i * kBatch > kQuad) decode_quad(i, kQuad, bm);
+  };
 
-  // Two-stage ping-pong: buffer 0 holds even batches, buffer 1 odd ones.
-  if (n_batches > 0) issue(0, my_val0, my_bm0);
-  for (int i = 0; i < n_batches; i += 2) {
-    if (i + 1 < n_batches) {
-      issue(i + 1, my_val1, my_bm1);
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kLoadsPerBatch));
-    } else {
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  // kDepth batches in flight: a stage holds batch i while batches i+1 and
+  // i+2 stream; a batch moves to LDS right before its decode. The loop has a
+  // single exit and every path through it issues the same loads, so the
+  // waits at its head count exactly one stage.
+  static_assert(kDepth == 3, "the loop below is unrolled for three stages");
+  if (n_batches > 0) {
+    uint4 s00, s01, s02, s03, s10, s11, s12, s13, s20, s21, s22, s23;
+    uint32_t s0b, s1b, s2b, bm;
+    // the stages must be issued in order (the waits count loads in order), so
+    // the scheduler may not interleave them
+    SPDP_ISSUE(0, s0);
+    __builtin_amdgcn_sched_barrier(0);
+    SPDP_ISSUE(1, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    SPDP_ISSUE(2, s2);
+    __builtin_amdgcn_sched_barrier(0);
+    for (int i = 0; i < n_batches; i += kDepth) {
+      SPDP_TO_LDS(s0, bm);
+      SPDP_ISSUE(i + 3, s0);
+      __builtin_amdgcn_sched_barrier(0);
+      decode(i, bm);
+      SPDP_TO_LDS(s1, bm);
+      SPDP_ISSUE(i + 4, s1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + 1 < n_batches) decode(i + 1, bm);
+      SPDP_TO_LDS(s2, bm);
+      SPDP_ISSUE(i + 5, s2);
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + 2 < n_batches) decode(i + 2, bm);
     }
-    __builtin_amdgcn_wave_barrier();
-    decode(i, my_val0);
-    if (i + 1 >= n_batches) break;
-    if (i + 2 < n_batches) {
-      issue(i + 2, my_val0, my_bm0);
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kLoadsPerBatch));
-    } else {
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-    }
-    __builtin_amdgcn_wave_barrier();
-    decode(i + 1, my_val1);
   }
+#undef SPDP_LOAD
+#undef SPDP_ISSUE
+#undef SPDP_TO_LDS
 
-  // ---- 5. reduce the 4 waves in LDS, write this segment's partial sums
-  const int mpad = a.n_stripes * a.tile_m;
-  float* red = reinterpret_cast<float*>(val0);
+  // ---- 5. reduce the 4 waves in LDS; segments other than the last publish
+  // their partial sums, the last one keeps its own in registers
+  const_ptr<KernelArgs> ka = reload_args<KernelArgs>();
+  const int mpad = ka->n_stripes * ka->tile_m;
+  const int n_seg = ka->segments;
+  const int nb = ka->batch;
+  const uint32_t epoch = ka->epoch;
+  const bool reducer = seg == n_seg - 1;
+  const int row = threadIdx.x;
+  float* red = reinterpret_cast<float*>(valbuf);
   constexpr int kSlice = Smem<NB>::kSlice;
+  float own[NB];
 #pragma unroll
   for (int b0 = 0; b0 < NB; b0 += kSlice) {
     __syncthreads();
@@ -324,64 +400,80 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 #pragma unroll
       for (int bb = 0; bb < kSlice; ++bb) red[(wave * kSlice + bb) * 256 + 64 * w + lane] = acc[w][b0 + bb];
     __syncthreads();
-    const int row = threadIdx.x;
-    if (row < 64 * WPC) {
 #pragma unroll
-      for (int bb = 0; bb < kSlice; ++bb) {
-        const int b = b0 + bb;
-        if (b < a.batch) {
-          float s = 0.0f;
+    for (int bb = 0; bb < kSlice; ++bb) {
+      float s = 0.0f;
+      if (row < 64 * WPC) {
 #pragma unroll
-          for (int wv = 0; wv < kWaves; ++wv) s += red[(wv * kSlice + bb) * 256 + row];
-          // device-coherent store: read back below by whichever workgroup
-          // of this stripe arrives last, possibly on another XCD
-          __hip_atomic_store(&a.partials[((size_t)seg * a.batch + b) * mpad + (size_t)r * a.tile_m + row],
-                             s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
+        for (int wv = 0; wv < kWaves; ++wv) s += red[(wv * kSlice + bb) * 256 + row];
       }
+      own[b0 + bb] = s;
     }
   }
-
-  // ---- split-K completion. The partial stores above bypass the per-XCD L2
-  // (device-scope atomics), so waiting for their completion before counting
-  // in publishes them without an L2-wide write-back; the last workgroup reads
-  // them with device-scope loads.
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0);
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(&a.counters[r], 1u, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (prev == (uint32_t)(a.segments - 1));
+  if (!reducer) {
+    if (row < 64 * WPC) {
+      unsigned long long* dst = ka->partials + (size_t)seg * nb * mpad + (size_t)r * ka->tile_m + row;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+        if (b < nb)
+          // device-coherent 8-byte store: value and tag land together, read
+          // by the stripe's last segment, possibly on another XCD
+          __hip_atomic_store(dst + (size_t)b * mpad,
+                             ((unsigned long long)epoch << 32) | __float_as_uint(own[b]),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    return;
   }
-  __syncthreads();
-  if (!s_last) return;
-  const int row = threadIdx.x;
-  const int m = r * a.tile_m + row;
-  if (row < 64 * WPC && m < a.rows) {
-    // All segments' partials of a token are requested before any is added, so
-    // the reduction costs one memory round trip per kFinal segments, and the
-    // sum runs in segment order (deterministic).
-    constexpr int kFinal = 32;
-    for (int b = 0; b < a.batch; ++b) {
+
+  // ---- the stripe's last segment: gather, add in segment order, write Y.
+  // A token's partials (kFinal at a time) are all requested before any is
+  // checked; those not yet tagged with this call's epoch are requested again
+  // until they are. The workgroups of lower segments of the stripe were
+  // dispatched before this one, so the wait ends; a bound on the rounds
+  // still makes every wave exit (the rows then read NaN).
+  const int m = r * ka->tile_m + row;
+  if (row < 64 * WPC && m < ka->rows) {
+    constexpr int kFinal = 16;
+    constexpr int kMaxRounds = 1 << 22;
+    const unsigned long long* src = ka->partials + m;
+    uint16_t* yout = ka->y + m;
+    const int rows = ka->rows;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (b >= nb) continue;
       float s = 0.0f;
-      for (int sg0 = 0; sg0 < a.segments; sg0 += kFinal) {
-        float v[kFinal];
+      bool lost = false;
+      for (int sg0 = 0; sg0 < n_seg - 1; sg0 += kFinal) {
+        unsigned long long v[kFinal];
 #pragma unroll
         for (int j = 0; j < kFinal; ++j) {
-          const int sg = min(sg0 + j, a.segments - 1);
-          v[j] = __hip_atomic_load(&a.partials[((size_t)sg * a.batch + b) * mpad + m], __ATOMIC_RELAXED,
+          const int sg = min(sg0 + j, n_seg - 2);
+          v[j] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
                                    __HIP_MEMORY_SCOPE_AGENT);
+        }
+        for (int round = 0;; ++round) {
+          bool ready = true;
+#pragma unroll
+          for (int j = 0; j < kFinal; ++j)
+            if (sg0 + j < n_seg - 1 && (uint32_t)(v[j] >> 32) != epoch) {
+              ready = false;
+              v[j] = __hip_atomic_load(src + ((size_t)(sg0 + j) * nb + b) * mpad, __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+            }
+          if (ready) break;
+          if (round >= kMaxRounds) {
+            lost = true;
+            break;
+          }
         }
 #pragma unroll
         for (int j = 0; j < kFinal; ++j)
-          if (sg0 + j < a.segments) s += v[j];
+          if (sg0 + j < n_seg - 1) s += __uint_as_float((uint32_t)v[j]);
       }
-      a.y[(size_t)b * a.rows + m] = __half_as_ushort(__float2half_rn(s));
+      s += own[b];
+      yout[(size_t)b * rows] = lost ? (uint16_t)0x7E00u : __half_as_ushort(__float2half_rn(s));
     }
   }
-  if (threadIdx.x == 0) __hip_atomic_store(&a.counters[r], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 using spdp::fail;
@@ -410,8 +502,11 @@ void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   *segments = (int)((cols + wc * kWaves - 1) / (wc * kWaves));
 }
 
+// The workspace holds {fp32, epoch} pairs for all segments but the last; it
+// starts zeroed, and epochs count from 1, so nothing in it matches a call
+// before that call has written it.
 int ensure_workspace(spdp_matrix* m, int batch, int segments) {
-  const size_t need = (size_t)segments * batch * m->n_stripes * m->tile_m;
+  const size_t need = std::max<size_t>(1, (size_t)(segments - 1) * batch * m->n_stripes * m->tile_m);
   if (need <= m->partial_floats) return SPDP_OK;
   if (m->d_partials) {
     hipError_t e = hipDeviceSynchronize();
@@ -420,12 +515,16 @@ int ensure_workspace(spdp_matrix* m, int batch, int segments) {
     m->d_partials = nullptr;
     m->partial_floats = 0;
   }
-  hipError_t e = hipMalloc(&m->d_partials, need * sizeof(float));
+  hipError_t e = hipMalloc(&m->d_partials, need * sizeof(unsigned long long));
   if (e != hipSuccess) {
     m->d_partials = nullptr;
     return e == hipErrorOutOfMemory ? fail(SPDP_ERR_OOM, "hipMalloc of the split-K workspace failed")
                                     : hip_fail(e, "hipMalloc");
   }
+  e = hipMemset(m->d_partials, 0, need * sizeof(unsigned long long));
+  if (e != hipSuccess) return hip_fail(e, "hipMemset");
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
   m->partial_floats = need;
   return SPDP_OK;
 }
@@ -436,13 +535,11 @@ void release_device(spdp_matrix* m) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
-  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values,
-                  m->d_partials, m->d_counters};
+  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_partials};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   m->d_tile_offset = m->d_col_info = m->d_bitmap = m->d_values = nullptr;
   m->d_partials = nullptr;
-  m->d_counters = nullptr;
   m->partial_floats = 0;
   if (prev >= 0) (void)hipSetDevice(prev);
 }
@@ -514,16 +611,6 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
   if (st == SPDP_OK) st = upload(m->bitmap, &m->d_bitmap);
   if (st == SPDP_OK) st = upload(m->values, &m->d_values);
   if (st == SPDP_OK) {
-    e = hipMalloc(&m->d_counters, (size_t)m->n_stripes * sizeof(uint32_t));
-    if (e != hipSuccess) {
-      m->d_counters = nullptr;
-      st = hip_fail(e, "hipMalloc");
-    } else {
-      e = hipMemset(m->d_counters, 0, (size_t)m->n_stripes * sizeof(uint32_t));
-      if (e != hipSuccess) st = hip_fail(e, "hipMemset");
-    }
-  }
-  if (st == SPDP_OK) {
     int segments = 1, wave_cols = 16;
     choose_split(m, &segments, &wave_cols);
     st = ensure_workspace(m, 1, segments);
@@ -584,8 +671,16 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float thresho
   args.values = static_cast<const uint16_t*>(h->d_values);
   args.x = X;
   args.y = Y;
+  // Epoch 0 never tags a call; on wrap-around the workspace is zeroed again
+  // (in stream order) so that no stale pair can match.
+  if (++h->epoch == 0) {
+    e = hipMemsetAsync(h->d_partials, 0, h->partial_floats * sizeof(unsigned long long),
+                       static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
+    h->epoch = 1;
+  }
   args.partials = h->d_partials;
-  args.counters = h->d_counters;
+  args.epoch = h->epoch;
   args.rows = (int)h->rows;
   args.cols = (int)h->cols;
   args.tile_m = h->tile_m;
