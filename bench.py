@@ -7,12 +7,18 @@ calls (3 x 3 points x 4 projections), each on its own encoded copy; copies
 rotate between steps so that every call streams from HBM rather than from
 the 256 MB Infinity Cache.
 
+By default each step is replayed as one captured HIP graph of its calls (the
+way a decode loop issues them; the kernel keeps no host-side state between
+calls, so replays are exact); --launch stream issues one host launch per call
+instead, and the JSON line reports that rate too.
+
 Prints one JSON line. ``value`` is the whole step's algorithmic bytes over its
 time (GB/s). Algorithmic bytes per call = for every row stripe and every
 column active for some token: ColInfo (4 B) + bitmap (tile_m/8 B) + padded
 values (2 B x pad8(nnz)); + 4 B per touched GTile (TileOffset); + x and y.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                       [--launch graph|stream]
 """
 
 from __future__ import annotations
@@ -50,6 +56,9 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device-to-device copy of this many MiB "
                          "(a known-size reference for hardware byte counters)")
+    ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
+                    help="graph: each step is one captured HIP graph of its calls (how a decode "
+                         "loop runs them); stream: one host launch per call")
     return ap.parse_args()
 
 
@@ -197,21 +206,51 @@ def main():
     prep_s = time.perf_counter() - t_prep
     stream = torch.cuda.current_stream(dev)
 
-    def step(i):
-        c = i % n_copies
-        for j, pt in enumerate(points):
-            copies[c][j].spmspv_into(X[c][j], pt["t"], Y[c][j], stream)
+    def launch_calls(c, idx):
+        for j in idx:
+            copies[c][j].spmspv_into(X[c][j], points[j]["t"], Y[c][j])
 
+    all_idx = list(range(len(points)))
+    graphs = {}
+
+    def capture(key, c, idx):
+        # capture on a side stream; replays go to the current stream
+        s = torch.cuda.Stream(device=dev)
+        s.wait_stream(torch.cuda.current_stream(dev))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            launch_calls(c, idx)
+        torch.cuda.current_stream(dev).wait_stream(s)
+        graphs[key] = g
+
+    def step(i, mode):
+        c = i % n_copies
+        if mode == "graph":
+            graphs[("step", c)].replay()
+        else:
+            launch_calls(c, all_idx)
+
+    def timed(fn, n):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(n):
+            fn(i)
+        e1.record(stream)
+        torch.cuda.synchronize(dev)
+        return e0.elapsed_time(e1)
+
+    # warm up eagerly (first calls load code, size workspaces), then capture
+    for i in range(max(1, args.warmup)):
+        step(i, "stream")
+    torch.cuda.synchronize(dev)
+    if args.launch == "graph":
+        for c in range(n_copies):
+            capture(("step", c), c, all_idx)
+        torch.cuda.synchronize(dev)
     for i in range(args.warmup):
-        step(i)
+        step(i, args.launch)
     torch.cuda.synchronize(dev)
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i)
-    ev1.record(stream)
-    torch.cuda.synchronize(dev)
-    total_ms = ev0.elapsed_time(ev1)
+    total_ms = timed(lambda i: step(args.warmup + i, args.launch), args.steps)
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20)
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
@@ -221,7 +260,7 @@ def main():
         torch.cuda.synchronize(dev)
         del src, dst
     if args.profile_only:
-        print(json.dumps({"profile_only": True, "ms_per_step": total_ms / args.steps,
+        print(json.dumps({"profile_only": True, "launch": args.launch, "ms_per_step": total_ms / args.steps,
                           "launches": (args.warmup + args.steps) * len(points),
                           "algorithmic_bytes_per_launch": sum(pt["bytes"] for pt in points) / len(points)}),
               flush=True)
@@ -229,26 +268,45 @@ def main():
     ms_per_step = total_ms / args.steps
     step_bytes = sum(pt["bytes"] for pt in points)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    # the same steps with one host launch per call, for comparison
+    stream_ms = timed(lambda i: step(args.warmup + i, "stream"), args.steps) / args.steps
 
-    # ---- kernel duration per sweep point: launches run back to back on one
-    # stream (no gaps between kernels), so HIP events around a run of
-    # launches divided by their number give the kernels' average duration;
-    # an event pair around every single launch would add its own overhead.
+    # ---- duration per sweep point: the point's calls run back to back (as a
+    # captured graph in graph mode), so HIP events around a run of them
+    # divided by their number give the kernels' average duration; an event
+    # pair around every single launch would add its own overhead.
     n_proj = len(wl["projections"])
     reps = max(2, min(10, args.steps))
     per_call = np.zeros(len(points))
     for k in range(0, len(points), n_proj):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for rep in range(reps):
-            c = rep % n_copies
-            for j in range(k, k + n_proj):
-                copies[c][j].spmspv_into(X[c][j], points[j]["t"], Y[c][j], stream)
-        e1.record(stream)
-        torch.cuda.synchronize(dev)
-        per_call[k:k + n_proj] = e0.elapsed_time(e1) / (reps * n_proj)
+        idx = list(range(k, k + n_proj))
+        if args.launch == "graph":
+            for c in range(n_copies):
+                capture(("pt", k, c), c, idx)
+            ms = timed(lambda r: graphs[("pt", k, r % n_copies)].replay(), reps)
+        else:
+            ms = timed(lambda r: launch_calls(r % n_copies, idx), reps)
+        per_call[k:k + n_proj] = ms / (reps * n_proj)
     kern_ms = ms_per_step
     achieved = step_bytes / (kern_ms * 1e-3) / 1e9
+    graphs.clear()
+
+    # ---- measured streaming peaks on this GPU: a 1 GiB device copy (read +
+    # write bytes) and a 1 GiB read-only reduction
+    n_pk = 1 << 30
+    a_pk = torch.empty(n_pk // 2, dtype=torch.float16, device=dev).fill_(1.0)
+    b_pk = torch.empty_like(a_pk)
+    for _ in range(2):
+        b_pk.copy_(a_pk)
+        a_pk.sum(dtype=torch.float32)
+    torch.cuda.synchronize(dev)
+    copy_ms = timed(lambda i: b_pk.copy_(a_pk), 5) / 5
+    read_ms = timed(lambda i: a_pk.sum(dtype=torch.float32), 5) / 5
+    peaks = {"copy_gbs": round(2 * n_pk / (copy_ms * 1e-3) / 1e9, 1),
+             "read_gbs": round(n_pk / (read_ms * 1e-3) / 1e9, 1),
+             "how": "torch copy_ of 1 GiB fp16 (read + write bytes) and torch sum of 1 GiB fp16 (read bytes), "
+                    "mean of 5 after 2 warm-ups"}
+    del a_pk, b_pk
 
     # ---- dense fp16 GEMV baseline (torch F.linear), rotated the same way
     dense = None
@@ -264,21 +322,35 @@ def main():
                 dW[(c, proj.name)] = torch.from_numpy(w16.view(np.int16)).view(torch.float16).to(dev)
         dX = {n: torch.from_numpy(xs[n].view(np.int16)).view(torch.float16).to(dev) for n in names}
 
-        def dstep(i):
-            c = i % n_dc
+        def dcalls(c):
             for n in names:
                 F.linear(dX[n], dW[(c, n)])
+
+        for c in range(n_dc):
+            dcalls(c)
+        torch.cuda.synchronize(dev)
+        dgraphs = []
+        if args.launch == "graph":
+            for c in range(n_dc):
+                s_cap = torch.cuda.Stream(device=dev)
+                s_cap.wait_stream(torch.cuda.current_stream(dev))
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=s_cap):
+                    dcalls(c)
+                torch.cuda.current_stream(dev).wait_stream(s_cap)
+                dgraphs.append(g)
+
+        def dstep(i):
+            if dgraphs:
+                dgraphs[i % n_dc].replay()
+            else:
+                dcalls(i % n_dc)
 
         for i in range(args.warmup):
             dstep(i)
         torch.cuda.synchronize(dev)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for i in range(args.steps):
-            dstep(i)
-        e1.record(stream)
-        torch.cuda.synchronize(dev)
-        d_us = e0.elapsed_time(e1) * 1e3 / (args.steps * len(names))
+        d_us = timed(dstep, args.steps) * 1e3 / (args.steps * len(names))
+        del dgraphs
         dense = {"us_per_call": d_us,
                  "gbs": (w_bytes / len(names) + 2 * batch * (wl["projections"][0].rows + wl["projections"][0].cols)) / (d_us * 1e-6) / 1e9}
         del dW
@@ -303,6 +375,7 @@ def main():
 
     traffic = read_traffic(args.workload)
     us_per_call = ms_per_step * 1e3 / len(points)
+    kernel_us = kern_ms * 1e3 / len(points)
     out = {
         "metric": "spMspV us/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
         "value": round(value, 2),
@@ -325,19 +398,24 @@ def main():
             "rotation_copies": n_copies, "accumulate": "f32",
         },
         "us_per_call": round(us_per_call, 3),
+        "us_per_call_stream_launch": round(stream_ms * 1e3 / len(points), 3),
+        "launch": args.launch,
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "measured_peaks": peaks,
+        "pct_of_measured_read_peak": round(100 * value / peaks["read_gbs"], 2),
         "roofline": {
             "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": traffic,
             "kernel": "spmspv_kernel",
-            "kernel_us_per_launch": round(kern_ms * 1e3 / len(points), 3),
-            "duration_source": "HIP events around the timed steps (back-to-back launches on one stream)",
+            "kernel_us_per_launch": round(kernel_us, 3),
+            "duration_source": "HIP events around the timed steps on the launch stream "
+                               f"({'captured graph per step' if args.launch == 'graph' else 'back-to-back launches'})",
             "algorithmic_bytes_per_launch": int(step_bytes / len(points)),
         },
         "cpu_baseline": cpu,
         "dense_gemv": dense,
-        "speedup_vs_dense": round(dense["us_per_call"] / (kern_ms * 1e3 / len(points)), 3) if dense else None,
+        "speedup_vs_dense": round(dense["us_per_call"] / kernel_us, 3) if dense else None,
         "points": pts_out,
         "prep_s": round(prep_s, 2),
         "encode_s_per_matrix": round(enc_s, 4),

@@ -25,11 +25,12 @@ struct spdp_matrix {
   void* d_bitmap = nullptr;
   void* d_values = nullptr;
 
-  // Split-K workspace: {fp32 partial sum, epoch} pairs
-  // [segments - 1][batch][n_stripes*tile_m], and the epoch of the last call.
+  // Split-K workspace: {fp32 partial sum, phase} pairs
+  // [segments - 1][batch][n_stripes*tile_m], and each row stripe's phase
+  // (advanced on the device by every call).
   unsigned long long* d_partials = nullptr;
   size_t partial_floats = 0;  // capacity in pairs
-  uint32_t epoch = 0;
+  uint32_t* d_phase = nullptr;
 };
 
 namespace spdp {

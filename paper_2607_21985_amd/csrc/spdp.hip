@@ -25,11 +25,13 @@
 //   5. split-K (Sec. 4.2.3): the workgroups of a row stripe cover disjoint K
 //      segments; each reduces its 4 waves in LDS. Every segment but the last
 //      stores its fp32 partial sums to a workspace, each value paired with
-//      the call's epoch number in one 8-byte store; the last segment's
+//      the stripe's phase number in one 8-byte store; the last segment's
 //      workgroup loads the other segments' partials until every one carries
-//      the current epoch, adds them in segment order (its own last) and
-//      writes fp16 Y (round to nearest even). No counter, no fence: a
-//      partial is usable as soon as its own store has landed.
+//      the current phase, adds them in segment order (its own last), writes
+//      fp16 Y (round to nearest even) and advances the stripe's phase for
+//      the next call. No counter, no fence, no host-side state: a partial
+//      is usable as soon as its own store has landed, and a captured graph
+//      replays correctly.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -50,7 +52,7 @@ constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one s
 constexpr int kBatch = 8;                 // active columns per pipeline stage of a wave
 constexpr int kQuad = 4;                  // columns decoded together
 constexpr int kMaxWaveCols = 128;         // columns of one wave's K range
-constexpr int kDepth = 3;                 // batches whose values are in flight per wave
+constexpr int kDepth = 2;                 // batches whose values are in flight per wave
 constexpr int kMaxBatch = 32;
 constexpr int kDummyBatch = kMaxWaveCols / kBatch;  // LDS batch of all-zero entries
 
@@ -61,9 +63,9 @@ struct KernelArgs {
   const uint16_t* values;
   const uint16_t* x;
   uint16_t* y;
-  // [segments - 1][batch][n_stripes * tile_m]: {fp32 bits, epoch} pairs
+  // [segments - 1][batch][n_stripes * tile_m]: {fp32 bits, phase} pairs
   unsigned long long* partials;
-  uint32_t epoch;      // this call's tag, never 0 (the workspace starts zeroed)
+  uint32_t* phase;     // [n_stripes], never 0 (the workspace starts zeroed)
   int rows, cols;
   int tile_m, tk_log2, n_colblocks, n_stripes;
   int batch;
@@ -159,11 +161,10 @@ template <int NB, int WPC>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char valbuf[kValBufBytes];
   // one entry per active column, in activity order: {value base, column
-  // index into ColInfo/bitmap, 16-byte chunks of values, unused}; batch
+  // index into ColInfo/bitmap << 6 | 16-byte chunks of values}; batch
   // kDummyBatch holds entries that load nothing of use (see below)
-  __shared__ uint4 ent_s[kWaves][kMaxWaveCols + kBatch];
+  __shared__ uint2 ent_s[kWaves][kMaxWaveCols + kBatch];
   __shared__ uint16_t xs_s[kWaves][kMaxWaveCols * NB];
-  __shared__ __attribute__((aligned(16))) uint32_t col_s[kWaves][kMaxWaveCols + kBatch];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
@@ -173,9 +174,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int tk_mask = (1 << a.tk_log2) - 1;
   const int g_row = r * a.n_colblocks;
 
-  uint4* ent_l = ent_s[wave];
+  uint2* ent_l = ent_s[wave];
   uint16_t* xs_l = xs_s[wave];
-  uint32_t* col_l = col_s[wave];
   unsigned char* my_val = valbuf + wave * (kBatch * kSlotBytes);
 
   float acc[WPC][NB];
@@ -184,6 +184,9 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
 
+  // the stripe's phase: written by the previous call's last segment, read
+  // by every workgroup of the stripe before any of them publishes
+  const uint32_t phase = ((const_ptr<uint32_t>)a.phase)[r];
   const int k_begin = (seg * kWaves + wave) * a.wave_cols;
   const int range = max(0, min(a.wave_cols, a.cols - k_begin));
 
@@ -224,8 +227,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     }
     if ((act >> lane) & 1) {
       const int pos = n_act + (int)mbcnt64(act);
-      ent_l[pos] = make_uint4(to[c] + (ci[c] >> 16), colx[c], ((ci[c] & 0xFFFFu) + 7u) >> 3, 0u);
-      col_l[pos] = colx[c];
+      ent_l[pos] = make_uint2(to[c] + (ci[c] >> 16), (colx[c] << 6) | (((ci[c] & 0xFFFFu) + 7u) >> 3));
 #pragma unroll
       for (int b = 0; b < NB; ++b) xs_l[pos * NB + b] = on[b] ? (uint16_t)xb[c][b] : (uint16_t)0;
     }
@@ -235,12 +237,10 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   // bitmap array's zeroed tail) and no values: they decode to nothing.
   // The dummy batch is all such entries; stages past the last batch load it.
   if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1))) {
-    ent_l[n_act + lane] = make_uint4(0u, a.zero_col, 0u, 0u);
-    col_l[n_act + lane] = a.zero_col;
+    ent_l[n_act + lane] = make_uint2(0u, a.zero_col << 6);
   }
   if (lane < kBatch) {
-    ent_l[kDummyBatch * kBatch + lane] = make_uint4(0u, a.zero_col, 0u, 0u);
-    col_l[kDummyBatch * kBatch + lane] = a.zero_col;
+    ent_l[kDummyBatch * kBatch + lane] = make_uint2(0u, a.zero_col << 6);
   }
 
   // ---- 2. pipeline over batches of kBatch active columns: while batch i is
@@ -264,15 +264,15 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   static_assert(kBatch * 2 * WPC <= 64, "a batch's bitmap words fit one dword per lane");
   const uint32_t bm_lane_off = (uint32_t)(lane % (2 * WPC)) * 4u;
   const int bm_col = (lane / (2 * WPC)) & (kBatch - 1);
-#define SPDP_LOAD(E, V) V = *reinterpret_cast<const uint4*>(a.values + (size_t)(E).x + 8 * (q < (int)(E).z ? q : 0))
+#define SPDP_LOAD(E, V) V = *reinterpret_cast<const uint4*>(a.values + (size_t)(E).x + 8 * (q < (int)((E).y & 63u) ? q : 0))
 #define SPDP_ISSUE(I, V)                                                                          \
   do {                                                                                            \
     const int bi_ = (I) < n_batches ? (I) : kDummyBatch;                                          \
-    const uint4 e0_ = ent_l[bi_ * kBatch + 0 + hsel];                                             \
-    const uint4 e1_ = ent_l[bi_ * kBatch + 2 + hsel];                                             \
-    const uint4 e2_ = ent_l[bi_ * kBatch + 4 + hsel];                                             \
-    const uint4 e3_ = ent_l[bi_ * kBatch + 6 + hsel];                                             \
-    const uint32_t bcol_ = col_l[bi_ * kBatch + bm_col];                                          \
+    const uint2 e0_ = ent_l[bi_ * kBatch + 0 + hsel];                                             \
+    const uint2 e1_ = ent_l[bi_ * kBatch + 2 + hsel];                                             \
+    const uint2 e2_ = ent_l[bi_ * kBatch + 4 + hsel];                                             \
+    const uint2 e3_ = ent_l[bi_ * kBatch + 6 + hsel];                                             \
+    const uint32_t bcol_ = ent_l[bi_ * kBatch + bm_col].y >> 6;                                   \
     SPDP_LOAD(e0_, V##0);                                                                         \
     SPDP_LOAD(e1_, V##1);                                                                         \
     SPDP_LOAD(e2_, V##2);                                                                         \
@@ -345,35 +345,50 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     if (n_act - i * kBatch > kQuad) decode_quad(i, kQuad, bm);
   };
 
-  // kDepth batches in flight: a stage holds batch i while batches i+1 and
-  // i+2 stream; a batch moves to LDS right before its decode. The loop has a
-  // single exit and every path through it issues the same loads, so the
-  // waits at its head count exactly one stage.
-  static_assert(kDepth == 3, "the loop below is unrolled for three stages");
+  // kDepth batches in flight: a stage holds batch i while the next kDepth-1
+  // batches stream; a batch moves to LDS right before its decode. The loop has
+  // a single exit and every path through it issues the same loads, so the
+  // waits at its head count exactly one stage. The stages must be issued in
+  // order (the waits count loads in order), so the scheduler may not
+  // interleave them.
+  static_assert(kDepth == 2 || kDepth == 3, "the loop below is unrolled for two or three stages");
   if (n_batches > 0) {
-    uint4 s00, s01, s02, s03, s10, s11, s12, s13, s20, s21, s22, s23;
-    uint32_t s0b, s1b, s2b, bm;
-    // the stages must be issued in order (the waits count loads in order), so
-    // the scheduler may not interleave them
+    uint4 s00, s01, s02, s03, s10, s11, s12, s13;
+    uint32_t s0b, s1b, bm;
     SPDP_ISSUE(0, s0);
     __builtin_amdgcn_sched_barrier(0);
     SPDP_ISSUE(1, s1);
     __builtin_amdgcn_sched_barrier(0);
-    SPDP_ISSUE(2, s2);
-    __builtin_amdgcn_sched_barrier(0);
-    for (int i = 0; i < n_batches; i += kDepth) {
-      SPDP_TO_LDS(s0, bm);
-      SPDP_ISSUE(i + 3, s0);
+    if constexpr (kDepth == 2) {
+      for (int i = 0; i < n_batches; i += 2) {
+        SPDP_TO_LDS(s0, bm);
+        SPDP_ISSUE(i + 2, s0);
+        __builtin_amdgcn_sched_barrier(0);
+        decode(i, bm);
+        SPDP_TO_LDS(s1, bm);
+        SPDP_ISSUE(i + 3, s1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (i + 1 < n_batches) decode(i + 1, bm);
+      }
+    } else {
+      uint4 s20, s21, s22, s23;
+      uint32_t s2b;
+      SPDP_ISSUE(2, s2);
       __builtin_amdgcn_sched_barrier(0);
-      decode(i, bm);
-      SPDP_TO_LDS(s1, bm);
-      SPDP_ISSUE(i + 4, s1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (i + 1 < n_batches) decode(i + 1, bm);
-      SPDP_TO_LDS(s2, bm);
-      SPDP_ISSUE(i + 5, s2);
-      __builtin_amdgcn_sched_barrier(0);
-      if (i + 2 < n_batches) decode(i + 2, bm);
+      for (int i = 0; i < n_batches; i += 3) {
+        SPDP_TO_LDS(s0, bm);
+        SPDP_ISSUE(i + 3, s0);
+        __builtin_amdgcn_sched_barrier(0);
+        decode(i, bm);
+        SPDP_TO_LDS(s1, bm);
+        SPDP_ISSUE(i + 4, s1);
+        __builtin_amdgcn_sched_barrier(0);
+        if (i + 1 < n_batches) decode(i + 1, bm);
+        SPDP_TO_LDS(s2, bm);
+        SPDP_ISSUE(i + 5, s2);
+        __builtin_amdgcn_sched_barrier(0);
+        if (i + 2 < n_batches) decode(i + 2, bm);
+      }
     }
   }
 #undef SPDP_LOAD
@@ -386,7 +401,6 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int mpad = ka->n_stripes * ka->tile_m;
   const int n_seg = ka->segments;
   const int nb = ka->batch;
-  const uint32_t epoch = ka->epoch;
   const bool reducer = seg == n_seg - 1;
   const int row = threadIdx.x;
   float* red = reinterpret_cast<float*>(valbuf);
@@ -419,7 +433,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
           // device-coherent 8-byte store: value and tag land together, read
           // by the stripe's last segment, possibly on another XCD
           __hip_atomic_store(dst + (size_t)b * mpad,
-                             ((unsigned long long)epoch << 32) | __float_as_uint(own[b]),
+                             ((unsigned long long)phase << 32) | __float_as_uint(own[b]),
                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     return;
@@ -427,13 +441,13 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 
   // ---- the stripe's last segment: gather, add in segment order, write Y.
   // A token's partials (kFinal at a time) are all requested before any is
-  // checked; those not yet tagged with this call's epoch are requested again
+  // checked; those not yet tagged with this call's phase are requested again
   // until they are. The workgroups of lower segments of the stripe were
   // dispatched before this one, so the wait ends; a bound on the rounds
   // still makes every wave exit (the rows then read NaN).
   const int m = r * ka->tile_m + row;
   if (row < 64 * WPC && m < ka->rows) {
-    constexpr int kFinal = 16;
+    constexpr int kFinal = 12;
     constexpr int kMaxRounds = 1 << 22;
     const unsigned long long* src = ka->partials + m;
     uint16_t* yout = ka->y + m;
@@ -441,24 +455,22 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       if (b >= nb) continue;
+      auto part = [&](int sg) {
+        return __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      };
       float s = 0.0f;
       bool lost = false;
       for (int sg0 = 0; sg0 < n_seg - 1; sg0 += kFinal) {
         unsigned long long v[kFinal];
 #pragma unroll
-        for (int j = 0; j < kFinal; ++j) {
-          const int sg = min(sg0 + j, n_seg - 2);
-          v[j] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
-                                   __HIP_MEMORY_SCOPE_AGENT);
-        }
+        for (int j = 0; j < kFinal; ++j) v[j] = part(min(sg0 + j, n_seg - 2));
         for (int round = 0;; ++round) {
           bool ready = true;
 #pragma unroll
           for (int j = 0; j < kFinal; ++j)
-            if (sg0 + j < n_seg - 1 && (uint32_t)(v[j] >> 32) != epoch) {
+            if (sg0 + j < n_seg - 1 && (uint32_t)(v[j] >> 32) != phase) {
               ready = false;
-              v[j] = __hip_atomic_load(src + ((size_t)(sg0 + j) * nb + b) * mpad, __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT);
+              v[j] = part(sg0 + j);
             }
           if (ready) break;
           if (round >= kMaxRounds) {
@@ -474,6 +486,9 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       yout[(size_t)b * rows] = lost ? (uint16_t)0x7E00u : __half_as_ushort(__float2half_rn(s));
     }
   }
+  // every partial of this call has been read: the next call uses a new tag
+  // (0 is skipped, the workspace's initial contents)
+  if (threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
 }
 
 using spdp::fail;
@@ -502,8 +517,8 @@ void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   *segments = (int)((cols + wc * kWaves - 1) / (wc * kWaves));
 }
 
-// The workspace holds {fp32, epoch} pairs for all segments but the last; it
-// starts zeroed, and epochs count from 1, so nothing in it matches a call
+// The workspace holds {fp32, phase} pairs for all segments but the last; it
+// starts zeroed and phases are never 0, so nothing in it matches a call
 // before that call has written it.
 int ensure_workspace(spdp_matrix* m, int batch, int segments) {
   const size_t need = std::max<size_t>(1, (size_t)(segments - 1) * batch * m->n_stripes * m->tile_m);
@@ -535,11 +550,12 @@ void release_device(spdp_matrix* m) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
-  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_partials};
+  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_partials, m->d_phase};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   m->d_tile_offset = m->d_col_info = m->d_bitmap = m->d_values = nullptr;
   m->d_partials = nullptr;
+  m->d_phase = nullptr;
   m->partial_floats = 0;
   if (prev >= 0) (void)hipSetDevice(prev);
 }
@@ -599,6 +615,12 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
     delete m;
     return st;
   }
+  // the kernel packs a GTile column index (the all-zero padding column
+  // included) into 26 bits
+  if (m->n_gtiles * m->tile_k + 1 >= (int64_t(1) << 26)) {
+    delete m;
+    return fail(SPDP_ERR_UNSUPPORTED, "more than 2^26 - 2 GTile columns (row stripes x padded columns)");
+  }
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) {
@@ -610,6 +632,18 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
   if (st == SPDP_OK) st = upload(m->col_info, &m->d_col_info);
   if (st == SPDP_OK) st = upload(m->bitmap, &m->d_bitmap);
   if (st == SPDP_OK) st = upload(m->values, &m->d_values);
+  if (st == SPDP_OK) {
+    // every stripe starts in phase 1
+    std::vector<uint32_t> ones((size_t)m->n_stripes, 1u);
+    e = hipMalloc(&m->d_phase, ones.size() * sizeof(uint32_t));
+    if (e != hipSuccess) {
+      m->d_phase = nullptr;
+      st = hip_fail(e, "hipMalloc");
+    } else {
+      e = hipMemcpy(m->d_phase, ones.data(), ones.size() * sizeof(uint32_t), hipMemcpyHostToDevice);
+      if (e != hipSuccess) st = hip_fail(e, "hipMemcpy");
+    }
+  }
   if (st == SPDP_OK) {
     int segments = 1, wave_cols = 16;
     choose_split(m, &segments, &wave_cols);
@@ -671,16 +705,8 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float thresho
   args.values = static_cast<const uint16_t*>(h->d_values);
   args.x = X;
   args.y = Y;
-  // Epoch 0 never tags a call; on wrap-around the workspace is zeroed again
-  // (in stream order) so that no stale pair can match.
-  if (++h->epoch == 0) {
-    e = hipMemsetAsync(h->d_partials, 0, h->partial_floats * sizeof(unsigned long long),
-                       static_cast<hipStream_t>(stream));
-    if (e != hipSuccess) return hip_fail(e, "hipMemsetAsync");
-    h->epoch = 1;
-  }
   args.partials = h->d_partials;
-  args.epoch = h->epoch;
+  args.phase = h->d_phase;
   args.rows = (int)h->rows;
   args.cols = (int)h->cols;
   args.tile_m = h->tile_m;

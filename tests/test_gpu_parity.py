@@ -178,7 +178,7 @@ def test_output_fully_overwritten_and_repeatable():
     w, x, t = _case(600, 1500, (256, 16), 0.5, 0.5, 4, 17, 18)
     m = spdp.encode(w, (256, 16))
     y1 = _run_gpu(m, x, t)
-    y2 = _run_gpu(m, x, t)  # second call: split-K counters were re-armed by the first
+    y2 = _run_gpu(m, x, t)  # second call: the stripes' phases were advanced by the first
     assert np.array_equal(y1, y2), "two identical calls differ"
     y64, s64, _ = oracle.spmspv(w, x, t)
     _assert_close(y1, y64, s64, "repeat")
@@ -190,6 +190,66 @@ def test_output_fully_overwritten_and_repeatable():
         y64, s64, _ = oracle.spmspv(w, xb, tb)
         _assert_close(yb, y64, s64, f"batch {b}")
     m.close()
+
+
+def test_alternating_batches_never_read_stale_partials(monkeypatch):
+    """Split-K partials from an older call with a larger batch stay in the
+    workspace; every later call must ignore them (they carry an old phase)."""
+    monkeypatch.setenv("SPDP_SPLITK", "5")
+    w = oracle.magnitude_prune(synth.weights(520, 2600, 61), 0.5)
+    m = spdp.encode(w, (256, 16))
+    m.reserve(8)
+    for i, b in enumerate((8, 1, 3, 1, 8, 2, 8)):
+        print(f"[gpu] alternating batch {i}: b={b}", flush=True)
+        xb = synth.laplace_activations(b, 2600, 300 + i)
+        tb = float(oracle.threshold_for(xb, 0.4))
+        yb = _run_gpu(m, xb, tb)
+        y64, s64, _ = oracle.spmspv(w, xb, tb)
+        _assert_close(yb, y64, s64, f"alternating batch {i} (b={b})")
+    m.close()
+
+
+def test_graph_replay_matches_eager():
+    """Calls captured in a HIP graph and replayed: no host-side state is baked
+    into the capture, so every replay (with other work and synchronizations
+    in between) gives the eager result."""
+    dev = _dev()
+    cases = [_case(900, 2100, (256, 16), 0.5, p, b, 71 + i, 81 + i) for i, (p, b) in enumerate([(0.5, 1), (0.0, 3)])]
+    mats = [spdp.encode(w, (256, 16)) for w, _, _ in cases]
+    for m, (_, x, _) in zip(mats, cases):
+        m.reserve(x.shape[0])
+    Xs = [_to_dev(x) for _, x, _ in cases]
+    Ys = [torch.zeros((x.shape[0], m.rows), dtype=torch.float16, device=dev) for (_, x, _), m in zip(cases, mats)]
+    eager = []
+    for m, X, Y, (_, _, t) in zip(mats, Xs, Ys, cases):
+        m.spmspv_into(X, t, Y)
+        eager.append(Y.clone())
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        for m, X, Y, (_, _, t) in zip(mats, Xs, Ys, cases):
+            m.spmspv_into(X, t, Y)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        print(f"[gpu] graph replay {rep}", flush=True)
+        for Y in Ys:
+            Y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (Y, E) in enumerate(zip(Ys, eager)):
+            assert torch.equal(Y, E), f"replay {rep}, call {i}: differs from the eager result"
+        # eager calls on the same handles between replays
+        for m, X, (_, _, t) in zip(mats, Xs, cases):
+            m(X, t)
+        torch.cuda.synchronize()
+    for (w, x, t), E in zip(cases, eager):
+        y64, s64, _ = oracle.spmspv(w, x, t)
+        _assert_close(E.cpu().numpy().astype(np.float64), y64, s64, "graph eager reference")
+    del g
+    for m in mats:
+        m.close()
 
 
 @pytest.mark.parametrize("splitk", ["1", "2", "3", "7", "64", "1000"])
