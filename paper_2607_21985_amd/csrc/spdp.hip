@@ -63,7 +63,7 @@ struct KernelArgs {
   const uint16_t* values;
   const uint16_t* x;
   uint16_t* y;
-  // [segments - 1][batch][n_stripes * tile_m]: {fp32 bits, phase} pairs
+  // [segments][batch][n_stripes * tile_m]: {fp32 bits, phase} pairs
   unsigned long long* partials;
   uint32_t* phase;     // [n_stripes], never 0 (the workspace starts zeroed)
   int rows, cols;
@@ -395,17 +395,18 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 #undef SPDP_ISSUE
 #undef SPDP_TO_LDS
 
-  // ---- 5. reduce the 4 waves in LDS; segments other than the last publish
-  // their partial sums, the last one keeps its own in registers
+  // ---- 5. reduce the 4 waves in LDS and publish this segment's partial
+  // sums: device-coherent 8-byte stores, so that value and tag land together
+  // and can be read from another XCD
   const_ptr<KernelArgs> ka = reload_args<KernelArgs>();
   const int mpad = ka->n_stripes * ka->tile_m;
   const int n_seg = ka->segments;
   const int nb = ka->batch;
-  const bool reducer = seg == n_seg - 1;
   const int row = threadIdx.x;
   float* red = reinterpret_cast<float*>(valbuf);
   constexpr int kSlice = Smem<NB>::kSlice;
-  float own[NB];
+  unsigned long long* dst = ka->partials + (size_t)seg * nb * mpad + (size_t)r * ka->tile_m + row;
+  const unsigned long long tag = (unsigned long long)phase << 32;
 #pragma unroll
   for (int b0 = 0; b0 < NB; b0 += kSlice) {
     __syncthreads();
@@ -416,79 +417,83 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     __syncthreads();
 #pragma unroll
     for (int bb = 0; bb < kSlice; ++bb) {
-      float s = 0.0f;
-      if (row < 64 * WPC) {
+      if (row < 64 * WPC && b0 + bb < nb) {
+        float s = 0.0f;
 #pragma unroll
         for (int wv = 0; wv < kWaves; ++wv) s += red[(wv * kSlice + bb) * 256 + row];
+        __hip_atomic_store(dst + (size_t)(b0 + bb) * mpad, tag | __float_as_uint(s), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
       }
-      own[b0 + bb] = s;
     }
-  }
-  if (!reducer) {
-    if (row < 64 * WPC) {
-      unsigned long long* dst = ka->partials + (size_t)seg * nb * mpad + (size_t)r * ka->tile_m + row;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-        if (b < nb)
-          // device-coherent 8-byte store: value and tag land together, read
-          // by the stripe's last segment, possibly on another XCD
-          __hip_atomic_store(dst + (size_t)b * mpad,
-                             ((unsigned long long)phase << 32) | __float_as_uint(own[b]),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
-    return;
   }
 
-  // ---- the stripe's last segment: gather, add in segment order, write Y.
-  // A token's partials (kFinal at a time) are all requested before any is
-  // checked; those not yet tagged with this call's phase are requested again
-  // until they are. The workgroups of lower segments of the stripe were
-  // dispatched before this one, so the wait ends; a bound on the rounds
-  // still makes every wave exit (the rows then read NaN).
-  const int m = r * ka->tile_m + row;
-  if (row < 64 * WPC && m < ka->rows) {
-    constexpr int kFinal = 12;
-    constexpr int kMaxRounds = 1 << 22;
-    const unsigned long long* src = ka->partials + m;
-    uint16_t* yout = ka->y + m;
-    const int rows = ka->rows;
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      if (b >= nb) continue;
-      auto part = [&](int sg) {
-        return __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      };
+  // ---- the stripe's last n_red segments gather: reducer j owns the 64-row
+  // blocks w = j, j + n_red, ...; its four waves split the segments (wave g
+  // takes segments g, g+4, ...), request all of a chunk of them at once,
+  // request again those not yet tagged with this call's phase, and add them
+  // in order; the four wave sums are added in wave order, so the result does
+  // not depend on timing. The workgroups of lower segments of the stripe were
+  // dispatched before these, so the wait ends; a bound on the rounds still
+  // makes every wave exit (the rows then read NaN).
+  const int n_red = min(n_seg, WPC);
+  const int jr = seg - (n_seg - n_red);
+  if (jr < 0) return;
+  constexpr int kGather = 12;  // partials in flight per lane
+  constexpr int kMaxRounds = 1 << 22;
+  const int rows = ka->rows;
+  for (int w = jr; w < WPC; w += n_red) {
+    const int m = r * ka->tile_m + 64 * w + lane;
+    const bool live = m < rows;
+    const unsigned long long* src = ka->partials + (live ? m : 0);
+    for (int b = 0; b < nb; ++b) {
       float s = 0.0f;
-      bool lost = false;
-      for (int sg0 = 0; sg0 < n_seg - 1; sg0 += kFinal) {
-        unsigned long long v[kFinal];
+      if (live) {
+        bool lost = false;
+        for (int sg0 = wave; sg0 < n_seg; sg0 += kWaves * kGather) {
+          unsigned long long v[kGather];
 #pragma unroll
-        for (int j = 0; j < kFinal; ++j) v[j] = part(min(sg0 + j, n_seg - 2));
-        for (int round = 0;; ++round) {
-          bool ready = true;
-#pragma unroll
-          for (int j = 0; j < kFinal; ++j)
-            if (sg0 + j < n_seg - 1 && (uint32_t)(v[j] >> 32) != phase) {
-              ready = false;
-              v[j] = part(sg0 + j);
-            }
-          if (ready) break;
-          if (round >= kMaxRounds) {
-            lost = true;
-            break;
+          for (int q = 0; q < kGather; ++q) {
+            const int sg = min(sg0 + kWaves * q, n_seg - 1);
+            v[q] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
           }
-        }
+          for (int round = 0;; ++round) {
+            bool ready = true;
 #pragma unroll
-        for (int j = 0; j < kFinal; ++j)
-          if (sg0 + j < n_seg - 1) s += __uint_as_float((uint32_t)v[j]);
+            for (int q = 0; q < kGather; ++q) {
+              const int sg = sg0 + kWaves * q;
+              if (sg < n_seg && (uint32_t)(v[q] >> 32) != phase) {
+                ready = false;
+                v[q] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+              }
+            }
+            if (ready) break;
+            if (round >= kMaxRounds) {
+              lost = true;
+              break;
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < kGather; ++q)
+            if (sg0 + kWaves * q < n_seg) s += __uint_as_float((uint32_t)v[q]);
+        }
+        if (lost) s = __builtin_nanf("");
       }
-      s += own[b];
-      yout[(size_t)b * rows] = lost ? (uint16_t)0x7E00u : __half_as_ushort(__float2half_rn(s));
+      __syncthreads();
+      red[wave * 64 + lane] = s;
+      __syncthreads();
+      if (wave == 0 && live) {
+        const float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
+        ka->y[(size_t)b * rows + m] = __half_as_ushort(__float2half_rn(t));
+      }
     }
   }
-  // every partial of this call has been read: the next call uses a new tag
-  // (0 is skipped, the workspace's initial contents)
-  if (threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
+  // every workgroup of the stripe has published (so has read the phase) by
+  // the time a reducer gets here, and the next call starts after this kernel
+  // ends: advance the tag (0 is skipped, the workspace's initial contents).
+  // A reducer still gathering keeps its own copy of the phase.
+  if (jr == n_red - 1 && threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
 }
 
 using spdp::fail;
@@ -517,11 +522,11 @@ void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   *segments = (int)((cols + wc * kWaves - 1) / (wc * kWaves));
 }
 
-// The workspace holds {fp32, phase} pairs for all segments but the last; it
+// The workspace holds {fp32, phase} pairs for all segments; it
 // starts zeroed and phases are never 0, so nothing in it matches a call
 // before that call has written it.
 int ensure_workspace(spdp_matrix* m, int batch, int segments) {
-  const size_t need = std::max<size_t>(1, (size_t)(segments - 1) * batch * m->n_stripes * m->tile_m);
+  const size_t need = (size_t)segments * batch * m->n_stripes * m->tile_m;
   if (need <= m->partial_floats) return SPDP_OK;
   if (m->d_partials) {
     hipError_t e = hipDeviceSynchronize();
