@@ -101,48 +101,56 @@ template <class T>
 using const_ptr = const __attribute__((address_space(4))) T*;
 
 // One column of one token: acc[w] += f32(v[w]) * f32(x) in the lanes whose
-// bit is set in word w, where v[w] and x are fp16 bits. The whole column is
-// one block so that nothing else runs under the narrowed EXEC: save EXEC
-// while ANDing it with the first word, AND the saved mask with each later
-// word, restore at the end (one scalar instruction per word, no branch).
-template <int WPC>
-__device__ __forceinline__ void masked_fma_column(float (&acc)[WPC][1], const uint32_t (&v)[WPC],
-                                                  uint32_t x, const uint64_t (&m)[WPC]) {
-  uint64_t save;
-#define SPDP_FMA(W) "v_fma_mix_f32 %[a" #W "], %[v" #W "], %[x], %[a" #W "] op_sel_hi:[1,1,0]\n\t"
-  if constexpr (WPC == 1) {
-    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0) "s_mov_b64 exec, %[sv]"
-                 : [a0] "+v"(acc[0][0]), [sv] "=&s"(save)
-                 : [m0] "s"(m[0]), [v0] "v"(v[0]), [x] "v"(x)
-                 : "scc");
-  } else if constexpr (WPC == 2) {
-    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
-                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1) "s_mov_b64 exec, %[sv]"
-                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [sv] "=&s"(save)
-                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [v0] "v"(v[0]), [v1] "v"(v[1]), [x] "v"(x)
-                 : "scc");
-  } else if constexpr (WPC == 3) {
-    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
-                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1)
-                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2) "s_mov_b64 exec, %[sv]"
-                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]), [sv] "=&s"(save)
-                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [v0] "v"(v[0]), [v1] "v"(v[1]),
-                   [v2] "v"(v[2]), [x] "v"(x)
-                 : "scc");
-  } else {
-    static_assert(WPC == 4, "at most four bitmap words per column");
-    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0)
-                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1)
-                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2)
-                 "s_and_b64 exec, %[sv], %[m3]\n\t" SPDP_FMA(3) "s_mov_b64 exec, %[sv]"
-                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]),
-                   [a3] "+v"(acc[3][0]), [sv] "=&s"(save)
-                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [m3] "s"(m[3]), [v0] "v"(v[0]),
-                   [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [x] "v"(x)
-                 : "scc");
+// bit is set in word w, where v[w] is fp16 bits and x the low (XHI false) or
+// high (XHI true) fp16 half of xpair. The whole column is one block so that
+// nothing else runs under the narrowed EXEC: save EXEC while ANDing it with
+// the first word, AND the saved mask with each later word, restore at the end
+// (one scalar instruction per word, no branch).
+#define SPDP_FMA(W, SEL) "v_fma_mix_f32 %[a" #W "], %[v" #W "], %[x], %[a" #W "] " SEL "\n\t"
+#define SPDP_COLUMN(SEL)                                                                              \
+  if constexpr (WPC == 1) {                                                                           \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0, SEL) "s_mov_b64 exec, %[sv]"      \
+                 : [a0] "+v"(acc[0][0]), [sv] "=&s"(save)                                             \
+                 : [m0] "s"(m[0]), [v0] "v"(v[0]), [x] "v"(xpair)                                     \
+                 : "scc");                                                                            \
+  } else if constexpr (WPC == 2) {                                                                    \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0, SEL)                              \
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1, SEL) "s_mov_b64 exec, %[sv]"          \
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [sv] "=&s"(save)                       \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [v0] "v"(v[0]), [v1] "v"(v[1]), [x] "v"(xpair)     \
+                 : "scc");                                                                            \
+  } else if constexpr (WPC == 3) {                                                                    \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0, SEL)                              \
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1, SEL)                                  \
+                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2, SEL) "s_mov_b64 exec, %[sv]"          \
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]), [sv] "=&s"(save) \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [v0] "v"(v[0]), [v1] "v"(v[1]),    \
+                   [v2] "v"(v[2]), [x] "v"(xpair)                                                     \
+                 : "scc");                                                                            \
+  } else {                                                                                            \
+    static_assert(WPC == 4, "at most four bitmap words per column");                                  \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA(0, SEL)                              \
+                 "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA(1, SEL)                                  \
+                 "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA(2, SEL)                                  \
+                 "s_and_b64 exec, %[sv], %[m3]\n\t" SPDP_FMA(3, SEL) "s_mov_b64 exec, %[sv]"          \
+                 : [a0] "+v"(acc[0][0]), [a1] "+v"(acc[1][0]), [a2] "+v"(acc[2][0]),                  \
+                   [a3] "+v"(acc[3][0]), [sv] "=&s"(save)                                             \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [m3] "s"(m[3]), [v0] "v"(v[0]),    \
+                   [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [x] "v"(xpair)                     \
+                 : "scc");                                                                            \
   }
-#undef SPDP_FMA
+template <int WPC, bool XHI>
+__device__ __forceinline__ void masked_fma_column(float (&acc)[WPC][1], const uint32_t (&v)[WPC],
+                                                  uint32_t xpair, const uint64_t (&m)[WPC]) {
+  uint64_t save;
+  if constexpr (XHI) {
+    SPDP_COLUMN("op_sel:[0,1,0] op_sel_hi:[1,1,0]")
+  } else {
+    SPDP_COLUMN("op_sel_hi:[1,1,0]")
+  }
 }
+#undef SPDP_COLUMN
+#undef SPDP_FMA
 
 // The kernel's argument block, read again from the kernel-argument segment
 // through a pointer the compiler cannot see through: fields used only after
@@ -164,7 +172,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   // index into ColInfo/bitmap << 6 | 16-byte chunks of values}; batch
   // kDummyBatch holds entries that load nothing of use (see below)
   __shared__ uint2 ent_s[kWaves][kMaxWaveCols + kBatch];
-  __shared__ uint16_t xs_s[kWaves][kMaxWaveCols * NB];
+  __shared__ __attribute__((aligned(16))) uint16_t xs_s[kWaves][kMaxWaveCols * NB];
   __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
@@ -319,10 +327,17 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     // become EXEC around single FMAs (no branch, no select); for more tokens
     // the compiler's FMA-plus-select on the word is used
     const int xrow = (i * kBatch + u0) * NB;
+    // one token: the quad's four fp16 activations in one 8-byte LDS read
+    uint2 xq = make_uint2(0u, 0u);
+    if constexpr (NB == 1) xq = *reinterpret_cast<const uint2*>(&xs_l[xrow]);
 #pragma unroll
     for (int c = 0; c < kQuad; ++c) {
       if constexpr (NB == 1) {
-        masked_fma_column<WPC>(acc, vb[c], (uint32_t)xs_l[xrow + c], words[c]);
+        const uint32_t xpair = c < 2 ? xq.x : xq.y;
+        if (c & 1)
+          masked_fma_column<WPC, true>(acc, vb[c], xpair, words[c]);
+        else
+          masked_fma_column<WPC, false>(acc, vb[c], xpair, words[c]);
       } else {
         float xv[NB];
 #pragma unroll
