@@ -68,7 +68,7 @@ typedef struct spdp_matrix* spdp_handle_t;
  *
  * Device memory for the four arrays plus a small split-K workspace is
  * allocated on the current device and owned by the handle. Returns
- * SPDP_ERR_UNSUPPORTED if the format would hold 2^32 or more values, or if
+ * SPDP_ERR_UNSUPPORTED if the padded values would take 4 GiB or more, or if
  * R * C * tile_k (GTile columns, plus one) reaches 2^26.
  */
 int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,

@@ -168,9 +168,10 @@ __device__ __forceinline__ const_ptr<Args> reload_args() {
 template <int NB, int WPC>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char valbuf[kValBufBytes];
-  // one entry per active column, in activity order: {value base, column
-  // index into ColInfo/bitmap << 6 | 16-byte chunks of values}; batch
-  // kDummyBatch holds entries that load nothing of use (see below)
+  // one entry per active column, in activity order: {byte offset of the
+  // column's values, column index into ColInfo/bitmap << 6 | index of its
+  // last 16-byte chunk}; batch kDummyBatch holds entries that load nothing
+  // of use (see below)
   __shared__ uint2 ent_s[kWaves][kMaxWaveCols + kBatch];
   __shared__ __attribute__((aligned(16))) uint16_t xs_s[kWaves][kMaxWaveCols * NB];
   __shared__ int s_last;
@@ -235,7 +236,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     }
     if ((act >> lane) & 1) {
       const int pos = n_act + (int)mbcnt64(act);
-      ent_l[pos] = make_uint2(to[c] + (ci[c] >> 16), (colx[c] << 6) | (((ci[c] & 0xFFFFu) + 7u) >> 3));
+      const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
+      ent_l[pos] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
 #pragma unroll
       for (int b = 0; b < NB; ++b) xs_l[pos * NB + b] = on[b] ? (uint16_t)xb[c][b] : (uint16_t)0;
     }
@@ -256,23 +258,25 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int n_batches = (n_act + kBatch - 1) / kBatch;
   const int hsel = lane >> 5;
   const int q = lane & 31;
+  const unsigned char* value_bytes = reinterpret_cast<const unsigned char*>(a.values);
   const unsigned char* bitmap_bytes = reinterpret_cast<const unsigned char*>(a.bitmap);
 
   // A stage holds one batch in registers. Values: lane l of load pr has 16
   // bytes of column 2pr + (l >= 32), chunk l & 31; lanes past a column's end
-  // re-read its first chunk (same cache line) and what they leave in the
-  // slot is never read. Bitmaps: lane l reads dword l % (2 WPC) of column
-  // (l / (2 WPC)) % 8; the data is unused (the decode reads the words with
-  // scalar loads) but the load brings the lines into L2 three batches ahead
-  // of those scalar loads, and it is waited for with the values. A stage past the last
-  // batch loads the dummy batch: every lane reads the same 16 bytes of values
-  // and one all-zero bitmap, so every stage issues the same loads and the
-  // in-order wait counts release exactly the oldest stage.
+  // re-read its last chunk (a line the column loads anyway) and what they
+  // leave in the slot is never read. Bitmaps: lane l holds dword l % (2 WPC)
+  // of column (l / (2 WPC)) % 8, so the decode reads the batch's words out of
+  // that register. A stage past the last batch loads the dummy batch (all
+  // lanes read the same 16 bytes of values and an all-zero bitmap), so every
+  // stage issues the same loads and the in-order wait counts release exactly
+  // the oldest stage. Offsets are 32-bit from a wave-uniform base (the value
+  // and bitmap arrays stay below 4 GiB).
   static_assert(kBatch == 8, "a stage is four 16-byte loads per lane");
   static_assert(kBatch * 2 * WPC <= 64, "a batch's bitmap words fit one dword per lane");
   const uint32_t bm_lane_off = (uint32_t)(lane % (2 * WPC)) * 4u;
   const int bm_col = (lane / (2 * WPC)) & (kBatch - 1);
-#define SPDP_LOAD(E, V) V = *reinterpret_cast<const uint4*>(a.values + (size_t)(E).x + 8 * (q < (int)((E).y & 63u) ? q : 0))
+#define SPDP_LOAD(E, V) \
+  V = *reinterpret_cast<const uint4*>(value_bytes + ((E).x + (min((uint32_t)q, (E).y & 63u) << 4)))
 #define SPDP_ISSUE(I, V)                                                                          \
   do {                                                                                            \
     const int bi_ = (I) < n_batches ? (I) : kDummyBatch;                                          \
@@ -285,7 +289,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     SPDP_LOAD(e1_, V##1);                                                                         \
     SPDP_LOAD(e2_, V##2);                                                                         \
     SPDP_LOAD(e3_, V##3);                                                                         \
-    V##b = *reinterpret_cast<const uint32_t*>(bitmap_bytes + (size_t)bcol_ * WPC * 8 + bm_lane_off); \
+    V##b = *reinterpret_cast<const uint32_t*>(bitmap_bytes + (bcol_ * (WPC * 8u) + bm_lane_off)); \
   } while (0)
 #define SPDP_TO_LDS(V, BM)                                                                           \
   do {                                                                                            \
@@ -296,10 +300,10 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     BM = V##b;                                                                                    \
   } while (0)
 
-  // Decode of batch i: its values are in the wave's LDS slots. The column
-  // indices move from LDS to scalar registers and the bitmap words come with
-  // scalar loads (their lines were pulled into L2 with the batch's values),
-  // so the words serve directly as MaskedPopcount masks and EXEC masks.
+  // Decode of batch i: its values are in the wave's LDS slots and its bitmap
+  // words in bm (one dword per lane, see above): v_readlane moves them to
+  // scalar registers, where they serve directly as MaskedPopcount masks and
+  // EXEC masks.
   auto decode_quad = [&](int i, int u0, uint32_t bm) {
     uint64_t words[kQuad][WPC];
 #pragma unroll
@@ -636,10 +640,15 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
     return st;
   }
   // the kernel packs a GTile column index (the all-zero padding column
-  // included) into 26 bits
+  // included) into 26 bits and addresses values and bitmaps with 32-bit
+  // byte offsets
   if (m->n_gtiles * m->tile_k + 1 >= (int64_t(1) << 26)) {
     delete m;
     return fail(SPDP_ERR_UNSUPPORTED, "more than 2^26 - 2 GTile columns (row stripes x padded columns)");
+  }
+  if ((uint64_t)m->values.size() * 2 + kTailBytes >= (uint64_t(1) << 32)) {
+    delete m;
+    return fail(SPDP_ERR_UNSUPPORTED, "more than 4 GiB of padded values");
   }
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
