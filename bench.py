@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama7b-attn")
     ap.add_argument("--batch", type=int, default=None, help="override the workload's batch")
+    ap.add_argument("--sw", default=None, help="override the weight-sparsity sweep (comma list)")
+    ap.add_argument("--p", default=None, help="override the activation-sparsity sweep (comma list)")
     ap.add_argument("--rotation-mb", type=float, default=600.0,
                     help="minimum distinct encoded bytes between two uses of one copy")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -168,6 +170,10 @@ def main():
     wl = synth.workload(args.workload)
     tile = wl["tile"]
     batch = args.batch if args.batch is not None else wl["batch"][0]
+    if args.sw:
+        wl = dict(wl, weight_sparsity=[float(v) for v in args.sw.split(",")])
+    if args.p:
+        wl = dict(wl, act_sparsity=[float(v) for v in args.p.split(",")])
 
     # ---- inputs: prune (library host C++), calibrate, encode rotated copies
     t_prep = time.perf_counter()
@@ -377,7 +383,7 @@ def main():
     us_per_call = ms_per_step * 1e3 / len(points)
     kernel_us = kern_ms * 1e3 / len(points)
     out = {
-        "metric": "spMspV us/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
+        "metric": "spMspV \u00b5s/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,

@@ -304,7 +304,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   // words in bm (one dword per lane, see above): v_readlane moves them to
   // scalar registers, where they serve directly as MaskedPopcount masks and
   // EXEC masks.
-  auto decode_quad = [&](int i, int u0, uint32_t bm) {
+  auto decode_quad = [&](int i, int u0, uint32_t bm) __attribute__((always_inline)) {
     uint64_t words[kQuad][WPC];
 #pragma unroll
     for (int c = 0; c < kQuad; ++c)
@@ -359,7 +359,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   // A batch is two quads; the second one of a batch with at most four real
   // columns reads only padding entries (all-zero words) and is skipped.
   static_assert(kBatch == 2 * kQuad, "a batch is two quads");
-  auto decode = [&](int i, uint32_t bm) {
+  auto decode = [&](int i, uint32_t bm) __attribute__((always_inline)) {
     decode_quad(i, 0, bm);
     if (n_act - i * kBatch > kQuad) decode_quad(i, kQuad, bm);
   };
@@ -457,54 +457,69 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
   const int n_red = min(n_seg, WPC);
   const int jr = seg - (n_seg - n_red);
   if (jr < 0) return;
-  constexpr int kGather = 12;  // partials in flight per lane
+  // A round requests kJ of the wave's segments for every token at once
+  // (about kGather partials in flight per lane).
+  constexpr int kGather = 12;
+  constexpr int kJ = NB >= kGather ? 1 : kGather / NB;
   constexpr int kMaxRounds = 1 << 22;
   const int rows = ka->rows;
   for (int w = jr; w < WPC; w += n_red) {
     const int m = r * ka->tile_m + 64 * w + lane;
     const bool live = m < rows;
     const unsigned long long* src = ka->partials + (live ? m : 0);
-    for (int b = 0; b < nb; ++b) {
-      float s = 0.0f;
-      if (live) {
-        bool lost = false;
-        for (int sg0 = wave; sg0 < n_seg; sg0 += kWaves * kGather) {
-          unsigned long long v[kGather];
+    float sums[NB];
 #pragma unroll
-          for (int q = 0; q < kGather; ++q) {
-            const int sg = min(sg0 + kWaves * q, n_seg - 1);
-            v[q] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
-                                     __HIP_MEMORY_SCOPE_AGENT);
-          }
-          for (int round = 0;; ++round) {
-            bool ready = true;
+    for (int b = 0; b < NB; ++b) sums[b] = 0.0f;
+    if (live) {
+      bool lost = false;
+      auto part = [&](int sg, int b) {
+        return __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      };
+      // this wave's segments: wave, wave + 4, ...
+      for (int sg0 = wave; sg0 < n_seg; sg0 += kWaves * kJ) {
+        unsigned long long v[kJ][NB];
 #pragma unroll
-            for (int q = 0; q < kGather; ++q) {
-              const int sg = sg0 + kWaves * q;
-              if (sg < n_seg && (uint32_t)(v[q] >> 32) != phase) {
+        for (int jj = 0; jj < kJ; ++jj)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            if (b < nb) v[jj][b] = part(min(sg0 + kWaves * jj, n_seg - 1), b);
+        for (int round = 0;; ++round) {
+          bool ready = true;
+#pragma unroll
+          for (int jj = 0; jj < kJ; ++jj)
+#pragma unroll
+            for (int b = 0; b < NB; ++b)
+              if (b < nb && sg0 + kWaves * jj < n_seg && (uint32_t)(v[jj][b] >> 32) != phase) {
                 ready = false;
-                v[q] = __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
-                                         __HIP_MEMORY_SCOPE_AGENT);
+                v[jj][b] = part(sg0 + kWaves * jj, b);
               }
-            }
-            if (ready) break;
-            if (round >= kMaxRounds) {
-              lost = true;
-              break;
-            }
+          if (ready) break;
+          if (round >= kMaxRounds) {
+            lost = true;
+            break;
           }
-#pragma unroll
-          for (int q = 0; q < kGather; ++q)
-            if (sg0 + kWaves * q < n_seg) s += __uint_as_float((uint32_t)v[q]);
         }
-        if (lost) s = __builtin_nanf("");
+#pragma unroll
+        for (int jj = 0; jj < kJ; ++jj)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+            if (b < nb && sg0 + kWaves * jj < n_seg) sums[b] += __uint_as_float((uint32_t)v[jj][b]);
       }
-      __syncthreads();
-      red[wave * 64 + lane] = s;
-      __syncthreads();
-      if (wave == 0 && live) {
-        const float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
-        ka->y[(size_t)b * rows + m] = __half_as_ushort(__float2half_rn(t));
+      if (lost)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) sums[b] = __builtin_nanf("");
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      if (b < nb) {  // uniform over the workgroup
+        __syncthreads();
+        red[wave * 64 + lane] = sums[b];
+        __syncthreads();
+        if (wave == 0 && live) {
+          const float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
+          ka->y[(size_t)b * rows + m] = __half_as_ushort(__float2half_rn(t));
+        }
       }
     }
   }
