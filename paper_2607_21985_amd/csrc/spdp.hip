@@ -331,9 +331,14 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     // become EXEC around single FMAs (no branch, no select); for more tokens
     // the compiler's FMA-plus-select on the word is used
     const int xrow = (i * kBatch + u0) * NB;
-    // one token: the quad's four fp16 activations in one 8-byte LDS read
+    // one token: the group's fp16 activations in one LDS read
     uint2 xq = make_uint2(0u, 0u);
-    if constexpr (NB == 1) xq = *reinterpret_cast<const uint2*>(&xs_l[xrow]);
+    if constexpr (NB == 1) {
+      if constexpr (kQuad == 4)
+        xq = *reinterpret_cast<const uint2*>(&xs_l[xrow]);
+      else
+        xq.x = *reinterpret_cast<const uint32_t*>(&xs_l[xrow]);
+    }
 #pragma unroll
     for (int c = 0; c < kQuad; ++c) {
       if constexpr (NB == 1) {
@@ -356,12 +361,13 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       }
     }
   };
-  // A batch is two quads; the second one of a batch with at most four real
-  // columns reads only padding entries (all-zero words) and is skipped.
-  static_assert(kBatch == 2 * kQuad, "a batch is two quads");
+  // A batch is kBatch / kQuad groups; a group holding only padding entries
+  // (all-zero words) is skipped.
+  static_assert(kQuad == 2 || kQuad == 4, "columns are decoded in pairs or quads");
   auto decode = [&](int i, uint32_t bm) __attribute__((always_inline)) {
-    decode_quad(i, 0, bm);
-    if (n_act - i * kBatch > kQuad) decode_quad(i, kQuad, bm);
+#pragma unroll
+    for (int g = 0; g < kBatch / kQuad; ++g)
+      if (g == 0 || n_act - i * kBatch > g * kQuad) decode_quad(i, g * kQuad, bm);
   };
 
   // kDepth batches in flight: a stage holds batch i while the next kDepth-1
@@ -536,13 +542,18 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(SPDP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Split-K heuristic: about 2048 waves (8 per CU on 256 CUs), every wave
+// Split-K heuristic: about 7168 waves (one full load of the 256 CUs at seven
+// workgroups each, so that early finishers are replaced), at most kMaxSegments
+// segments per stripe (the gather then needs one round of loads), every wave
 // covering a multiple of 16 columns and at most kMaxWaveCols of them.
 // SPDP_SPLITK overrides the number of segments (for tuning).
+constexpr int64_t kTargetWaves = 7168;
+constexpr int64_t kMaxSegments = 48;
 void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   const int64_t cols = m->cols;
   const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
-  int64_t want = std::max<int64_t>(1, 2048 / (kWaves * stripes));
+  int64_t want = std::min<int64_t>(kMaxSegments,
+                                   std::max<int64_t>(1, (kTargetWaves + kWaves * stripes - 1) / (kWaves * stripes)));
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1) want = v;
