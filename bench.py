@@ -7,10 +7,13 @@ calls (3 x 3 points x 4 projections), each on its own encoded copy; copies
 rotate between steps so that every call streams from HBM rather than from
 the 256 MB Infinity Cache.
 
-By default each step is replayed as one captured HIP graph of its calls (the
-way a decode loop issues them; the kernel keeps no host-side state between
-calls, so replays are exact); --launch stream issues one host launch per call
-instead, and the JSON line reports that rate too.
+Calls are issued the way a decoder issues them: projections of one sweep
+point that read the same layer input (q, k and v; gate and up) go out as one
+grouped launch (spdp_spmspv_many), the others (o, down) as single launches;
+--group none issues every product as its own launch, and the JSON line
+reports that rate too. By default each step is replayed as one captured HIP
+graph of its launches (the kernel keeps no host-side state between calls, so
+replays are exact); --launch stream issues one host launch per call instead.
 
 Prints one JSON line. ``value`` is the whole step's algorithmic bytes over its
 time (GB/s). Algorithmic bytes per call = for every row stripe and every
@@ -58,6 +61,8 @@ def parse():
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after the timed steps, run one device-to-device copy of this many MiB "
                          "(a known-size reference for hardware byte counters)")
+    ap.add_argument("--group", choices=("decoder", "none"), default="decoder",
+                    help="decoder: products that read one input are one grouped launch; none: one launch each")
     ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
                     help="graph: each step is one captured HIP graph of its calls (how a decode "
                          "loop runs them); stream: one host launch per call")
@@ -94,10 +99,10 @@ def kernel_source_sha() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload: str):
+def read_traffic(workload: str, group: str):
     """HBM bytes per launch from committed rocprofv3 counter summaries, if they
-    were taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", f"traffic_spmspv_{workload}.txt")
+    were taken on the current kernel source and launch grouping; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_spmspv_{workload}_{group}.txt")
     if not os.path.exists(path):
         return None
     text = open(path).read()
@@ -202,8 +207,32 @@ def main():
         pt["bytes"], pt["active_frac"] = call_bytes(f, pt["x"], spdp.threshold_code(pt["t"]))
         pt["rows"], pt["cols"] = f["rows"], f["cols"]
         del f
-    X = [[torch.from_numpy(pt["x"].view(np.int16)).view(torch.float16).to(dev) for pt in points]
-         for _ in range(n_copies)]
+    # one device copy of each distinct input per rotation copy (grouped
+    # products share it, as a decoder's q, k and v share the layer input)
+    X = []
+    for _ in range(n_copies):
+        by_input = {}
+        row = []
+        for pt in points:
+            key = (pt["sw"], pt["p"], pt["proj"].x_seed, pt["proj"].x_kind, pt["proj"].cols)
+            if key not in by_input:
+                by_input[key] = torch.from_numpy(pt["x"].view(np.int16)).view(torch.float16).to(dev)
+            row.append(by_input[key])
+        X.append(row)
+
+    # launch units: the products of one sweep point that read one input form a
+    # group (at most 8), every other product is a unit of its own
+    def make_units(idx, grouped):
+        units, open_ = [], {}
+        for j in idx:
+            pt = points[j]
+            key = (pt["sw"], pt["p"], pt["proj"].x_seed, pt["proj"].x_kind, pt["proj"].cols)
+            if grouped and key in open_ and len(units[open_[key]]) < 8:
+                units[open_[key]].append(j)
+            else:
+                open_[key] = len(units)
+                units.append([j])
+        return units
     Y = [[torch.empty((batch, pt["rows"]), dtype=torch.float16, device=dev) for pt in points]
          for _ in range(n_copies)]
     for cp in copies:
@@ -212,11 +241,18 @@ def main():
     prep_s = time.perf_counter() - t_prep
     stream = torch.cuda.current_stream(dev)
 
-    def launch_calls(c, idx):
-        for j in idx:
-            copies[c][j].spmspv_into(X[c][j], points[j]["t"], Y[c][j])
+    def launch_calls(c, units):
+        for u in units:
+            if len(u) == 1:
+                copies[c][u[0]].spmspv_into(X[c][u[0]], points[u[0]]["t"], Y[c][u[0]])
+            else:
+                spdp.spmspv_many([copies[c][j] for j in u], [X[c][j] for j in u],
+                                 [points[j]["t"] for j in u], [Y[c][j] for j in u])
 
     all_idx = list(range(len(points)))
+    grouped = args.group == "decoder"
+    step_units = make_units(all_idx, grouped)
+    single_units = make_units(all_idx, False)
     graphs = {}
 
     def capture(key, c, idx):
@@ -229,12 +265,12 @@ def main():
         torch.cuda.current_stream(dev).wait_stream(s)
         graphs[key] = g
 
-    def step(i, mode):
+    def step(i, mode, key="step", units=None):
         c = i % n_copies
         if mode == "graph":
-            graphs[("step", c)].replay()
+            graphs[(key, c)].replay()
         else:
-            launch_calls(c, all_idx)
+            launch_calls(c, units if units is not None else step_units)
 
     def timed(fn, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -251,7 +287,8 @@ def main():
     torch.cuda.synchronize(dev)
     if args.launch == "graph":
         for c in range(n_copies):
-            capture(("step", c), c, all_idx)
+            capture(("step", c), c, step_units)
+            capture(("single", c), c, single_units)
         torch.cuda.synchronize(dev)
     for i in range(args.warmup):
         step(i, args.launch)
@@ -266,16 +303,20 @@ def main():
         torch.cuda.synchronize(dev)
         del src, dst
     if args.profile_only:
-        print(json.dumps({"profile_only": True, "launch": args.launch, "ms_per_step": total_ms / args.steps,
-                          "launches": (args.warmup + args.steps) * len(points),
-                          "algorithmic_bytes_per_launch": sum(pt["bytes"] for pt in points) / len(points)}),
+        print(json.dumps({"profile_only": True, "launch": args.launch, "group": args.group,
+                          "ms_per_step": total_ms / args.steps,
+                          "launches": (2 * args.warmup + args.steps) * len(step_units),
+                          "algorithmic_bytes_per_launch": sum(pt["bytes"] for pt in points) / len(step_units)}),
               flush=True)
         return
     ms_per_step = total_ms / args.steps
     step_bytes = sum(pt["bytes"] for pt in points)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    # the same steps with one host launch per call, for comparison
+    # the same steps with one host launch per call, and with every product
+    # as its own launch, for comparison
     stream_ms = timed(lambda i: step(args.warmup + i, "stream"), args.steps) / args.steps
+    single_ms = timed(lambda i: step(args.warmup + i, args.launch, "single", single_units),
+                      args.steps) / args.steps
 
     # ---- duration per sweep point: the point's calls run back to back (as a
     # captured graph in graph mode), so HIP events around a run of them
@@ -285,7 +326,7 @@ def main():
     reps = max(2, min(10, args.steps))
     per_call = np.zeros(len(points))
     for k in range(0, len(points), n_proj):
-        idx = list(range(k, k + n_proj))
+        idx = make_units(list(range(k, k + n_proj)), grouped)
         if args.launch == "graph":
             for c in range(n_copies):
                 capture(("pt", k, c), c, idx)
@@ -379,9 +420,10 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(points)
 
-    traffic = read_traffic(args.workload)
+    traffic = read_traffic(args.workload, args.group)
+    n_launch = len(step_units)
     us_per_call = ms_per_step * 1e3 / len(points)
-    kernel_us = kern_ms * 1e3 / len(points)
+    kernel_us = kern_ms * 1e3 / n_launch
     out = {
         "metric": "spMspV \u00b5s/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
         "value": round(value, 2),
@@ -401,9 +443,12 @@ def main():
             "projections": [proj.name for proj in wl["projections"]],
             "weight_sparsity": wl["weight_sparsity"], "act_sparsity": wl["act_sparsity"],
             "batch": batch, "tile": list(tile), "calls_per_step": len(points),
+            "launches_per_step": n_launch, "grouping": args.group,
             "rotation_copies": n_copies, "accumulate": "f32",
         },
         "us_per_call": round(us_per_call, 3),
+        "us_per_call_ungrouped": round(single_ms * 1e3 / len(points), 3),
+        "gbs_ungrouped": round(step_bytes / (single_ms * 1e-3) / 1e9, 2),
         "us_per_call_stream_launch": round(stream_ms * 1e3 / len(points), 3),
         "launch": args.launch,
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
@@ -417,11 +462,11 @@ def main():
             "kernel_us_per_launch": round(kernel_us, 3),
             "duration_source": "HIP events around the timed steps on the launch stream "
                                f"({'captured graph per step' if args.launch == 'graph' else 'back-to-back launches'})",
-            "algorithmic_bytes_per_launch": int(step_bytes / len(points)),
+            "algorithmic_bytes_per_launch": int(step_bytes / n_launch),
         },
         "cpu_baseline": cpu,
         "dense_gemv": dense,
-        "speedup_vs_dense": round(dense["us_per_call"] / kernel_us, 3) if dense else None,
+        "speedup_vs_dense": round(dense["us_per_call"] / us_per_call, 3) if dense else None,
         "points": pts_out,
         "prep_s": round(prep_s, 2),
         "encode_s_per_matrix": round(enc_s, 4),

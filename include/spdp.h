@@ -107,13 +107,41 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
                 float threshold, uint16_t* Y, void* stream);
 
+/*
+ * spdp_spmspv_many -- several independent products in one launch:
+ * Y[i] = W_i . mask(X[i]) with threshold thresholds[i], for i < count. This
+ * is how a decoder issues the projections that read the same layer input
+ * (q, k and v; gate and up), whose fixed per-launch latency would otherwise
+ * be paid once per matrix. Each product follows the rules of spdp_spmspv.
+ *
+ *   handles     count handles (device copies on the current device), all
+ *               with the same tile_m; no handle may appear twice (its
+ *               workspace serves one product at a time).
+ *   count       1 <= count <= 8.
+ *   X, Y        count device pointers each (X[i]: batch x cols_i, Y[i]:
+ *               batch x rows_i, 16-byte aligned). An output must not overlap
+ *               any input or any other output of the call; inputs may be
+ *               shared (q, k and v read one X).
+ *   batch       tokens of every product, 1 <= batch <= 32.
+ *   thresholds  count thresholds (host array).
+ *   stream      hipStream_t to enqueue on.
+ *
+ * Errors are those of spdp_spmspv plus SPDP_ERR_INVALID_ARG for a bad count,
+ * a repeated handle, mixed tile_m or overlapping outputs; on any error
+ * nothing is launched. spdp_spmspv(h, ...) is this call with count 1.
+ */
+int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count,
+                     const uint16_t* const* X, int32_t batch,
+                     const float* thresholds, uint16_t* const* Y, void* stream);
+
 /* spdp_reserve -- size the handle's workspace for batches up to max_batch. */
 int spdp_reserve(spdp_handle_t h, int32_t max_batch);
 
 /*
  * spdp_free -- release a handle. Waits for the device to finish work that
- * may still use it. spdp_free(NULL) does nothing. Using h afterwards is
- * undefined.
+ * may still use it (a device synchronization, so it must not run while a
+ * stream capture is in progress). spdp_free(NULL) does nothing. Using h
+ * afterwards is undefined.
  */
 void spdp_free(spdp_handle_t h);
 

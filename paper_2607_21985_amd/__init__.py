@@ -28,6 +28,7 @@ __all__ = [
     "lib_path",
     "encode",
     "encode_host",
+    "spmspv_many",
     "prune_magnitude",
     "calibrate_threshold",
     "threshold_code",
@@ -38,7 +39,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libspdp.so"
 
 EXPORTED_SYMBOLS = (
-    "spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_reserve", "spdp_free",
+    "spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_reserve", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
 )
@@ -93,6 +94,9 @@ def lib() -> ctypes.CDLL:
     L.spdp_encode.argtypes = [u16p, i64, i64, i32, i32, ctypes.POINTER(H)]
     L.spdp_encode_host.argtypes = [u16p, i64, i64, i32, i32, ctypes.POINTER(H)]
     L.spdp_spmspv.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    L.spdp_spmspv_many.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
+                                   ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_void_p),
+                                   ctypes.c_void_p]
     L.spdp_reserve.argtypes = [H, i32]
     L.spdp_free.argtypes = [H]
     L.spdp_free.restype = None
@@ -104,7 +108,8 @@ def lib() -> ctypes.CDLL:
     L.spdp_strerror.restype = ctypes.c_char_p
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = ctypes.c_char_p
-    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_reserve", "spdp_format",
+    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_reserve",
+                 "spdp_format",
                  "spdp_prune_magnitude", "spdp_calibrate_threshold", "spdp_threshold_code"):
         getattr(L, name).restype = ctypes.c_int
     _lib = L
@@ -196,15 +201,43 @@ class Matrix:
         return y
 
     def close(self) -> None:
+        """Free the handle (synchronizes the device; never while a stream capture runs)."""
         if getattr(self, "_h", None):
             lib().spdp_free(self._h)
             self._h = None
+        _free_deferred()
 
     def __del__(self):
+        # spdp_free synchronizes the device, which would invalidate a HIP
+        # graph capture in progress: a handle that becomes garbage during a
+        # capture is freed at the next close() or encode() instead.
         try:
-            self.close()
+            h = getattr(self, "_h", None)
+            if not h:
+                return
+            self._h = None
+            if _capturing():
+                _DEFERRED.append(h)
+            else:
+                lib().spdp_free(h)
         except Exception:
             pass
+
+
+_DEFERRED: list = []
+
+
+def _capturing() -> bool:
+    try:
+        import torch
+        return bool(torch.cuda.is_available() and torch.cuda.is_current_stream_capturing())
+    except Exception:
+        return False
+
+
+def _free_deferred() -> None:
+    while _DEFERRED and not _capturing():
+        lib().spdp_free(_DEFERRED.pop())
 
 
 def encode(w: np.ndarray, tile=(256, 16)) -> Matrix:
@@ -212,10 +245,41 @@ def encode(w: np.ndarray, tile=(256, 16)) -> Matrix:
     wb = _u16(w)
     if wb.ndim != 2:
         raise ValueError("w must be 2-D")
+    _free_deferred()
     h = ctypes.c_void_p()
     _check(lib().spdp_encode(_ptr(wb), wb.shape[0], wb.shape[1], int(tile[0]), int(tile[1]),
                              ctypes.byref(h)))
     return Matrix(h)
+
+
+def spmspv_many(mats, xs, thresholds, ys, stream=None) -> None:
+    """Enqueue ``ys[i] = W_i . mask(xs[i])`` for every i in one launch.
+
+    ``mats`` are encoded matrices with one tile height, ``xs``/``ys`` torch
+    fp16 device tensors ``[batch, cols_i]`` / ``[batch, rows_i]`` (one batch
+    for all), ``thresholds`` one float per product. Inputs may be shared.
+    """
+    import torch
+    n = len(mats)
+    if not (len(xs) == len(ys) == len(thresholds) == n):
+        raise ValueError("mats, xs, thresholds and ys must have one entry per product")
+    for m, x, y in zip(mats, xs, ys):
+        if x.dtype != torch.float16 or y.dtype != torch.float16:
+            raise TypeError("x and y must be torch.float16")
+        if x.dim() != 2 or x.shape[1] != m.cols or not x.is_contiguous():
+            raise ValueError(f"x must be a contiguous [batch, {m.cols}] tensor")
+        if tuple(y.shape) != (x.shape[0], m.rows) or not y.is_contiguous():
+            raise ValueError(f"y must be a contiguous [{x.shape[0]}, {m.rows}] tensor")
+        if x.shape[0] != xs[0].shape[0]:
+            raise ValueError("every product of one call takes the same batch")
+        if not (x.is_cuda and y.is_cuda):
+            raise ValueError("x and y must be device tensors")
+    s = stream if stream is not None else torch.cuda.current_stream(xs[0].device)
+    hs = (ctypes.c_void_p * n)(*[m._h for m in mats])
+    xp = (ctypes.c_void_p * n)(*[x.data_ptr() for x in xs])
+    yp = (ctypes.c_void_p * n)(*[y.data_ptr() for y in ys])
+    ts = (ctypes.c_float * n)(*[float(t) for t in thresholds])
+    _check(lib().spdp_spmspv_many(hs, n, xp, int(xs[0].shape[0]), ts, yp, ctypes.c_void_p(s.cuda_stream)))
 
 
 def encode_host(w: np.ndarray, tile=(256, 16)) -> Matrix:

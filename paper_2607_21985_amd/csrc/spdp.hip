@@ -2,36 +2,38 @@
 // kernel over Tiled-CBC weights (Sec. 4.2) and the C-ABI entry points that
 // own device memory.
 //
-// One launch per call does the whole path:
-//   1. activity: each wave reads its K range of the activations and takes
-//      the strict magnitude test |x| > t as an integer compare on fp16 bits;
-//      64-lane ballots (union over the batch) compact the active columns into
-//      a per-wave list in LDS (Sec. 4.2, XTile loading and the
-//      activation-aware selection of GTile loading);
-//   2. metadata then data (Sec. 4.2.2): ColInfo and TileOffset of the range
-//      arrive in the same round trip as the activations; the list then
-//      drives batches of 8 active columns whose padded values (16-byte vector
-//      loads, two columns per load instruction) and bitmap words stream into
-//      registers three batches ahead of the decode; a batch moves to LDS
-//      right before it is decoded;
-//   3. bitmap decode (HAD-SMBD, Sec. 4.2.1): lane i owns row 64w+i of bitmap
-//      word w; its value sits at the masked popcount of the word below bit i
-//      (v_mbcnt_lo/hi, the MaskedPopcount of the paper) plus the popcount of
-//      the earlier words, and the word itself (read out of the batch's
-//      registers with v_readlane) is the execution mask, so rows without a
-//      nonzero issue no LDS read and no FMA;
-//   4. accumulate in fp32 on the vector ALUs with fp16 operands (v_fma_mix),
-//      no matrix cores (Sec. 3.3 challenge 2, Sec. 4.2 step 5);
-//   5. split-K (Sec. 4.2.3): the workgroups of a row stripe cover disjoint K
-//      segments; each reduces its 4 waves in LDS. Every segment but the last
-//      stores its fp32 partial sums to a workspace, each value paired with
-//      the stripe's phase number in one 8-byte store; the last segment's
-//      workgroup loads the other segments' partials until every one carries
-//      the current phase, adds them in segment order (its own last), writes
-//      fp16 Y (round to nearest even) and advances the stripe's phase for
-//      the next call. No counter, no fence, no host-side state: a partial
-//      is usable as soon as its own store has landed, and a captured graph
-//      replays correctly.
+// One launch runs one or several independent products (a decoder's q, k and
+// v, or gate and up, read one input); each product is a grid row of
+// workgroups, one per (row stripe, K segment). A workgroup does the whole
+// path for its piece:
+//   1. activity: each wave reads a K range of the activations and takes the
+//      strict magnitude test |x| > t as an integer compare on fp16 bits;
+//      64-lane ballots (union over the batch) and mbcnt positions compact the
+//      workgroup's active columns into one list in LDS (Sec. 4.2, XTile
+//      loading and the activation-aware selection of GTile loading); ColInfo
+//      and TileOffset of the range arrive in the same round trip as the
+//      activations;
+//   2. data (Sec. 4.2.2, metadata first, data second): the list is cut into
+//      batches of four columns, spread evenly over the four waves; each wave
+//      streams its batches through a two-slot ring in LDS with global->LDS
+//      DMA (16-byte loads of the padded values, two columns per instruction,
+//      plus the batch's bitmap words), so loads in flight hold no registers;
+//   3. bitmap decode (HAD-SMBD, Sec. 4.2.1): the bitmap words come from
+//      scalar loads (their lines are in L2 once the batch's DMA has landed);
+//      lane i of word w reads its value at the word's masked popcount below
+//      bit i (v_mbcnt_lo/hi, the paper's MaskedPopcount) plus the popcount of
+//      the column's earlier words;
+//   4. accumulate in fp32 on the vector ALUs with fp16 operands (v_fma_mix
+//      under EXEC = the bitmap word: rows without a nonzero do nothing), no
+//      matrix cores (Sec. 3.3 challenge 2, Sec. 4.2 step 5);
+//   5. split-K (Sec. 4.2.3): each workgroup reduces its 4 waves in LDS and
+//      stores its fp32 partial sums to the product's workspace, each value
+//      paired with the stripe's phase number in one 8-byte store; the
+//      stripe's last segments gather the partials until every one carries
+//      the current phase, add them in a fixed order, write fp16 Y (round to
+//      nearest even) and advance the stripe's phase for the next call. No
+//      counter, no fence, no host-side state: a partial is usable as soon as
+//      its own store has landed, and a captured graph replays correctly.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
@@ -49,14 +51,18 @@ constexpr int kWaves = 4;                 // waves per workgroup
 constexpr int kThreads = 64 * kWaves;
 constexpr int kMaxWords = 4;              // tile_m <= 256: at most 4 bitmap words per column
 constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one stripe (fp16)
-constexpr int kBatch = 8;                 // active columns per pipeline stage of a wave
+constexpr int kBatch = 4;                 // active columns per DMA batch (one decode quad)
 constexpr int kQuad = 4;                  // columns decoded together
-constexpr int kMaxWaveCols = 128;         // columns of one wave's K range
-constexpr int kDepth = 2;                 // batches whose values are in flight per wave
+constexpr int kMaxWaveCols = 128;         // columns whose activity one wave tests
+constexpr int kMaxWgCols = kWaves * kMaxWaveCols;
 constexpr int kMaxBatch = 32;
-constexpr int kDummyBatch = kMaxWaveCols / kBatch;  // LDS batch of all-zero entries
+constexpr int kBmBytes = kBatch * kMaxWords * 8;          // bitmap words of one batch
+constexpr int kBatchBytes = kBatch * kSlotBytes + kBmBytes;  // one ring slot
+constexpr int kDmaPerBatch = kBatch / 2 + 1;  // 16-byte value loads (two columns each) + one bitmap load
 
-struct KernelArgs {
+// One product of a launch: the matrix's device arrays, the call's input and
+// output, and the matrix's split.
+struct MatArgs {
   const uint32_t* tile_offset;
   const uint32_t* col_info;
   const uint64_t* bitmap;
@@ -68,22 +74,32 @@ struct KernelArgs {
   uint32_t* phase;     // [n_stripes], never 0 (the workspace starts zeroed)
   int rows, cols;
   int tile_m, tk_log2, n_colblocks, n_stripes;
-  int batch;
   int code;       // threshold code: active iff code < (x & 0x7fff) <= 0x7c00
   int wave_cols;  // columns per wave (multiple of 16, <= kMaxWaveCols)
   int segments;   // workgroups per row stripe
+  int n_wg;       // segments * n_stripes
   uint32_t zero_col;  // column index whose bitmap lies in the zeroed tail padding
 };
 
-// LDS use: one value slot buffer per wave (the batch being decoded; the
-// batches in flight live in registers).
-constexpr int kValBufBytes = kWaves * kBatch * kSlotBytes;
+// A launch runs up to kMaxGroup independent products (same tile height and
+// batch): grid row y serves product y, its workgroup x being stripe
+// x / segments, segment x % segments (segments ascending within a stripe);
+// workgroups past the product's n_wg exit at once.
+constexpr int kMaxGroup = 8;
+struct LaunchArgs {
+  MatArgs m[kMaxGroup];
+  int batch;
+};
 
+// Per-wave ring of batch slots in LDS, filled by global->LDS DMA: deep enough
+// that at the Llama-7B shapes a wave's whole share is requested at once.
 template <int NB>
 struct Smem {
+  static constexpr int kSlots = 2;
+  static constexpr int kRingBytes = kWaves * kSlots * kBatchBytes;
   static constexpr int kSlice = NB < 4 ? NB : 4;  // tokens per cross-wave reduction pass
   static constexpr int kRed = kWaves * kSlice * 256 * 4;
-  static_assert(kRed <= kValBufBytes, "reduction reuses the value buffer");
+  static_assert(kRed <= kRingBytes, "reduction reuses the ring");
 };
 
 __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
@@ -91,14 +107,14 @@ __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  return __half2float(__ushort_as_half((unsigned short)h));
-}
-
 // Pointers into the constant address space: reads through them are scalar
 // loads.
 template <class T>
 using const_ptr = const __attribute__((address_space(4))) T*;
+
+__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
+  return __half2float(__ushort_as_half((unsigned short)h));
+}
 
 // One column of one token: acc[w] += f32(v[w]) * f32(x) in the lanes whose
 // bit is set in word w, where v[w] is fp16 bits and x the low (XHI false) or
@@ -163,29 +179,70 @@ __device__ __forceinline__ const_ptr<Args> reload_args() {
   return p;
 }
 
+// Global -> LDS DMA of 16 (or 4) bytes per lane from base + off: lane l's
+// bytes land at lds + 16 l (4 l); lanes outside EXEC write nothing. Issued
+// as assembly so that the compiler does not order every later LDS read
+// behind all outstanding DMA (the loads target ring slots that the reads
+// below do not touch); the waits for them are explicit.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// The compiler's hazard checks do not look inside inline assembly: a vector
+// memory instruction needs 5 wait states after a VALU instruction writes an
+// SGPR it reads (the compiler may have just restored the base pointer from a
+// VGPR lane with v_readlane) and 1 after an M0 write, so each load is
+// preceded by s_nop 4.
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+__device__ __forceinline__ void dma4(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
 // column (tile_m / 64).
 template <int NB, int WPC>
-__global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char valbuf[kValBufBytes];
-  // one entry per active column, in activity order: {byte offset of the
+__global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
+  using S = Smem<NB>;
+  constexpr int kSlots = S::kSlots;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[S::kRingBytes];
+  // the workgroup's active columns in activity order: {byte offset of the
   // column's values, column index into ColInfo/bitmap << 6 | index of its
-  // last 16-byte chunk}; batch kDummyBatch holds entries that load nothing
-  // of use (see below)
-  __shared__ uint2 ent_s[kWaves][kMaxWaveCols + kBatch];
-  __shared__ __attribute__((aligned(16))) uint16_t xs_s[kWaves][kMaxWaveCols * NB];
-  __shared__ int s_last;
+  // last 16-byte chunk}; padded to a whole batch with entries that load
+  // nothing of use
+  __shared__ uint2 ent_s[kMaxWgCols + kBatch];
+  __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kMaxWgCols + kBatch) * NB];
+  __shared__ int cnt_s[kWaves];
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int seg = blockIdx.x;
-  const int r = blockIdx.y;
-  const int tk_mask = (1 << a.tk_log2) - 1;
-  const int g_row = r * a.n_colblocks;
-
-  uint2* ent_l = ent_s[wave];
-  uint16_t* xs_l = xs_s[wave];
-  unsigned char* my_val = valbuf + wave * (kBatch * kSlotBytes);
+  // the product this workgroup serves, and its (stripe, segment)
+  const const_ptr<LaunchArgs> L = reload_args<LaunchArgs>();
+  const int mi = blockIdx.y;
+  const const_ptr<MatArgs> A = &L->m[mi];
+  // every field this prologue needs is requested before the first test, so
+  // that the kernel-argument reads form one round trip
+  const uint32_t local = blockIdx.x;
+  const uint32_t n_wg = (uint32_t)A->n_wg;
+  const uint32_t n_seg0 = (uint32_t)A->segments;
+  const int batch = L->batch;
+  const int tk_log2 = A->tk_log2;
+  const int n_colblocks = A->n_colblocks;
+  const int code = A->code;
+  const int cols = A->cols;
+  const int wave_cols = A->wave_cols;
+  const uint32_t* const phase_p = A->phase;
+  asm volatile("" ::"s"(n_seg0), "s"(batch), "s"(tk_log2), "s"(n_colblocks), "s"(code), "s"(cols),
+               "s"(wave_cols), "s"(phase_p));
+  if (local >= n_wg) return;  // the whole workgroup: no barrier has been reached
+  const int r = (int)(local / n_seg0);
+  const int seg = (int)(local - (uint32_t)r * n_seg0);
+  const int tk_mask = (1 << tk_log2) - 1;
+  const int g_row = r * n_colblocks;
 
   float acc[WPC][NB];
 #pragma unroll
@@ -195,11 +252,11 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
 
   // the stripe's phase: written by the previous call's last segment, read
   // by every workgroup of the stripe before any of them publishes
-  const uint32_t phase = ((const_ptr<uint32_t>)a.phase)[r];
-  const int k_begin = (seg * kWaves + wave) * a.wave_cols;
-  const int range = max(0, min(a.wave_cols, a.cols - k_begin));
+  const uint32_t phase = ((const_ptr<uint32_t>)phase_p)[r];
+  const int k_begin = (seg * kWaves + wave) * wave_cols;
+  const int range = max(0, min(wave_cols, cols - k_begin));
 
-  // ---- 1. the wave's K range: activations and column metadata in one round
+  // ---- 1. each wave's K range: activations and column metadata in one round
   // trip (ColInfo/TileOffset are fetched for every column of the range, which
   // removes a dependent memory round trip; their cache lines are shared by
   // neighbouring columns, so little extra traffic results).
@@ -210,150 +267,149 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
     const int off = 64 * c + lane;
     const bool in = off < range;
     const int k = k_begin + (in ? off : 0);
-    const int g = g_row + (k >> a.tk_log2);
-    colx[c] = ((uint32_t)g << a.tk_log2) + (uint32_t)(k & tk_mask);
+    const int g = g_row + (k >> tk_log2);
+    colx[c] = ((uint32_t)g << tk_log2) + (uint32_t)(k & tk_mask);
     ci[c] = 0u;
     to[c] = 0u;
     if (64 * c < range) {
-      ci[c] = a.col_info[colx[c]];
-      to[c] = a.tile_offset[g];
+      ci[c] = A->col_info[colx[c]];
+      to[c] = A->tile_offset[g];
     }
 #pragma unroll
-    for (int b = 0; b < NB; ++b) xb[c][b] = (in && b < a.batch) ? a.x[(size_t)b * a.cols + k] : 0u;
+    for (int b = 0; b < NB; ++b) xb[c][b] = (in && b < batch) ? A->x[(size_t)b * cols + k] : 0u;
   }
-  int n_act = 0;
+  // activity (union over the tokens), then the workgroup-wide list: each
+  // wave's active columns follow those of the lower waves
+  uint64_t actm[kChunks];
+  int n_w = 0;
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
-    const int off = 64 * c + lane;
-    const bool in = off < range;
+    const bool in = 64 * c + lane < range;
     uint64_t act = 0;
-    bool on[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int mag = (int)(xb[c][b] & 0x7FFFu);
-      on[b] = in && b < a.batch && mag > a.code && mag <= 0x7C00;
-      act |= __builtin_amdgcn_ballot_w64(on[b]);
+      act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
     }
-    if ((act >> lane) & 1) {
-      const int pos = n_act + (int)mbcnt64(act);
-      const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
-      ent_l[pos] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
+    actm[c] = act;
+    n_w += __builtin_popcountll(act);
+  }
+  if (lane == 0) cnt_s[wave] = n_w;
+  __syncthreads();
+  int total = 0, pos = 0;
 #pragma unroll
-      for (int b = 0; b < NB; ++b) xs_l[pos * NB + b] = on[b] ? (uint16_t)xb[c][b] : (uint16_t)0;
+  for (int v = 0; v < kWaves; ++v) {
+    const int cv = cnt_s[v];
+    pos += v < wave ? cv : 0;
+    total += cv;
+  }
+#pragma unroll
+  for (int c = 0; c < kChunks; ++c) {
+    if ((actm[c] >> lane) & 1) {
+      const int p = pos + (int)mbcnt64(actm[c]);
+      const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
+      ent_s[p] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int mag = (int)(xb[c][b] & 0x7FFFu);
+        const bool on = b < batch && mag > code && mag <= 0x7C00;
+        xs_s[p * NB + b] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+      }
     }
-    n_act += __builtin_popcountll(act);
+    pos += __builtin_popcountll(actm[c]);
   }
   // Pad the last batch with entries that read an all-zero bitmap (in the
-  // bitmap array's zeroed tail) and no values: they decode to nothing.
-  // The dummy batch is all such entries; stages past the last batch load it.
-  if (lane < ((kBatch - (n_act & (kBatch - 1))) & (kBatch - 1))) {
-    ent_l[n_act + lane] = make_uint2(0u, a.zero_col << 6);
+  // bitmap array's zeroed tail) and the first 16 bytes of the values: they
+  // decode to nothing.
+  if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) {
+    ent_s[total + lane] = make_uint2(0u, A->zero_col << 6);
+#pragma unroll
+    for (int b = 0; b < NB; ++b) xs_s[(total + lane) * NB + b] = 0;
   }
-  if (lane < kBatch) {
-    ent_l[kDummyBatch * kBatch + lane] = make_uint2(0u, a.zero_col << 6);
-  }
+  __syncthreads();
 
-  // ---- 2. pipeline over batches of kBatch active columns: while batch i is
-  // decoded, batch i+1's values and bitmaps are already streaming into LDS.
-  const int n_batches = (n_act + kBatch - 1) / kBatch;
+  // ---- 2. the batches are split evenly over the waves; each wave streams its
+  // share through its ring of kSlots batch slots (LDS DMA, no registers held
+  // by loads in flight) and decodes a batch as soon as its loads have landed.
+  const int n_bt = (total + kBatch - 1) / kBatch;
+  const int bb0 = n_bt * wave / kWaves;
+  const int n_mine = n_bt * (wave + 1) / kWaves - bb0;
   const int hsel = lane >> 5;
   const int q = lane & 31;
-  const unsigned char* value_bytes = reinterpret_cast<const unsigned char*>(a.values);
-  const unsigned char* bitmap_bytes = reinterpret_cast<const unsigned char*>(a.bitmap);
-
-  // A stage holds one batch in registers. Values: lane l of load pr has 16
-  // bytes of column 2pr + (l >= 32), chunk l & 31; lanes past a column's end
-  // re-read its last chunk (a line the column loads anyway) and what they
-  // leave in the slot is never read. Bitmaps: lane l holds dword l % (2 WPC)
-  // of column (l / (2 WPC)) % 8, so the decode reads the batch's words out of
-  // that register. A stage past the last batch loads the dummy batch (all
-  // lanes read the same 16 bytes of values and an all-zero bitmap), so every
-  // stage issues the same loads and the in-order wait counts release exactly
-  // the oldest stage. Offsets are 32-bit from a wave-uniform base (the value
-  // and bitmap arrays stay below 4 GiB).
-  static_assert(kBatch == 8, "a stage is four 16-byte loads per lane");
-  static_assert(kBatch * 2 * WPC <= 64, "a batch's bitmap words fit one dword per lane");
-  const uint32_t bm_lane_off = (uint32_t)(lane % (2 * WPC)) * 4u;
-  const int bm_col = (lane / (2 * WPC)) & (kBatch - 1);
-#define SPDP_LOAD(E, V) \
-  V = *reinterpret_cast<const uint4*>(value_bytes + ((E).x + (min((uint32_t)q, (E).y & 63u) << 4)))
-#define SPDP_ISSUE(I, V)                                                                          \
-  do {                                                                                            \
-    const int bi_ = (I) < n_batches ? (I) : kDummyBatch;                                          \
-    const uint2 e0_ = ent_l[bi_ * kBatch + 0 + hsel];                                             \
-    const uint2 e1_ = ent_l[bi_ * kBatch + 2 + hsel];                                             \
-    const uint2 e2_ = ent_l[bi_ * kBatch + 4 + hsel];                                             \
-    const uint2 e3_ = ent_l[bi_ * kBatch + 6 + hsel];                                             \
-    const uint32_t bcol_ = ent_l[bi_ * kBatch + bm_col].y >> 6;                                   \
-    SPDP_LOAD(e0_, V##0);                                                                         \
-    SPDP_LOAD(e1_, V##1);                                                                         \
-    SPDP_LOAD(e2_, V##2);                                                                         \
-    SPDP_LOAD(e3_, V##3);                                                                         \
-    V##b = *reinterpret_cast<const uint32_t*>(bitmap_bytes + (bcol_ * (WPC * 8u) + bm_lane_off)); \
-  } while (0)
-#define SPDP_TO_LDS(V, BM)                                                                           \
-  do {                                                                                            \
-    *reinterpret_cast<uint4*>(my_val + 0 * kSlotBytes + 16 * lane) = V##0;                        \
-    *reinterpret_cast<uint4*>(my_val + 2 * kSlotBytes + 16 * lane) = V##1;                        \
-    *reinterpret_cast<uint4*>(my_val + 4 * kSlotBytes + 16 * lane) = V##2;                        \
-    *reinterpret_cast<uint4*>(my_val + 6 * kSlotBytes + 16 * lane) = V##3;                        \
-    BM = V##b;                                                                                    \
-  } while (0)
-
-  // Decode of batch i: its values are in the wave's LDS slots and its bitmap
-  // words in bm (one dword per lane, see above): v_readlane moves them to
-  // scalar registers, where they serve directly as MaskedPopcount masks and
-  // EXEC masks.
-  auto decode_quad = [&](int i, int u0, uint32_t bm) __attribute__((always_inline)) {
-    uint64_t words[kQuad][WPC];
+  unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
+  const void* const values = A->values;
+  const void* const bitmap = A->bitmap;
+  // Values: lane l of load pr brings 16 bytes of column 2pr + (l >= 32),
+  // chunk l & 31, to that column's 512-byte slot; lanes past a column's end
+  // re-read its last chunk (a line the column loads anyway). Bitmaps: lane l
+  // < 16 WPC brings dword l of the batch's words (column l / (2 WPC)).
+  auto issue = [&](int i) __attribute__((always_inline)) {
+    const int e0 = (bb0 + i) * kBatch;
+    const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)lds_addr(my_ring + (i % kSlots) * kBatchBytes));
 #pragma unroll
-    for (int c = 0; c < kQuad; ++c)
+    for (int pr = 0; pr < kBatch / 2; ++pr) {
+      const uint2 e = ent_s[e0 + 2 * pr + hsel];
+      dma16(values, e.x + (min((uint32_t)q, e.y & 63u) << 4), slot + pr * 2 * kSlotBytes);
+    }
+    if (lane < 2 * WPC * kBatch) {
+      const uint2 e = ent_s[e0 + lane / (2 * WPC)];
+      dma4(bitmap, (e.y >> 6) * (WPC * 8u) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
+    }
+  };
+
+  // Decode of four columns of a landed batch. The bitmap words come from
+  // scalar loads of the bitmap array (the batch's DMA has just brought their
+  // lines into L2) straight into scalar registers, where they serve as
+  // MaskedPopcount masks and as EXEC masks of the value reads.
+  const const_ptr<unsigned char> bitmap_s = (const_ptr<unsigned char>)bitmap;
+  auto load_masks = [&](uint64_t (&m)[kQuad][WPC], uint32_t bo_v, int u0) __attribute__((always_inline)) {
 #pragma unroll
-      for (int w = 0; w < WPC; ++w) {
-        const int l = (u0 + c) * 2 * WPC + 2 * w;
-        words[c][w] = (uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)bm, l) |
-                      ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)bm, l + 1) << 32);
-      }
+    for (int c = 0; c < kQuad; ++c) {
+      const uint32_t bo = (uint32_t)__builtin_amdgcn_readlane((int)bo_v, u0 + c);
+      const const_ptr<uint64_t> bp = (const_ptr<uint64_t>)(bitmap_s + bo);
+#pragma unroll
+      for (int w = 0; w < WPC; ++w) m[c][w] = bp[w];
+    }
+  };
+  auto decode_quad = [&](const unsigned char* slot, int e0, int u0, const uint64_t (&m)[kQuad][WPC])
+      __attribute__((always_inline)) {
     // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
-    // below the lane plus the popcounts of the column's earlier words
+    // below the lane plus the popcounts of the column's earlier words (every
+    // lane reads; lanes whose bit is clear read a neighbour inside the slot
+    // and are masked off below)
     uint32_t vb[kQuad][WPC];
 #pragma unroll
     for (int c = 0; c < kQuad; ++c) {
-      const uint16_t* slot = reinterpret_cast<const uint16_t*>(my_val + (u0 + c) * kSlotBytes);
+      const uint16_t* vslot = reinterpret_cast<const uint16_t*>(slot + (u0 + c) * kSlotBytes);
       uint32_t prefix = 0;
 #pragma unroll
       for (int w = 0; w < WPC; ++w) {
-        vb[c][w] = slot[prefix + mbcnt64(words[c][w])];
-        prefix += (uint32_t)__builtin_popcountll(words[c][w]);
+        vb[c][w] = vslot[prefix + mbcnt64(m[c][w])];
+        prefix += (uint32_t)__builtin_popcountll(m[c][w]);
       }
     }
     // 4. accumulate where the bitmap bit is set: for one token the words
     // become EXEC around single FMAs (no branch, no select); for more tokens
-    // the compiler's FMA-plus-select on the word is used
-    const int xrow = (i * kBatch + u0) * NB;
-    // one token: the group's fp16 activations in one LDS read
+    // the compiler's FMA under the word mask is used
+    const int xrow = (e0 + u0) * NB;
     uint2 xq = make_uint2(0u, 0u);
-    if constexpr (NB == 1) {
-      if constexpr (kQuad == 4)
-        xq = *reinterpret_cast<const uint2*>(&xs_l[xrow]);
-      else
-        xq.x = *reinterpret_cast<const uint32_t*>(&xs_l[xrow]);
-    }
+    if constexpr (NB == 1) xq = *reinterpret_cast<const uint2*>(&xs_s[xrow]);
 #pragma unroll
     for (int c = 0; c < kQuad; ++c) {
       if constexpr (NB == 1) {
         const uint32_t xpair = c < 2 ? xq.x : xq.y;
         if (c & 1)
-          masked_fma_column<WPC, true>(acc, vb[c], xpair, words[c]);
+          masked_fma_column<WPC, true>(acc, vb[c], xpair, m[c]);
         else
-          masked_fma_column<WPC, false>(acc, vb[c], xpair, words[c]);
+          masked_fma_column<WPC, false>(acc, vb[c], xpair, m[c]);
       } else {
         float xv[NB];
 #pragma unroll
-        for (int b = 0; b < NB; ++b) xv[b] = half_bits_to_float(xs_l[xrow + c * NB + b]);
+        for (int b = 0; b < NB; ++b) xv[b] = half_bits_to_float(xs_s[xrow + c * NB + b]);
 #pragma unroll
         for (int w = 0; w < WPC; ++w)
-          if (__builtin_amdgcn_inverse_ballot_w64(words[c][w])) {
+          if (__builtin_amdgcn_inverse_ballot_w64(m[c][w])) {
             const float v = half_bits_to_float(vb[c][w]);
 #pragma unroll
             for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[b], acc[w][b]);
@@ -361,74 +417,52 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(KernelArgs a) {
       }
     }
   };
-  // A batch is kBatch / kQuad groups; a group holding only padding entries
-  // (all-zero words) is skipped.
-  static_assert(kQuad == 2 || kQuad == 4, "columns are decoded in pairs or quads");
-  auto decode = [&](int i, uint32_t bm) __attribute__((always_inline)) {
-#pragma unroll
-    for (int g = 0; g < kBatch / kQuad; ++g)
-      if (g == 0 || n_act - i * kBatch > g * kQuad) decode_quad(i, g * kQuad, bm);
-  };
+  static_assert(kQuad == 4 && kBatch % kQuad == 0, "a batch is decoded in quads");
 
-  // kDepth batches in flight: a stage holds batch i while the next kDepth-1
-  // batches stream; a batch moves to LDS right before its decode. The loop has
-  // a single exit and every path through it issues the same loads, so the
-  // waits at its head count exactly one stage. The stages must be issued in
-  // order (the waits count loads in order), so the scheduler may not
-  // interleave them.
-  static_assert(kDepth == 2 || kDepth == 3, "the loop below is unrolled for two or three stages");
-  if (n_batches > 0) {
-    uint4 s00, s01, s02, s03, s10, s11, s12, s13;
-    uint32_t s0b, s1b, bm;
-    SPDP_ISSUE(0, s0);
-    __builtin_amdgcn_sched_barrier(0);
-    SPDP_ISSUE(1, s1);
-    __builtin_amdgcn_sched_barrier(0);
-    if constexpr (kDepth == 2) {
-      for (int i = 0; i < n_batches; i += 2) {
-        SPDP_TO_LDS(s0, bm);
-        SPDP_ISSUE(i + 2, s0);
-        __builtin_amdgcn_sched_barrier(0);
-        decode(i, bm);
-        SPDP_TO_LDS(s1, bm);
-        SPDP_ISSUE(i + 3, s1);
-        __builtin_amdgcn_sched_barrier(0);
-        if (i + 1 < n_batches) decode(i + 1, bm);
-      }
-    } else {
-      uint4 s20, s21, s22, s23;
-      uint32_t s2b;
-      SPDP_ISSUE(2, s2);
-      __builtin_amdgcn_sched_barrier(0);
-      for (int i = 0; i < n_batches; i += 3) {
-        SPDP_TO_LDS(s0, bm);
-        SPDP_ISSUE(i + 3, s0);
-        __builtin_amdgcn_sched_barrier(0);
-        decode(i, bm);
-        SPDP_TO_LDS(s1, bm);
-        SPDP_ISSUE(i + 4, s1);
-        __builtin_amdgcn_sched_barrier(0);
-        if (i + 1 < n_batches) decode(i + 1, bm);
-        SPDP_TO_LDS(s2, bm);
-        SPDP_ISSUE(i + 5, s2);
-        __builtin_amdgcn_sched_barrier(0);
-        if (i + 2 < n_batches) decode(i + 2, bm);
+  // The ring: batches 0 .. kSlots-1 are requested up front; after batch i is
+  // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
+  // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
+  // requested after i) loads outstanding".
+  const int n_first = min(n_mine, kSlots);
+  for (int i = 0; i < n_first; ++i) issue(i);
+  for (int i = 0; i < n_mine; ++i) {
+    const int later = min(n_mine - 1 - i, kSlots - 1);
+    if (later >= 3)
+      wait_vmcnt<3 * kDmaPerBatch>();
+    else if (later == 2)
+      wait_vmcnt<2 * kDmaPerBatch>();
+    else if (later == 1)
+      wait_vmcnt<kDmaPerBatch>();
+    else
+      wait_vmcnt<0>();
+    const unsigned char* slot = my_ring + (i % kSlots) * kBatchBytes;
+    const int e0 = (bb0 + i) * kBatch;
+    // byte offsets of the batch's bitmaps: lane u < 8 holds column u's
+    const uint32_t bo_v = (ent_s[e0 + (lane & (kBatch - 1))].y >> 6) * (WPC * 8u);
+#pragma unroll
+    for (int u0 = 0; u0 < kBatch; u0 += kQuad) {
+      // a quad of padding entries only (past the workgroup's list) is skipped
+      if (u0 == 0 || total - e0 > u0) {
+        uint64_t m[kQuad][WPC];
+        load_masks(m, bo_v, u0);
+        decode_quad(slot, e0, u0, m);
       }
     }
+    if (i + kSlots < n_mine) {
+      // the slot's LDS reads have completed (their results were consumed)
+      issue(i + kSlots);
+    }
   }
-#undef SPDP_LOAD
-#undef SPDP_ISSUE
-#undef SPDP_TO_LDS
 
   // ---- 5. reduce the 4 waves in LDS and publish this segment's partial
   // sums: device-coherent 8-byte stores, so that value and tag land together
   // and can be read from another XCD
-  const_ptr<KernelArgs> ka = reload_args<KernelArgs>();
+  const_ptr<MatArgs> ka = &reload_args<LaunchArgs>()->m[mi];
   const int mpad = ka->n_stripes * ka->tile_m;
   const int n_seg = ka->segments;
-  const int nb = ka->batch;
+  const int nb = batch;
   const int row = threadIdx.x;
-  float* red = reinterpret_cast<float*>(valbuf);
+  float* red = reinterpret_cast<float*>(ring);
   constexpr int kSlice = Smem<NB>::kSlice;
   unsigned long long* dst = ka->partials + (size_t)seg * nb * mpad + (size_t)r * ka->tile_m + row;
   const unsigned long long tag = (unsigned long long)phase << 32;
@@ -634,19 +668,74 @@ int upload(const std::vector<T>& v, void** dst) {
 }
 
 template <int NB, int WPC>
-hipError_t launch_one(const KernelArgs& args, dim3 grid, hipStream_t stream) {
+hipError_t launch_one(const LaunchArgs& args, dim3 grid, hipStream_t stream) {
   hipLaunchKernelGGL((spmspv_kernel<NB, WPC>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
 template <int NB>
-hipError_t launch(const KernelArgs& args, int wpc, dim3 grid, hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, dim3 grid, hipStream_t stream) {
   switch (wpc) {
     case 1: return launch_one<NB, 1>(args, grid, stream);
     case 2: return launch_one<NB, 2>(args, grid, stream);
     case 3: return launch_one<NB, 3>(args, grid, stream);
     default: return launch_one<NB, 4>(args, grid, stream);
   }
+}
+
+// Validates one product of a call and fills its kernel arguments (sizing
+// the handle's workspace for the batch if needed).
+int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, uint16_t* Y, int dev,
+            MatArgs* out, int64_t* n_wg) {
+  if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
+  if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
+  if (!X || !Y) return fail(SPDP_ERR_INVALID_ARG, "X or Y is NULL");
+  if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
+    return fail(SPDP_ERR_INVALID_ARG, "X and Y must be 16-byte aligned");
+  {
+    const uintptr_t x0 = reinterpret_cast<uintptr_t>(X);
+    const uintptr_t x1 = x0 + (uintptr_t)batch * h->cols * 2;
+    const uintptr_t y0 = reinterpret_cast<uintptr_t>(Y);
+    const uintptr_t y1 = y0 + (uintptr_t)batch * h->rows * 2;
+    if (x0 < y1 && y0 < x1) return fail(SPDP_ERR_INVALID_ARG, "X and Y overlap");
+  }
+  int32_t code = 0;
+  int st = spdp_threshold_code(threshold, &code);
+  if (st != SPDP_OK) return st;
+  if (dev != h->device) return fail(SPDP_ERR_INVALID_ARG, "current device differs from the handle's");
+
+  int segments = 1, wave_cols = 16;
+  choose_split(h, &segments, &wave_cols);
+  st = ensure_workspace(h, batch, segments);
+  if (st != SPDP_OK) return st;
+
+  MatArgs& a = *out;
+  a.tile_offset = static_cast<const uint32_t*>(h->d_tile_offset);
+  a.col_info = static_cast<const uint32_t*>(h->d_col_info);
+  a.bitmap = static_cast<const uint64_t*>(h->d_bitmap);
+  a.values = static_cast<const uint16_t*>(h->d_values);
+  a.x = X;
+  a.y = Y;
+  a.partials = h->d_partials;
+  a.phase = h->d_phase;
+  a.rows = (int)h->rows;
+  a.cols = (int)h->cols;
+  a.tile_m = h->tile_m;
+  a.zero_col = (uint32_t)(h->n_gtiles * h->tile_k);
+  a.tk_log2 = __builtin_ctz((unsigned)h->tile_k);
+  a.n_colblocks = (int)h->n_colblocks;
+  a.n_stripes = (int)h->n_stripes;
+  a.code = code;
+  a.wave_cols = wave_cols;
+  a.segments = segments;
+  *n_wg = (int64_t)segments * h->n_stripes;
+  a.n_wg = (int)*n_wg;
+  return SPDP_OK;
+}
+
+bool overlap(const void* p, size_t pn, const void* q, size_t qn) {
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(p), b0 = reinterpret_cast<uintptr_t>(q);
+  return a0 < b0 + qn && b0 < a0 + pn;
 }
 
 }  // namespace
@@ -724,73 +813,67 @@ int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
   return ensure_workspace(h, max_batch, segments);
 }
 
-int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold,
-                uint16_t* Y, void* stream) {
+int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
+                     int32_t batch, const float* thresholds, uint16_t* const* Y, void* stream) {
   spdp::clear_error();
-  if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
-  if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
-  if (!X || !Y) return fail(SPDP_ERR_INVALID_ARG, "X or Y is NULL");
+  if (!handles || !X || !Y || !thresholds) return fail(SPDP_ERR_INVALID_ARG, "an argument array is NULL");
+  if (count < 1 || count > kMaxGroup) return fail(SPDP_ERR_INVALID_ARG, "count must lie in [1, 8]");
   if (batch < 1 || batch > kMaxBatch) return fail(SPDP_ERR_INVALID_ARG, "batch must lie in [1, 32]");
-  if ((reinterpret_cast<uintptr_t>(X) | reinterpret_cast<uintptr_t>(Y)) & 15)
-    return fail(SPDP_ERR_INVALID_ARG, "X and Y must be 16-byte aligned");
-  {
-    const uintptr_t x0 = reinterpret_cast<uintptr_t>(X);
-    const uintptr_t x1 = x0 + (uintptr_t)batch * h->cols * 2;
-    const uintptr_t y0 = reinterpret_cast<uintptr_t>(Y);
-    const uintptr_t y1 = y0 + (uintptr_t)batch * h->rows * 2;
-    if (x0 < y1 && y0 < x1) return fail(SPDP_ERR_INVALID_ARG, "X and Y overlap");
+  for (int i = 0; i < count; ++i) {
+    if (!handles[i]) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
+    if (handles[i]->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
   }
-  int32_t code = 0;
-  int st = spdp_threshold_code(threshold, &code);
-  if (st != SPDP_OK) return st;
+  for (int i = 0; i < count; ++i) {
+    for (int j = 0; j < i; ++j) {
+      if (handles[i] == handles[j])
+        return fail(SPDP_ERR_INVALID_ARG, "a handle appears twice in one call (its workspace is shared)");
+      {
+        const size_t xi = (size_t)batch * handles[i]->cols * 2, yi = (size_t)batch * handles[i]->rows * 2;
+        const size_t xj = (size_t)batch * handles[j]->cols * 2, yj = (size_t)batch * handles[j]->rows * 2;
+        if (overlap(Y[i], yi, Y[j], yj) || overlap(Y[i], yi, X[j], xj) || overlap(Y[j], yj, X[i], xi))
+          return fail(SPDP_ERR_INVALID_ARG, "an output overlaps another product's input or output");
+      }
+    }
+  }
   int dev = -1;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  if (dev != h->device) return fail(SPDP_ERR_INVALID_ARG, "current device differs from the handle's");
+  LaunchArgs la;
+  std::memset(&la, 0, sizeof(la));
+  la.batch = batch;
+  int64_t widest = 0;
+  for (int i = 0; i < count; ++i) {
+    int64_t n_wg = 0;
+    const int st = prepare(handles[i], X[i], batch, thresholds[i], Y[i], dev, &la.m[i], &n_wg);
+    if (st != SPDP_OK) return st;
+    if (handles[i]->tile_m != handles[0]->tile_m)
+      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
+    if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
+    widest = std::max(widest, n_wg);
+  }
 
-  int segments = 1, wave_cols = 16;
-  choose_split(h, &segments, &wave_cols);
-  st = ensure_workspace(h, batch, segments);
-  if (st != SPDP_OK) return st;
-
-  KernelArgs args;
-  args.tile_offset = static_cast<const uint32_t*>(h->d_tile_offset);
-  args.col_info = static_cast<const uint32_t*>(h->d_col_info);
-  args.bitmap = static_cast<const uint64_t*>(h->d_bitmap);
-  args.values = static_cast<const uint16_t*>(h->d_values);
-  args.x = X;
-  args.y = Y;
-  args.partials = h->d_partials;
-  args.phase = h->d_phase;
-  args.rows = (int)h->rows;
-  args.cols = (int)h->cols;
-  args.tile_m = h->tile_m;
-  const int wpc = h->tile_m / 64;
-  args.zero_col = (uint32_t)(h->n_gtiles * h->tile_k);
-  args.tk_log2 = __builtin_ctz((unsigned)h->tile_k);
-  args.n_colblocks = (int)h->n_colblocks;
-  args.n_stripes = (int)h->n_stripes;
-  args.batch = batch;
-  args.code = code;
-  args.wave_cols = wave_cols;
-  args.segments = segments;
-
-  const dim3 grid((unsigned)segments, (unsigned)h->n_stripes);
+  const int wpc = handles[0]->tile_m / 64;
+  const dim3 grid((unsigned)widest, (unsigned)count);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (batch <= 1)
-    e = launch<1>(args, wpc, grid, s);
+    e = launch<1>(la, wpc, grid, s);
   else if (batch <= 2)
-    e = launch<2>(args, wpc, grid, s);
+    e = launch<2>(la, wpc, grid, s);
   else if (batch <= 4)
-    e = launch<4>(args, wpc, grid, s);
+    e = launch<4>(la, wpc, grid, s);
   else if (batch <= 8)
-    e = launch<8>(args, wpc, grid, s);
+    e = launch<8>(la, wpc, grid, s);
   else if (batch <= 16)
-    e = launch<16>(args, wpc, grid, s);
+    e = launch<16>(la, wpc, grid, s);
   else
-    e = launch<32>(args, wpc, grid, s);
+    e = launch<32>(la, wpc, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
+}
+
+int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold,
+                uint16_t* Y, void* stream) {
+  return spdp_spmspv_many(&h, 1, &X, batch, &threshold, &Y, stream);
 }
 
 void spdp_free(spdp_handle_t h) {

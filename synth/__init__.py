@@ -99,8 +99,10 @@ WORKLOADS = {
         projections=[_proj("w", 1024, 1024, 101, 102)],
         weight_sparsity=[0.5], act_sparsity=[0.5], batch=[1], tile=(64, 64)),
     "llama7b-attn": dict(
-        projections=[_proj(n, 4096, 4096, 201 + i, 211 + i)
-                     for i, n in enumerate(("q", "k", "v", "o"))],
+        projections=[_proj("q", 4096, 4096, 201, 211),   # q, k, v read the layer input
+                     _proj("k", 4096, 4096, 202, 211),
+                     _proj("v", 4096, 4096, 203, 211),
+                     _proj("o", 4096, 4096, 204, 212)],  # o reads the attention output
         weight_sparsity=[0.5, 0.6, 0.7], act_sparsity=[0.0, 0.25, 0.5],
         batch=[1], tile=(256, 16)),
     "llama7b-mlp": dict(

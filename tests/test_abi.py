@@ -111,3 +111,32 @@ def test_format_view_fields():
     assert f["tile_offset"].size == 31 and f["col_info"].size == 120 and f["bitmap"].size == 120
     assert m.device == -1
     assert all(v is None for v in m.device_pointers().values())
+
+
+def test_spmspv_many_argument_errors():
+    """Host-side checks of the grouped call (no device needed)."""
+    L = spdp.lib()
+    a = spdp.encode_host(np.ones((64, 16), dtype=np.float16), (64, 16))
+    b = spdp.encode_host(np.ones((64, 16), dtype=np.float16), (64, 16))
+    x = np.zeros(256, dtype=np.uint16)
+    H = ctypes.c_void_p
+    P = ctypes.c_void_p
+    xs = (P * 2)(x.ctypes.data, x.ctypes.data)
+    ys = (P * 2)(x.ctypes.data + 128, x.ctypes.data + 256)
+    ts = (ctypes.c_float * 2)(0.0, 0.0)
+    hs = (H * 2)(a._h.value, b._h.value)
+    assert L.spdp_spmspv_many(None, 1, xs, 1, ts, ys, None) == ERR_INVALID
+    assert L.spdp_spmspv_many(hs, 1, None, 1, ts, ys, None) == ERR_INVALID
+    assert L.spdp_spmspv_many(hs, 1, xs, 1, None, ys, None) == ERR_INVALID
+    for count in (0, 9, -1):
+        assert L.spdp_spmspv_many(hs, count, xs, 1, ts, ys, None) == ERR_INVALID
+    assert L.spdp_spmspv_many(hs, 2, xs, 0, ts, ys, None) == ERR_INVALID
+    assert L.spdp_spmspv_many(hs, 2, xs, 33, ts, ys, None) == ERR_INVALID
+    nul = (H * 2)(None, a._h.value)
+    assert L.spdp_spmspv_many(nul, 2, xs, 1, ts, ys, None) == ERR_INVALID
+    assert b"NULL" in L.spdp_last_error()
+    # host-only handles are rejected before any device work
+    assert L.spdp_spmspv_many(hs, 2, xs, 1, ts, ys, None) == ERR_INVALID
+    assert b"device" in L.spdp_last_error()
+    a.close()
+    b.close()

@@ -1,0 +1,134 @@
+"""GPU parity of the grouped call (spdp_spmspv_many): several independent
+products in one launch. Each product is checked against the CPU oracle and
+must be bit-identical to the same product run alone (the kernel's summation
+order does not depend on what else the launch carries)."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+import paper_2607_21985_amd as spdp  # noqa: E402
+
+from test_gpu_parity import _assert_close, _dev, _to_dev  # noqa: E402
+
+
+def _products(shapes, sw, p, batch, seed, share_x=False):
+    out = []
+    x_shared = None
+    for i, (rows, cols) in enumerate(shapes):
+        w = oracle.magnitude_prune(synth.weights(rows, cols, seed + i), sw)
+        if share_x and x_shared is not None and x_shared.shape[1] == cols:
+            x = x_shared
+        else:
+            x = synth.laplace_activations(batch, cols, seed + 100 + i)
+            x_shared = x
+        t = float(oracle.threshold_for(x, p))
+        out.append((w, x, t))
+    return out
+
+
+@pytest.mark.parametrize("shapes,tile,sw,p,batch,share_x", [
+    ([(512, 1024), (300, 1024), (1000, 777)], (256, 16), 0.5, 0.5, 1, False),
+    ([(4096, 4096), (4096, 4096), (4096, 4096)], (256, 16), 0.6, 0.5, 1, True),   # q, k, v on one input
+    ([(1100, 4096), (1100, 4096)], (256, 16), 0.6, 0.5, 3, True),                 # gate, up
+    ([(130, 200), (64, 64), (257, 1000), (90, 33), (700, 300)], (64, 8), 0.5, 0.3, 2, False),
+    ([(256, 256)] * 8, (128, 16), 0.7, 0.25, 1, False),
+])
+def test_many_matches_oracle_and_single_calls(shapes, tile, sw, p, batch, share_x):
+    dev = _dev()
+    prods = _products(shapes, sw, p, batch, 900 + len(shapes), share_x)
+    mats = [spdp.encode(w, tile) for w, _, _ in prods]
+    Xs, xs_by_id = [], {}
+    for _, x, _ in prods:
+        if id(x) not in xs_by_id:
+            xs_by_id[id(x)] = _to_dev(x)
+        Xs.append(xs_by_id[id(x)])
+    Yg = [torch.full((batch, m.rows), float("nan"), dtype=torch.float16, device=dev) for m in mats]
+    print(f"[gpu] many: {len(mats)} products {shapes[:2]}... tile {tile} b={batch}", flush=True)
+    spdp.spmspv_many(mats, Xs, [t for _, _, t in prods], Yg)
+    torch.cuda.synchronize()
+    for i, ((w, x, t), m, X, Y) in enumerate(zip(prods, mats, Xs, Yg)):
+        y = Y.cpu().numpy().astype(np.float64)
+        y64, s64, _ = oracle.spmspv(w, x, t)
+        _assert_close(y, y64, s64, f"product {i}")
+        Ys = torch.full_like(Y, float("nan"))
+        m.spmspv_into(X, t, Ys)
+        torch.cuda.synchronize()
+        assert torch.equal(Ys, Y), f"product {i}: grouped result differs from the single call"
+    for m in mats:
+        m.close()
+
+
+def test_many_repeated_and_graph_replayed():
+    """Grouped calls back to back, then captured and replayed with eager calls
+    in between: every result equals the first eager one."""
+    dev = _dev()
+    prods = _products([(900, 2100), (600, 2100), (1300, 2100)], 0.5, 0.5, 1, 77, share_x=True)
+    mats = [spdp.encode(w, (256, 16)) for w, _, _ in prods]
+    X = _to_dev(prods[0][1])
+    ts = [t for _, _, t in prods]
+    Ys = [torch.zeros((1, m.rows), dtype=torch.float16, device=dev) for m in mats]
+    spdp.spmspv_many(mats, [X] * 3, ts, Ys)
+    torch.cuda.synchronize()
+    ref = [Y.clone() for Y in Ys]
+    for rep in range(3):
+        spdp.spmspv_many(mats, [X] * 3, ts, Ys)
+    torch.cuda.synchronize()
+    assert all(torch.equal(Y, R) for Y, R in zip(Ys, ref))
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        spdp.spmspv_many(mats, [X] * 3, ts, Ys)
+    torch.cuda.synchronize()
+    for rep in range(4):
+        print(f"[gpu] grouped graph replay {rep}", flush=True)
+        for Y in Ys:
+            Y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert all(torch.equal(Y, R) for Y, R in zip(Ys, ref)), f"replay {rep}"
+        for m, t in zip(mats, ts):
+            m(X, t)
+        torch.cuda.synchronize()
+    for (w, x, t), R in zip(prods, ref):
+        y64, s64, _ = oracle.spmspv(w, x, t)
+        _assert_close(R.cpu().numpy().astype(np.float64), y64, s64, "grouped reference")
+    del g
+    for m in mats:
+        m.close()
+
+
+def test_many_argument_errors_on_device():
+    dev = _dev()
+    L = spdp.lib()
+    w = oracle.magnitude_prune(synth.weights(256, 512, 5), 0.5)
+    a, b = spdp.encode(w, (256, 16)), spdp.encode(w, (256, 16))
+    c = spdp.encode(w, (128, 16))
+    X = torch.zeros((1, 512), dtype=torch.float16, device=dev)
+    Y = torch.zeros((2, 256), dtype=torch.float16, device=dev)
+    P = ctypes.c_void_p
+
+    def call(hs, xs, ys, ts=(0.0, 0.0)):
+        n = len(hs)
+        return L.spdp_spmspv_many((P * n)(*[h._h.value for h in hs]), n,
+                                  (P * n)(*[x.data_ptr() for x in xs]), 1,
+                                  (ctypes.c_float * n)(*ts), (P * n)(*[y.data_ptr() for y in ys]), None)
+
+    y0, y1 = Y[0:1], Y[1:2]
+    assert call([a, a], [X, X], [y0, y1]) == -1 and b"twice" in L.spdp_last_error()
+    assert call([a, c], [X, X], [y0, y1]) == -1 and b"tile_m" in L.spdp_last_error()
+    assert call([a, b], [X, X], [y0, y0]) == -1 and b"overlap" in L.spdp_last_error()
+    assert call([a, b], [X, y0], [y0, y1]) == -1 and b"overlap" in L.spdp_last_error()
+    assert call([a, b], [X, X], [y0, y1], (0.0, float("nan"))) == -1
+    assert call([a, b], [X, X], [y0, y1]) == 0
+    torch.cuda.synchronize()
+    for m in (a, b, c):
+        m.close()
