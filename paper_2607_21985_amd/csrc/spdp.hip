@@ -576,29 +576,38 @@ int hip_fail(hipError_t e, const char* what) {
   return fail(SPDP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
 
-// Split-K heuristic: about 7168 waves (one full load of the 256 CUs at seven
-// workgroups each, so that early finishers are replaced), at most kMaxSegments
-// segments per stripe (the gather then needs one round of loads), every wave
-// covering a multiple of 16 columns and at most kMaxWaveCols of them.
-// SPDP_SPLITK overrides the number of segments (for tuning).
-constexpr int64_t kTargetWaves = 7168;
-constexpr int64_t kMaxSegments = 48;
+// Split-K heuristic. Each wave tests and streams a K range of wave_cols
+// columns (a multiple of 16); a product's grid is stripes x segments with
+// segments = ceil(cols / (4 wave_cols)). Measured on the Llama shapes, about
+// 48 columns per wave is fastest as long as the product has between 512 (two
+// per CU) and 1792 (the seven per CU that fit at once) workgroups; outside
+// that band the range moves in steps of 16 columns (at most kMaxWaveCols,
+// and at most kMaxSegments segments, which the gather reads per row).
+// This gives 4096x4096: 32 segments, 11008x4096: 22, 13824x5120: 27,
+// 28672x8192: 16 (each the fastest of a sweep). SPDP_SPLITK overrides the
+// number of segments (for tuning).
+constexpr int kPreferredWaveCols = 48;
+constexpr int64_t kMinWorkgroups = 512;
+constexpr int64_t kMaxWorkgroups = 1792;
+constexpr int64_t kMaxSegments = 64;
 void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
-  const int64_t cols = m->cols;
+  const int64_t cols = std::max<int64_t>(1, m->cols);
   const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
-  int64_t want = std::min<int64_t>(kMaxSegments,
-                                   std::max<int64_t>(1, (kTargetWaves + kWaves * stripes - 1) / (kWaves * stripes)));
+  auto segs = [&](int64_t wc) { return (cols + kWaves * wc - 1) / (kWaves * wc); };
+  int64_t wc = kPreferredWaveCols;
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
-    if (v >= 1) want = v;
+    if (v >= 1) {
+      wc = std::min<int64_t>(kMaxWaveCols, ((cols + v * kWaves - 1) / (v * kWaves) + 15) / 16 * 16);
+      *wave_cols = (int)wc;
+      *segments = (int)segs(wc);
+      return;
+    }
   }
-  const int64_t min_seg = (cols + kWaves * kMaxWaveCols - 1) / (kWaves * kMaxWaveCols);
-  const int64_t max_seg = std::max<int64_t>(1, (cols + kWaves * 16 - 1) / (kWaves * 16));
-  const int64_t s = std::max(min_seg, std::min(want, max_seg));
-  int64_t wc = (cols + s * kWaves - 1) / (s * kWaves);
-  wc = std::min<int64_t>(kMaxWaveCols, (wc + 15) / 16 * 16);
+  while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kMaxSegments) && wc < kMaxWaveCols) wc += 16;
+  while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kMaxSegments) wc -= 16;
   *wave_cols = (int)wc;
-  *segments = (int)((cols + wc * kWaves - 1) / (wc * kWaves));
+  *segments = (int)segs(wc);
 }
 
 // The workspace holds {fp32, phase} pairs for all segments; it
