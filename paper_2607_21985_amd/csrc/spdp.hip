@@ -112,10 +112,6 @@ __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
 template <class T>
 using const_ptr = const __attribute__((address_space(4))) T*;
 
-__device__ __forceinline__ float half_bits_to_float(uint32_t h) {
-  return __half2float(__ushort_as_half((unsigned short)h));
-}
-
 // One column of one token: acc[w] += f32(v[w]) * f32(x) in the lanes whose
 // bit is set in word w, where v[w] is fp16 bits and x the low (XHI false) or
 // high (XHI true) fp16 half of xpair. The whole column is one block so that
@@ -167,6 +163,13 @@ __device__ __forceinline__ void masked_fma_column(float (&acc)[WPC][1], const ui
 }
 #undef SPDP_COLUMN
 #undef SPDP_FMA
+
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+// acc + lo(v) * lo(x) + hi(v) * hi(x) in fp32 (fp16 products are exact in fp32)
+__device__ __forceinline__ float dot2(uint32_t v, uint32_t x, float acc) {
+  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, v), __builtin_bit_cast(half2_t, x), acc, false);
+}
 
 // The kernel's argument block, read again from the kernel-argument segment
 // through a pointer the compiler cannot see through: fields used only after
@@ -313,7 +316,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       for (int b = 0; b < NB; ++b) {
         const int mag = (int)(xb[c][b] & 0x7FFFu);
         const bool on = b < batch && mag > code && mag <= 0x7C00;
-        xs_s[p * NB + b] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+        xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
       }
     }
     pos += __builtin_popcountll(actm[c]);
@@ -324,7 +327,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) {
     ent_s[total + lane] = make_uint2(0u, A->zero_col << 6);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) xs_s[(total + lane) * NB + b] = 0;
+    for (int b = 0; b < NB; ++b) xs_s[(((total + lane) >> 1) * NB + b) * 2 + ((total + lane) & 1)] = 0;
   }
   __syncthreads();
 
@@ -389,31 +392,39 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
         prefix += (uint32_t)__builtin_popcountll(m[c][w]);
       }
     }
-    // 4. accumulate where the bitmap bit is set: for one token the words
-    // become EXEC around single FMAs (no branch, no select); for more tokens
-    // the compiler's FMA under the word mask is used
-    const int xrow = (e0 + u0) * NB;
-    uint2 xq = make_uint2(0u, 0u);
-    if constexpr (NB == 1) xq = *reinterpret_cast<const uint2*>(&xs_s[xrow]);
+    // 4. accumulate in fp32. One token: the words become EXEC around single
+    // FMAs (v_fma_mix, fp16 operands; no branch, no select). More tokens:
+    // lanes whose bit is clear are zeroed (v_cndmask on the word), the two
+    // columns of a pair are packed into one register, and one dot product
+    // per token (v_dot2_f32_f16 against the pair's two activations) adds
+    // both columns: NB/2 instructions per word instead of NB.
+    if constexpr (NB == 1) {
+      const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[e0 + u0]);
 #pragma unroll
-    for (int c = 0; c < kQuad; ++c) {
-      if constexpr (NB == 1) {
+      for (int c = 0; c < kQuad; ++c) {
         const uint32_t xpair = c < 2 ? xq.x : xq.y;
         if (c & 1)
           masked_fma_column<WPC, true>(acc, vb[c], xpair, m[c]);
         else
           masked_fma_column<WPC, false>(acc, vb[c], xpair, m[c]);
-      } else {
-        float xv[NB];
+      }
+    } else {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) xv[b] = half_bits_to_float(xs_s[xrow + c * NB + b]);
+      for (int pr = 0; pr < 2; ++pr) {
+        uint32_t pv[WPC];
 #pragma unroll
-        for (int w = 0; w < WPC; ++w)
-          if (__builtin_amdgcn_inverse_ballot_w64(m[c][w])) {
-            const float v = half_bits_to_float(vb[c][w]);
+        for (int w = 0; w < WPC; ++w) {
+          const uint32_t lo = __builtin_amdgcn_inverse_ballot_w64(m[2 * pr][w]) ? vb[2 * pr][w] : 0u;
+          const uint32_t hi = __builtin_amdgcn_inverse_ballot_w64(m[2 * pr + 1][w]) ? vb[2 * pr + 1][w] : 0u;
+          pv[w] = lo | (hi << 16);
+        }
+        const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
 #pragma unroll
-            for (int b = 0; b < NB; ++b) acc[w][b] = __builtin_fmaf(v, xv[b], acc[w][b]);
-          }
+        for (int b = 0; b < NB; ++b) {
+          const uint32_t x2 = xp[b];
+#pragma unroll
+          for (int w = 0; w < WPC; ++w) acc[w][b] = dot2(pv[w], x2, acc[w][b]);
+        }
       }
     }
   };
