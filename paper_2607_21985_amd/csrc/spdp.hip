@@ -239,8 +239,15 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const int cols = A->cols;
   const int wave_cols = A->wave_cols;
   const uint32_t* const phase_p = A->phase;
+  const uint32_t* const col_info_p = A->col_info;
+  const uint32_t* const tile_offset_p = A->tile_offset;
+  const uint16_t* const x_p = A->x;
+  const void* const values = A->values;
+  const void* const bitmap = A->bitmap;
+  const uint32_t zero_col = A->zero_col;
   asm volatile("" ::"s"(n_seg0), "s"(batch), "s"(tk_log2), "s"(n_colblocks), "s"(code), "s"(cols),
-               "s"(wave_cols), "s"(phase_p));
+               "s"(wave_cols), "s"(phase_p), "s"(col_info_p), "s"(tile_offset_p), "s"(x_p), "s"(values),
+               "s"(bitmap), "s"(zero_col));
   if (local >= n_wg) return;  // the whole workgroup: no barrier has been reached
   const int r = (int)(local / n_seg0);
   const int seg = (int)(local - (uint32_t)r * n_seg0);
@@ -253,9 +260,6 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
 
-  // the stripe's phase: written by the previous call's last segment, read
-  // by every workgroup of the stripe before any of them publishes
-  const uint32_t phase = ((const_ptr<uint32_t>)phase_p)[r];
   const int k_begin = (seg * kWaves + wave) * wave_cols;
   const int range = max(0, min(wave_cols, cols - k_begin));
 
@@ -263,24 +267,32 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // trip (ColInfo/TileOffset are fetched for every column of the range, which
   // removes a dependent memory round trip; their cache lines are shared by
   // neighbouring columns, so little extra traffic results).
+  // All loads are unconditional so that they leave back to back and are
+  // waited for once: lanes past the range (and waves past the last column)
+  // read column k_begin's or column 0's entries, tokens past the batch read
+  // the last token; none of those is used below.
   constexpr int kChunks = kMaxWaveCols / 64;
   uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
+  const int k_safe = k_begin < cols ? k_begin : 0;
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const int off = 64 * c + lane;
-    const bool in = off < range;
-    const int k = k_begin + (in ? off : 0);
+    const int k = off < range ? k_begin + off : k_safe;
     const int g = g_row + (k >> tk_log2);
     colx[c] = ((uint32_t)g << tk_log2) + (uint32_t)(k & tk_mask);
-    ci[c] = 0u;
-    to[c] = 0u;
-    if (64 * c < range) {
-      ci[c] = A->col_info[colx[c]];
-      to[c] = A->tile_offset[g];
-    }
+    ci[c] = col_info_p[colx[c]];
+    to[c] = tile_offset_p[g];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) xb[c][b] = (in && b < batch) ? A->x[(size_t)b * cols + k] : 0u;
+    for (int b = 0; b < NB; ++b) xb[c][b] = x_p[(size_t)min(b, batch - 1) * cols + k];
   }
+  // the stripe's phase: written by the previous call's last segment, read
+  // by every workgroup of the stripe before any of them publishes (the
+  // kernel boundary makes the write visible, so an ordinary cached load
+  // serves). A vector load issued after the loads above, so that waiting for
+  // them does not wait for it (loads return in order), waited for after the
+  // list is built; a scalar load would share the LDS wait counter, and the
+  // compiler would wait for it at the first LDS barrier.
+  const uint32_t phase_lane = __hip_atomic_load(phase_p + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   // activity (union over the tokens), then the workgroup-wide list: each
   // wave's active columns follow those of the lower waves
   uint64_t actm[kChunks];
@@ -325,7 +337,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // bitmap array's zeroed tail) and the first 16 bytes of the values: they
   // decode to nothing.
   if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) {
-    ent_s[total + lane] = make_uint2(0u, A->zero_col << 6);
+    ent_s[total + lane] = make_uint2(0u, zero_col << 6);
 #pragma unroll
     for (int b = 0; b < NB; ++b) xs_s[(((total + lane) >> 1) * NB + b) * 2 + ((total + lane) & 1)] = 0;
   }
@@ -340,8 +352,6 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const int hsel = lane >> 5;
   const int q = lane & 31;
   unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
-  const void* const values = A->values;
-  const void* const bitmap = A->bitmap;
   // Values: lane l of load pr brings 16 bytes of column 2pr + (l >= 32),
   // chunk l & 31, to that column's 512-byte slot; lanes past a column's end
   // re-read its last chunk (a line the column loads anyway). Bitmaps: lane l
@@ -434,6 +444,12 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
   // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
   // requested after i) loads outstanding".
+  // The phase load is the only vector load the compiler tracks; it must have
+  // landed before the DMA loop: the compiler does not see the DMA loads, so
+  // a wait it placed for a load of its own inside the loop would count them
+  // and drain the pipeline.
+  const uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
+  asm volatile("" ::"s"(phase));
   const int n_first = min(n_mine, kSlots);
   for (int i = 0; i < n_first; ++i) issue(i);
   for (int i = 0; i < n_mine; ++i) {
