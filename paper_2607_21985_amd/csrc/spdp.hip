@@ -394,12 +394,17 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     uint32_t vb[kQuad][WPC];
 #pragma unroll
     for (int c = 0; c < kQuad; ++c) {
-      const uint16_t* vslot = reinterpret_cast<const uint16_t*>(slot + (u0 + c) * kSlotBytes);
-      uint32_t prefix = 0;
+      // running LDS byte address of the word's first value (scalar): one
+      // popcount and one shift-add per word
+      uint32_t sb = lds_addr(slot + (u0 + c) * kSlotBytes);
 #pragma unroll
       for (int w = 0; w < WPC; ++w) {
-        vb[c][w] = vslot[prefix + mbcnt64(m[c][w])];
-        prefix += (uint32_t)__builtin_popcountll(m[c][w]);
+        const uint32_t a = sb + 2u * mbcnt64(m[c][w]);
+        vb[c][w] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)a;
+        if (w + 1 < WPC) {
+          const uint32_t pop = (uint32_t)__builtin_popcountll(m[c][w]);
+          asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+        }
       }
     }
     // 4. accumulate in fp32. One token: the words become EXEC around single
