@@ -55,6 +55,13 @@ constexpr int kBatch = 4;                 // active columns per DMA batch (one d
 constexpr int kQuad = 4;                  // columns decoded together
 constexpr int kMaxWaveCols = 128;         // columns whose activity one wave tests
 constexpr int kMaxWgCols = kWaves * kMaxWaveCols;
+// With early first batches the workgroup list holds at most kMaxWgCols -
+// kWaves kBatch columns (each wave's first kBatch active columns form its
+// own first batch) plus the last batch's padding, and the waves' first
+// batches follow it at kFirstList; without, the list may use every entry.
+constexpr int kFirstList = kMaxWgCols - kWaves * kBatch + kBatch;
+static_assert(kFirstList % kBatch == 0 && kFirstList + kWaves * kBatch == kMaxWgCols + kBatch,
+              "list layout");
 constexpr int kMaxBatch = 32;
 constexpr int kBmBytes = kBatch * kMaxWords * 8;          // bitmap words of one batch
 constexpr int kBatchBytes = kBatch * kSlotBytes + kBmBytes;  // one ring slot
@@ -79,6 +86,10 @@ struct MatArgs {
   int segments;   // workgroups per row stripe
   int n_wg;       // segments * n_stripes
   uint32_t zero_col;  // column index whose bitmap lies in the zeroed tail padding
+  // nonzero: each wave requests its first batch before the workgroup list is
+  // built (a property of the product and the batch, never of the launch, so
+  // that grouping does not change the summation order)
+  int early_first;
 };
 
 // A launch runs up to kMaxGroup independent products (same tile height and
@@ -208,7 +219,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
 // column (tile_m / 64).
-template <int NB, int WPC>
+template <int NB, int WPC, bool EARLY>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
@@ -233,6 +244,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const uint32_t n_wg = (uint32_t)A->n_wg;
   const uint32_t n_seg0 = (uint32_t)A->segments;
   const int batch = L->batch;
+  const int early_first = EARLY ? A->early_first : 0;
   const int tk_log2 = A->tk_log2;
   const int n_colblocks = A->n_colblocks;
   const int code = A->code;
@@ -247,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const uint32_t zero_col = A->zero_col;
   asm volatile("" ::"s"(n_seg0), "s"(batch), "s"(tk_log2), "s"(n_colblocks), "s"(code), "s"(cols),
                "s"(wave_cols), "s"(phase_p), "s"(col_info_p), "s"(tile_offset_p), "s"(x_p), "s"(values),
-               "s"(bitmap), "s"(zero_col));
+               "s"(bitmap), "s"(zero_col), "s"(early_first));
   if (local >= n_wg) return;  // the whole workgroup: no barrier has been reached
   const int r = (int)(local / n_seg0);
   const int seg = (int)(local - (uint32_t)r * n_seg0);
@@ -293,8 +305,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // list is built; a scalar load would share the LDS wait counter, and the
   // compiler would wait for it at the first LDS barrier.
   const uint32_t phase_lane = __hip_atomic_load(phase_p + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  // activity (union over the tokens), then the workgroup-wide list: each
-  // wave's active columns follow those of the lower waves
+  // activity (union over the tokens)
   uint64_t actm[kChunks];
   int n_w = 0;
 #pragma unroll
@@ -309,57 +320,39 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     actm[c] = act;
     n_w += __builtin_popcountll(act);
   }
-  if (lane == 0) cnt_s[wave] = n_w;
-  __syncthreads();
-  int total = 0, pos = 0;
+  // list entry p of this lane's column of chunk c, with its masked
+  // activations (pair-interleaved: entries 2j and 2j+1 share a dword per
+  // token); entries of the all-zero column pad a batch: they read the
+  // bitmap array's zeroed tail and the first 16 bytes of the values, and
+  // decode to nothing
+  auto put = [&](int c, int p) __attribute__((always_inline)) {
+    const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
+    ent_s[p] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
 #pragma unroll
-  for (int v = 0; v < kWaves; ++v) {
-    const int cv = cnt_s[v];
-    pos += v < wave ? cv : 0;
-    total += cv;
-  }
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    if ((actm[c] >> lane) & 1) {
-      const int p = pos + (int)mbcnt64(actm[c]);
-      const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
-      ent_s[p] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int mag = (int)(xb[c][b] & 0x7FFFu);
-        const bool on = b < batch && mag > code && mag <= 0x7C00;
-        xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
-      }
+    for (int b = 0; b < NB; ++b) {
+      const int mag = (int)(xb[c][b] & 0x7FFFu);
+      const bool on = b < batch && mag > code && mag <= 0x7C00;
+      xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
     }
-    pos += __builtin_popcountll(actm[c]);
-  }
-  // Pad the last batch with entries that read an all-zero bitmap (in the
-  // bitmap array's zeroed tail) and the first 16 bytes of the values: they
-  // decode to nothing.
-  if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) {
-    ent_s[total + lane] = make_uint2(0u, zero_col << 6);
+  };
+  auto put_zero = [&](int p) __attribute__((always_inline)) {
+    ent_s[p] = make_uint2(0u, zero_col << 6);
 #pragma unroll
-    for (int b = 0; b < NB; ++b) xs_s[(((total + lane) >> 1) * NB + b) * 2 + ((total + lane) & 1)] = 0;
-  }
-  __syncthreads();
+    for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = 0;
+  };
 
-  // ---- 2. the batches are split evenly over the waves; each wave streams its
-  // share through its ring of kSlots batch slots (LDS DMA, no registers held
-  // by loads in flight) and decodes a batch as soon as its loads have landed.
-  const int n_bt = (total + kBatch - 1) / kBatch;
-  const int bb0 = n_bt * wave / kWaves;
-  const int n_mine = n_bt * (wave + 1) / kWaves - bb0;
-  const int hsel = lane >> 5;
-  const int q = lane & 31;
-  unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
+  // A batch = kBatch list entries, streamed through the wave's ring of kSlots
+  // batch slots in LDS (LDS DMA, no registers held by loads in flight).
   // Values: lane l of load pr brings 16 bytes of column 2pr + (l >= 32),
   // chunk l & 31, to that column's 512-byte slot; lanes past a column's end
   // re-read its last chunk (a line the column loads anyway). Bitmaps: lane l
   // < 16 WPC brings dword l of the batch's words (column l / (2 WPC)).
-  auto issue = [&](int i) __attribute__((always_inline)) {
-    const int e0 = (bb0 + i) * kBatch;
+  const int hsel = lane >> 5;
+  const int q = lane & 31;
+  unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
+  auto issue_at = [&](int e0, int si) __attribute__((always_inline)) {
     const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(
-        (int)lds_addr(my_ring + (i % kSlots) * kBatchBytes));
+        (int)lds_addr(my_ring + si * kBatchBytes));
 #pragma unroll
     for (int pr = 0; pr < kBatch / 2; ++pr) {
       const uint2 e = ent_s[e0 + 2 * pr + hsel];
@@ -370,6 +363,69 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       dma4(bitmap, (e.y >> 6) * (WPC * 8u) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
     }
   };
+
+  // ---- 2a. (when the launch asks for it) the wave's first batch: its own
+  // first kBatch active columns, listed at the tail of the list arrays and
+  // requested at once, so that their loads are in flight while the
+  // workgroup builds its list (two barriers) from the remaining columns. The phase load has landed with
+  // the loads above (loads return in order); it is read here because it is
+  // the only vector load the compiler tracks and must be complete before the
+  // first DMA: the compiler does not see those loads, so a wait it placed
+  // for a load of its own among them would count them and drain the ring.
+  const uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
+  asm volatile("" ::"s"(phase));
+  const bool has_first = EARLY && early_first && n_w > 0;
+  const int e_first = kFirstList + kBatch * wave;
+  if (has_first) {
+    int rank0 = 0;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if ((actm[c] >> lane) & 1) {
+        const int rk = rank0 + (int)mbcnt64(actm[c]);
+        if (rk < kBatch) put(c, e_first + rk);
+      }
+      rank0 += __builtin_popcountll(actm[c]);
+    }
+    if (lane >= n_w && lane < kBatch) put_zero(e_first + lane);
+    issue_at(e_first, 0);
+  }
+
+  // ---- 2b. the workgroup-wide list of the remaining active columns: each
+  // wave's follow those of the lower waves
+  const int n_skip = EARLY && has_first ? kBatch : 0;  // ranks already in the first batch
+  if (lane == 0) cnt_s[wave] = max(n_w - n_skip, 0);
+  __syncthreads();
+  int total = 0, pos = 0;
+#pragma unroll
+  for (int v = 0; v < kWaves; ++v) {
+    const int cv = cnt_s[v];
+    pos += v < wave ? cv : 0;
+    total += cv;
+  }
+  {
+    int rank0 = 0;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if ((actm[c] >> lane) & 1) {
+        const int rk = rank0 + (int)mbcnt64(actm[c]);
+        if (rk >= n_skip) put(c, pos + rk - n_skip);
+      }
+      rank0 += __builtin_popcountll(actm[c]);
+    }
+  }
+  // pad the list's last batch
+  if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) put_zero(total + lane);
+  __syncthreads();
+
+  // ---- 2c. the list's batches are split evenly over the waves; each wave
+  // streams its first batch, then its share, and decodes a batch as soon as
+  // its loads have landed.
+  const int n_bt = (total + kBatch - 1) / kBatch;
+  const int bb0 = n_bt * wave / kWaves;
+  const int n_first = EARLY && has_first ? 1 : 0;
+  const int n_mine = n_bt * (wave + 1) / kWaves - bb0 + n_first;
+  auto entry0 = [&](int i) { return n_first && i == 0 ? e_first : (bb0 + i - n_first) * kBatch; };
+  auto issue = [&](int i) __attribute__((always_inline)) { issue_at(entry0(i), i % kSlots); };
 
   // Decode of four columns of a landed batch. The bitmap words come from
   // scalar loads of the bitmap array (the batch's DMA has just brought their
@@ -449,14 +505,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
   // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
   // requested after i) loads outstanding".
-  // The phase load is the only vector load the compiler tracks; it must have
-  // landed before the DMA loop: the compiler does not see the DMA loads, so
-  // a wait it placed for a load of its own inside the loop would count them
-  // and drain the pipeline.
-  const uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
-  asm volatile("" ::"s"(phase));
-  const int n_first = min(n_mine, kSlots);
-  for (int i = 0; i < n_first; ++i) issue(i);
+  for (int i = n_first; i < min(n_mine, kSlots); ++i) issue(i);
   for (int i = 0; i < n_mine; ++i) {
     const int later = min(n_mine - 1 - i, kSlots - 1);
     if (later >= 3)
@@ -468,13 +517,13 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     else
       wait_vmcnt<0>();
     const unsigned char* slot = my_ring + (i % kSlots) * kBatchBytes;
-    const int e0 = (bb0 + i) * kBatch;
+    const int e0 = entry0(i);
     // byte offsets of the batch's bitmaps: lane u < 8 holds column u's
     const uint32_t bo_v = (ent_s[e0 + (lane & (kBatch - 1))].y >> 6) * (WPC * 8u);
 #pragma unroll
     for (int u0 = 0; u0 < kBatch; u0 += kQuad) {
       // a quad of padding entries only (past the workgroup's list) is skipped
-      if (u0 == 0 || total - e0 > u0) {
+      if (u0 == 0 || e0 >= kFirstList || total - e0 > u0) {
         uint64_t m[kQuad][WPC];
         load_masks(m, bo_v, u0);
         decode_quad(slot, e0, u0, m);
@@ -709,19 +758,42 @@ int upload(const std::vector<T>& v, void** dst) {
 }
 
 template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, dim3 grid, hipStream_t stream) {
-  hipLaunchKernelGGL((spmspv_kernel<NB, WPC>), grid, dim3(kThreads), 0, stream, args);
+hipError_t launch_one(const LaunchArgs& args, bool early, dim3 grid, hipStream_t stream) {
+  // only the one-token kernel has the early-first-batch form (no product with
+  // more tokens asks for it)
+  if constexpr (NB == 1) {
+    if (early) {
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true>), grid, dim3(kThreads), 0, stream, args);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, dim3 grid, hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, dim3 grid, hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, grid, stream);
-    case 2: return launch_one<NB, 2>(args, grid, stream);
-    case 3: return launch_one<NB, 3>(args, grid, stream);
-    default: return launch_one<NB, 4>(args, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, grid, stream);
+    default: return launch_one<NB, 4>(args, early, grid, stream);
   }
+}
+
+// Early first batches (each wave requests its own first four active columns
+// before the workgroup builds its list) pay where a product is latency-bound:
+// measured -6 % on a lone 4096x4096 product (512 workgroups), -2 % at
+// 11008x4096 (946); with five or more workgroups per CU, or with more than
+// one token, the latency is hidden anyway and the extra prologue work costs
+// 1-3 %. Decided per product (its own workgroups), so that a product gives
+// the same bits alone and in a group. SPDP_EARLY_FIRST=0 or 1 overrides (for
+// tuning).
+constexpr int64_t kEarlyFirstMaxWorkgroups = 1024;
+int early_first(int batch, int64_t workgroups) {
+  if (batch != 1) return 0;  // the form exists for one token only
+  if (const char* env = std::getenv("SPDP_EARLY_FIRST")) return std::atoi(env) != 0 ? 1 : 0;
+  return workgroups <= kEarlyFirstMaxWorkgroups ? 1 : 0;
 }
 
 // Validates one product of a call and fills its kernel arguments (sizing
@@ -771,6 +843,7 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   a.segments = segments;
   *n_wg = (int64_t)segments * h->n_stripes;
   a.n_wg = (int)*n_wg;
+  a.early_first = early_first(batch, *n_wg);
   return SPDP_OK;
 }
 
@@ -883,6 +956,7 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t
   std::memset(&la, 0, sizeof(la));
   la.batch = batch;
   int64_t widest = 0;
+  bool early = false;
   for (int i = 0; i < count; ++i) {
     int64_t n_wg = 0;
     const int st = prepare(handles[i], X[i], batch, thresholds[i], Y[i], dev, &la.m[i], &n_wg);
@@ -891,23 +965,24 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t
       return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
     if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
     widest = std::max(widest, n_wg);
+    early = early || la.m[i].early_first;
   }
 
   const int wpc = handles[0]->tile_m / 64;
   const dim3 grid((unsigned)widest, (unsigned)count);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (batch <= 1)
-    e = launch<1>(la, wpc, grid, s);
+    e = launch<1>(la, wpc, early, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, grid, s);
+    e = launch<2>(la, wpc, early, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, grid, s);
+    e = launch<4>(la, wpc, early, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, grid, s);
+    e = launch<8>(la, wpc, early, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, grid, s);
+    e = launch<16>(la, wpc, early, grid, s);
   else
-    e = launch<32>(la, wpc, grid, s);
+    e = launch<32>(la, wpc, early, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }

@@ -133,6 +133,32 @@ def test_small_against_oracle(rows, cols, tile, sw, p, batch):
     _check_full(w, x, t, tile, f"small {rows}x{cols} tile={tile} sw={sw} p={p} B={batch}")
 
 
+# Both launch forms, forced: each wave's first batch requested before the
+# workgroup list is built (SPDP_EARLY_FIRST=1) or all batches taken from the
+# list (0). The cases include waves left with fewer than four active columns
+# or none (high p), several tokens, and full 128-column waves with every
+# column active (the largest list either form builds).
+EARLY = [
+    # rows, cols, tile, sw, p, batch, splitk
+    (333, 517, (256, 16), 0.5, 0.5, 1, None),
+    (513, 1000, (256, 16), 0.6, 0.97, 1, None),
+    (700, 2900, (128, 8), 0.5, 0.9, 3, 7),
+    (300, 2048, (64, 1), 0.5, 0.5, 8, None),
+    (512, 1111, (256, 16), 0.6, 0.4, 32, None),
+    (1024, 8192, (256, 16), 0.5, 0.0, 1, 16),
+]
+
+
+@pytest.mark.parametrize("early", ["0", "1"])
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch,splitk", EARLY)
+def test_launch_forms_against_oracle(monkeypatch, early, rows, cols, tile, sw, p, batch, splitk):
+    monkeypatch.setenv("SPDP_EARLY_FIRST", early)
+    if splitk:
+        monkeypatch.setenv("SPDP_SPLITK", str(splitk))
+    w, x, t = _case(rows, cols, tile, sw, p, batch, rows * 5 + cols, cols * 7 + batch)
+    _check_full(w, x, t, tile, f"early={early} {rows}x{cols} tile={tile} sw={sw} p={p} B={batch}")
+
+
 def test_dense_no_threshold_is_gemv():
     w, x, _ = _case(300, 700, (256, 16), 0.0, 0.0, 2, 5, 6)
     _check_full(w, x, -1.0, (256, 16), "dense")
