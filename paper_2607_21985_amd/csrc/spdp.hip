@@ -644,11 +644,14 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       }
     }
   }
-  // every workgroup of the stripe has published (so has read the phase) by
-  // the time a reducer gets here, and the next call starts after this kernel
-  // ends: advance the tag (0 is skipped, the workspace's initial contents).
-  // A reducer still gathering keeps its own copy of the phase.
-  if (jr == n_red - 1 && threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
+  // Reducer 0 gathers row 0 of the stripe, a row that always exists (the
+  // last reducer's rows can all lie past a ragged end, and it would then wait
+  // for nothing), and its four waves together wait for every segment, so past
+  // its barriers every workgroup of the stripe has published, and so has
+  // read the phase; the next call starts after this kernel ends: advance the
+  // tag (0 is skipped, the workspace's initial contents). The other reducers
+  // keep their own copies of the phase.
+  if (jr == 0 && threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
 }
 
 using spdp::fail;
