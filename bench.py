@@ -63,6 +63,11 @@ def parse():
                          "(a known-size reference for hardware byte counters)")
     ap.add_argument("--group", choices=("decoder", "none"), default="decoder",
                     help="decoder: products that read one input are one grouped launch; none: one launch each")
+    ap.add_argument("--calibration", type=int, default=0, metavar="TOKENS",
+                    help="0: each input is thresholded at its own p-th |x| percentile (the workload "
+                         "definition); N > 0: each layer's threshold is the p-quantile of |x| over N "
+                         "separately drawn calibration tokens of that layer, applied to the inputs "
+                         "(offline calibration as in the paper's DP setup)")
     ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
                     help="graph: each step is one captured HIP graph of its calls (how a decode "
                          "loop runs them); stream: one host launch per call")
@@ -89,6 +94,13 @@ def call_bytes(fmt: dict, x16: np.ndarray, code: int) -> tuple[int, float]:
     b = x16.shape[0]
     total += 2 * b * K + 2 * b * M
     return total, float(act.mean())
+
+
+def dropped_fraction(x16: np.ndarray, code: int) -> float:
+    """Fraction of the entries (all tokens) the threshold drops: the realized
+    dynamic sparsity, decided by the kernel's integer rule."""
+    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
+    return float(1.0 - ((mag > code) & (mag <= 0x7C00)).mean()) if mag.size else 0.0
 
 
 def kernel_source_sha() -> str:
@@ -187,12 +199,23 @@ def main():
         for proj in wl["projections"]:
             pruned[(sw, proj.name)] = spdp.prune_magnitude(proj.weight(), sw)
     xs = {proj.name: proj.activations(batch) for proj in wl["projections"]}
+    # offline calibration sets: one per layer input (projections that read
+    # one input share it), drawn apart from the inputs (draw 1)
+    cal = {}
+    if args.calibration > 0:
+        for proj in wl["projections"]:
+            key = (proj.x_seed, proj.x_kind, proj.cols)
+            if key not in cal:
+                cal[key] = proj.activations(args.calibration, draw=1)
     points = []
     for sw in wl["weight_sparsity"]:
         for p in wl["act_sparsity"]:
             for proj in wl["projections"]:
                 x = xs[proj.name]
-                t = spdp.calibrate_threshold(x, p)
+                if cal:
+                    t = spdp.calibrate_threshold(cal[(proj.x_seed, proj.x_kind, proj.cols)], p)
+                else:
+                    t = spdp.calibrate_threshold(x, p)
                 points.append({"sw": sw, "p": p, "proj": proj, "x": x, "t": t,
                                "w": pruned[(sw, proj.name)],
                                "label": f"{proj.name}@sw{sw:g}/p{p:g}"})
@@ -205,6 +228,7 @@ def main():
     for pt, m in zip(points, copy0):
         f = m.format()
         pt["bytes"], pt["active_frac"] = call_bytes(f, pt["x"], spdp.threshold_code(pt["t"]))
+        pt["dropped"] = dropped_fraction(pt["x"], spdp.threshold_code(pt["t"]))
         pt["rows"], pt["cols"] = f["rows"], f["cols"]
         del f
     # one device copy of each distinct input per rotation copy (grouped
@@ -411,6 +435,7 @@ def main():
         d = {"sw": grp[0]["sw"], "p": grp[0]["p"], "us_per_call": round(us, 3),
              "gbs": round(byts / (us * n_proj * 1e-6) / 1e9, 1),
              "active_frac": round(float(np.mean([pt["active_frac"] for pt in grp])), 4),
+             "act_sparsity_realized": round(float(np.mean([pt["dropped"] for pt in grp])), 4),
              "bytes_per_call": int(byts / n_proj)}
         if dense:
             d["speedup_vs_dense"] = round(dense["us_per_call"] / us, 3)
@@ -445,6 +470,10 @@ def main():
             "batch": batch, "tile": list(tile), "calls_per_step": len(points),
             "launches_per_step": n_launch, "grouping": args.group,
             "rotation_copies": n_copies, "accumulate": "f32",
+            "threshold": ({"rule": "offline calibration", "calibration_tokens": args.calibration,
+                           "how": "p-quantile of |x| over separately drawn tokens of each layer input"}
+                          if args.calibration > 0 else
+                          {"rule": "own percentile", "how": "p-quantile of |x| over the input itself"}),
         },
         "us_per_call": round(us_per_call, 3),
         "us_per_call_ungrouped": round(single_ms * 1e3 / len(points), 3),

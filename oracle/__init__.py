@@ -55,6 +55,8 @@ __all__ = [
     "TiledCBC",
     "magnitude_prune",
     "threshold_for",
+    "calibrated_threshold",
+    "realized_sparsity",
     "active_mask",
     "masked_activations",
     "encode",
@@ -143,6 +145,26 @@ def threshold_for(x: np.ndarray, p: float) -> np.float32:
     v = np.sort(np.abs(x.astype(np.float64)).reshape(-1))
     idx = int(math.ceil(p * v.size)) - 1
     return np.float32(v[idx])
+
+
+def calibrated_threshold(samples: np.ndarray, p: float) -> np.float32:
+    """A layer's threshold calibrated offline (Sec. 5.1, the DP setup).
+
+    The layer's activation magnitudes over a calibration set (tokens drawn
+    separately from the inputs the threshold is later applied to) form an
+    empirical CDF; the threshold for a target dynamic sparsity p is its
+    p-quantile. That is the quantile rule of ``threshold_for`` applied to the
+    calibration set instead of to the input itself.
+    """
+    return threshold_for(samples, p)
+
+
+def realized_sparsity(x: np.ndarray, t: float) -> float:
+    """Fraction of the entries of ``x`` the rule ``|x| > t`` drops."""
+    x = np.asarray(x, dtype=np.float16)
+    if x.size == 0:
+        return 0.0
+    return float(1.0 - active_mask(x.reshape(1, -1), t).mean())
 
 
 def active_mask(x: np.ndarray, t: float) -> np.ndarray:

@@ -15,7 +15,11 @@ decode time, Sec. 5.3; activations thresholded TEAL-style, Sec. 2.2 and 5.1):
 * down-projection inputs: SiLU(g) * u of standard-normal pre-activations.
 
 Every array is returned as ``numpy.float16``. Draw order is fixed as written
-so that a (shape, seed) pair always yields the same bits.
+so that a (shape, seed) pair always yields the same bits. ``draw`` > 0 gives
+further, independent tokens of the same layer (a calibration set or held-out
+inputs): their own random stream, the layer's outlier channels kept (those
+belong to the layer, as in a trained model); ``draw`` = 0 is the original
+draw.
 """
 
 from __future__ import annotations
@@ -47,19 +51,21 @@ def weights(rows: int, cols: int, seed: int) -> np.ndarray:
     return g.astype(np.float16)
 
 
-def laplace_activations(batch: int, cols: int, seed: int) -> np.ndarray:
+def laplace_activations(batch: int, cols: int, seed: int, draw: int = 0) -> np.ndarray:
     """fp16 activations ``batch x cols``: Laplace(0, 1), 1 % outlier channels x20."""
     rng = np.random.default_rng(seed)
     n_out = int(round(0.01 * cols))
     outliers = rng.choice(cols, n_out, replace=False)
+    if draw:
+        rng = np.random.default_rng((seed, draw))
     x = rng.laplace(0.0, 1.0, (batch, cols))
     x[:, outliers] *= 20.0
     return x.astype(np.float16)
 
 
-def swiglu_activations(batch: int, cols: int, seed: int) -> np.ndarray:
+def swiglu_activations(batch: int, cols: int, seed: int, draw: int = 0) -> np.ndarray:
     """fp16 down-projection inputs ``SiLU(g) * u`` with g, u ~ N(0, 1)."""
-    rng = np.random.default_rng(seed)
+    rng = np.random.default_rng((seed, draw) if draw else seed)
     g = rng.normal(0.0, 1.0, (batch, cols))
     u = rng.normal(0.0, 1.0, (batch, cols))
     x = g / (1.0 + np.exp(-g)) * u
@@ -80,11 +86,11 @@ class Projection:
     def weight(self) -> np.ndarray:
         return weights(self.rows, self.cols, self.w_seed)
 
-    def activations(self, batch: int) -> np.ndarray:
+    def activations(self, batch: int, draw: int = 0) -> np.ndarray:
         if self.x_kind == "laplace":
-            return laplace_activations(batch, self.cols, self.x_seed)
+            return laplace_activations(batch, self.cols, self.x_seed, draw)
         if self.x_kind == "swiglu":
-            return swiglu_activations(batch, self.cols, self.x_seed)
+            return swiglu_activations(batch, self.cols, self.x_seed, draw)
         raise ValueError(f"unknown activation kind {self.x_kind!r}")
 
 

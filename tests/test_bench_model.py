@@ -22,3 +22,13 @@ def test_call_bytes_matches_oracle(rows, cols, tile, sw, p, batch):
     ref = oracle.encode(w, *tile)
     assert got == oracle.algorithmic_bytes(ref, x, t)
     assert frac == pytest.approx(oracle.active_mask(x, t).any(axis=0).mean())
+
+
+@pytest.mark.parametrize("p,batch,draw_t", [(0.5, 1, 0), (0.25, 4, 1), (0.7, 2, 1), (0.0, 1, 0)])
+def test_dropped_fraction_matches_oracle(p, batch, draw_t):
+    """Realized dynamic sparsity as the bench reports it, with the threshold
+    taken from the input itself (draw 0) or from a calibration set (draw 1)."""
+    x = synth.laplace_activations(batch, 2048, 9)
+    src = x if draw_t == 0 else synth.laplace_activations(100, 2048, 9, draw=1)
+    t = float(oracle.calibrated_threshold(src, p))
+    assert bench.dropped_fraction(x, spdp.threshold_code(t)) == oracle.realized_sparsity(x, t)

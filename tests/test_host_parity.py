@@ -79,6 +79,14 @@ def test_calibrate_matches_oracle(p, kind, b, k, seed):
     assert np.float32(spdp.calibrate_threshold(x, p)) == oracle.threshold_for(x, p)
 
 
+def test_calibrate_on_a_calibration_set_matches_oracle():
+    """Offline calibration over 300 separately drawn tokens of a layer."""
+    for x in (synth.laplace_activations(300, 4096, 211, draw=1),
+              synth.swiglu_activations(300, 11008, 313, draw=1)):
+        for p in (0.25, 0.5, 0.7):
+            assert np.float32(spdp.calibrate_threshold(x, p)) == oracle.calibrated_threshold(x, p)
+
+
 def test_calibrate_empty_and_ties():
     assert spdp.calibrate_threshold(np.zeros(0, dtype=np.float16), 0.5) == -1.0
     x = np.array([[1.0, -1.0, 1.0, 2.0, 0.0, -0.0, 3.0, 1.0]], dtype=np.float16)

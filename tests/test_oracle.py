@@ -247,6 +247,67 @@ def test_threshold_with_ties():
     assert act.tolist() == [[False, False, False, True, False, False, True, False]]
 
 
+# ---------------------------------------------------------------------------
+# Offline calibration (Sec. 5.1, the DP setup): a layer's threshold is the
+# quantile of the empirical CDF of its activation magnitudes over a separate
+# calibration set, then applied to inputs the calibration never saw.
+
+def _mixture_quantile(p, frac_out, scale=20.0):
+    """p-quantile of |x| for Laplace(0, 1) entries of which a fraction
+    frac_out is scaled by `scale`: F(t) = (1 - f)(1 - e^-t) + f(1 - e^(-t/scale)),
+    solved by bisection."""
+    lo, hi = 0.0, 1000.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        f = (1 - frac_out) * (1 - math.exp(-mid)) + frac_out * (1 - math.exp(-mid / scale))
+        lo, hi = (mid, hi) if f < p else (lo, mid)
+    return 0.5 * (lo + hi)
+
+
+@pytest.mark.parametrize("p", [0.25, 0.5, 0.7])
+def test_calibrated_threshold_is_the_distributions_quantile(p):
+    k = 4096
+    cal = synth.laplace_activations(300, k, 211, draw=1)
+    t = float(oracle.calibrated_threshold(cal, p))
+    exact = _mixture_quantile(p, round(0.01 * k) / k)
+    # the quantile of 1.2 M draws deviates by < 1e-3 (standard error ~ 2e-4
+    # to 5e-4 here), fp16 rounding of |x| near t by < 4e-4
+    assert abs(t - exact) < 5e-3, (t, exact)
+
+
+def test_calibrated_threshold_holds_on_unseen_tokens():
+    cal = synth.laplace_activations(300, 4096, 211, draw=1)
+    held = synth.laplace_activations(64, 4096, 211, draw=2)
+    x = synth.laplace_activations(1, 4096, 211)
+    for p in (0.25, 0.5, 0.7):
+        t = oracle.calibrated_threshold(cal, p)
+        # 262144 held-out entries: standard deviation of the fraction < 1e-3
+        assert abs(oracle.realized_sparsity(held, t) - p) < 0.01
+        # the input's own percentile drops p of it, up to ties at t
+        assert abs(oracle.realized_sparsity(x, oracle.threshold_for(x, p)) - p) < 5e-3
+
+
+def test_realized_sparsity_counts_dropped_entries():
+    x = np.array([[1.0, -1.0, 0.5, 2.0], [0.0, -3.0, 1.0, 0.25]], dtype=np.float16)
+    assert oracle.realized_sparsity(x, 1.0) == 6 / 8      # |x| > 1 keeps 2.0 and -3.0
+    assert oracle.realized_sparsity(x, -1.0) == 0.0
+    assert oracle.realized_sparsity(x, 3.0) == 1.0
+
+
+def test_calibration_draws_keep_the_layers_outlier_channels():
+    base = synth.laplace_activations(2, 512, 77)
+    assert np.array_equal(base.view(np.uint16), synth.laplace_activations(2, 512, 77, draw=0).view(np.uint16))
+    d1 = synth.laplace_activations(200, 512, 77, draw=1)
+    d2 = synth.laplace_activations(200, 512, 77, draw=2)
+    assert not np.array_equal(d1.view(np.uint16), d2.view(np.uint16))
+    # the 5 outlier channels (1 % of 512) stand out in both draws
+    top = [set(np.argsort(-np.abs(d.astype(np.float64)).mean(axis=0))[:5].tolist()) for d in (d1, d2)]
+    assert top[0] == top[1]
+    s0 = synth.swiglu_activations(2, 300, 5)
+    assert np.array_equal(s0.view(np.uint16), synth.swiglu_activations(2, 300, 5, draw=0).view(np.uint16))
+    assert not np.array_equal(s0.view(np.uint16), synth.swiglu_activations(2, 300, 5, draw=1).view(np.uint16))
+
+
 def test_active_mask_elementwise_definition():
     bits = np.arange(0, 1 << 16, dtype=np.uint32).astype(np.uint16)
     x = bits.view(np.float16).reshape(1, -1)
