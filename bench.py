@@ -41,6 +41,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
+# MI355X published fp32 vector peak: 256 CUs x 4 SIMDs x 64 lanes x 4 flops
+# per cycle (a two-wide fp32 FMA, or v_dot2_f32_f16's two fp16 products added
+# into fp32) x 2.4 GHz
+VEC_PEAK_TFLOPS = 157.3
 
 
 def parse():
@@ -94,6 +98,17 @@ def call_bytes(fmt: dict, x16: np.ndarray, code: int) -> tuple[int, float]:
     b = x16.shape[0]
     total += 2 * b * K + 2 * b * M
     return total, float(act.mean())
+
+
+def call_flops(fmt: dict, x16: np.ndarray, code: int) -> int:
+    """Useful flops of one call: 2 x the (token, nonzero weight of an active
+    column) products, the work the method cannot avoid."""
+    R, C, tk = fmt["n_stripes"], fmt["n_colblocks"], fmt["tile_k"]
+    K = fmt["cols"]
+    nnz_col = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64).sum(axis=0)[:K]
+    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
+    act = (mag > code) & (mag <= 0x7C00)                          # [B, K]
+    return int(2 * (act * nnz_col[None, :]).sum())
 
 
 def dropped_fraction(x16: np.ndarray, code: int) -> float:
@@ -229,6 +244,7 @@ def main():
         f = m.format()
         pt["bytes"], pt["active_frac"] = call_bytes(f, pt["x"], spdp.threshold_code(pt["t"]))
         pt["dropped"] = dropped_fraction(pt["x"], spdp.threshold_code(pt["t"]))
+        pt["flops"] = call_flops(f, pt["x"], spdp.threshold_code(pt["t"]))
         pt["rows"], pt["cols"] = f["rows"], f["cols"]
         del f
     # one device copy of each distinct input per rotation copy (grouped
@@ -360,6 +376,11 @@ def main():
         per_call[k:k + n_proj] = ms / (reps * n_proj)
     kern_ms = ms_per_step
     achieved = step_bytes / (kern_ms * 1e-3) / 1e9
+    # the two roofs: T_roof = max(bytes / HBM peak, useful flops / vector peak)
+    step_flops = sum(pt["flops"] for pt in points)
+    t_hbm_us = step_bytes / (HBM_PEAK_GBS * 1e9) * 1e6
+    t_alu_us = step_flops / (VEC_PEAK_TFLOPS * 1e12) * 1e6
+    alu_bound = t_alu_us > t_hbm_us
     graphs.clear()
 
     # ---- measured streaming peaks on this GPU: a 1 GiB device copy (read +
@@ -484,9 +505,15 @@ def main():
         "measured_peaks": peaks,
         "pct_of_measured_read_peak": round(100 * value / peaks["read_gbs"], 2),
         "roofline": {
-            "bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            **({"bound": "alu", "achieved": round(step_flops / (kern_ms * 1e-3) / 1e12, 3),
+                "peak": VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(t_alu_us / (kern_ms * 1e3), 4)} if alu_bound else
+               {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}),
             "traffic": traffic,
+            "t_roof_us_per_step": {"hbm": round(t_hbm_us, 3), "alu": round(t_alu_us, 3),
+                                   "binding": "alu" if alu_bound else "hbm"},
+            "useful_flops_per_launch": int(step_flops / n_launch),
             "kernel": "spmspv_kernel",
             "kernel_us_per_launch": round(kernel_us, 3),
             "duration_source": "HIP events around the timed steps on the launch stream "

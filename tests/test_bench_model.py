@@ -32,3 +32,15 @@ def test_dropped_fraction_matches_oracle(p, batch, draw_t):
     src = x if draw_t == 0 else synth.laplace_activations(100, 2048, 9, draw=1)
     t = float(oracle.calibrated_threshold(src, p))
     assert bench.dropped_fraction(x, spdp.threshold_code(t)) == oracle.realized_sparsity(x, t)
+
+
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch", [
+    (700, 900, (256, 16), 0.6, 0.25, 1), (300, 1000, (128, 8), 0.5, 0.0, 3),
+    (333, 517, (192, 4), 0.7, 0.5, 8), (129, 2000, (64, 64), 0.5, 0.6, 32),
+])
+def test_call_flops_matches_oracle(rows, cols, tile, sw, p, batch):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows * cols), sw)
+    x = synth.laplace_activations(batch, cols, 11)
+    t = float(oracle.threshold_for(x, p))
+    f = spdp.encode_host(w, tile).format()
+    assert bench.call_flops(f, x, spdp.threshold_code(t)) == oracle.useful_flops(w, x, t)
