@@ -175,6 +175,47 @@ __device__ __forceinline__ void masked_fma_column(float (&acc)[WPC][1], const ui
 #undef SPDP_COLUMN
 #undef SPDP_FMA
 
+// The same for two tokens: one EXEC word, then one FMA per token (x0, x1:
+// the tokens' dwords of the column's pair, the half picked by op_sel).
+#define SPDP_FMA2(W, SEL) "v_fma_mix_f32 %[a" #W "0], %[v" #W "], %[x0], %[a" #W "0] " SEL "\n\t" \
+                            "v_fma_mix_f32 %[a" #W "1], %[v" #W "], %[x1], %[a" #W "1] " SEL "\n\t"
+#define SPDP_COLUMN2(SEL) \
+  if constexpr (WPC == 1) {                                                          \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA2(0, SEL) "s_mov_b64 exec, %[sv]" \
+                 : [a00] "+v"(acc[0][0]), [a01] "+v"(acc[0][1]), [sv] "=&s"(save) \
+                 : [m0] "s"(m[0]), [v0] "v"(v[0]), [x0] "v"(x0), [x1] "v"(x1) \
+                 : "scc"); \
+  } else if constexpr (WPC == 2) {                                                          \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA2(0, SEL) "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA2(1, SEL) "s_mov_b64 exec, %[sv]" \
+                 : [a00] "+v"(acc[0][0]), [a01] "+v"(acc[0][1]), [a10] "+v"(acc[1][0]), [a11] "+v"(acc[1][1]), [sv] "=&s"(save) \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [v0] "v"(v[0]), [v1] "v"(v[1]), [x0] "v"(x0), [x1] "v"(x1) \
+                 : "scc"); \
+  } else if constexpr (WPC == 3) {                                                          \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA2(0, SEL) "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA2(1, SEL) "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA2(2, SEL) "s_mov_b64 exec, %[sv]" \
+                 : [a00] "+v"(acc[0][0]), [a01] "+v"(acc[0][1]), [a10] "+v"(acc[1][0]), [a11] "+v"(acc[1][1]), [a20] "+v"(acc[2][0]), [a21] "+v"(acc[2][1]), [sv] "=&s"(save) \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [x0] "v"(x0), [x1] "v"(x1) \
+                 : "scc"); \
+  } else if constexpr (WPC == 4) {                                                          \
+    asm volatile("s_and_saveexec_b64 %[sv], %[m0]\n\t" SPDP_FMA2(0, SEL) "s_and_b64 exec, %[sv], %[m1]\n\t" SPDP_FMA2(1, SEL) "s_and_b64 exec, %[sv], %[m2]\n\t" SPDP_FMA2(2, SEL) "s_and_b64 exec, %[sv], %[m3]\n\t" SPDP_FMA2(3, SEL) "s_mov_b64 exec, %[sv]" \
+                 : [a00] "+v"(acc[0][0]), [a01] "+v"(acc[0][1]), [a10] "+v"(acc[1][0]), [a11] "+v"(acc[1][1]), [a20] "+v"(acc[2][0]), [a21] "+v"(acc[2][1]), [a30] "+v"(acc[3][0]), [a31] "+v"(acc[3][1]), [sv] "=&s"(save) \
+                 : [m0] "s"(m[0]), [m1] "s"(m[1]), [m2] "s"(m[2]), [m3] "s"(m[3]), [v0] "v"(v[0]), [v1] "v"(v[1]), [v2] "v"(v[2]), [v3] "v"(v[3]), [x0] "v"(x0), [x1] "v"(x1) \
+                 : "scc"); \
+  }
+template <int WPC, bool XHI>
+__device__ __forceinline__ void masked_fma_column2(float (&acc)[WPC][2], const uint32_t (&v)[WPC], uint32_t x0,
+                                                   uint32_t x1, const uint64_t (&m)[WPC]) {
+  uint64_t save;
+  static_assert(WPC >= 1 && WPC <= 4, "at most four bitmap words per column");
+  if constexpr (XHI) {
+    SPDP_COLUMN2("op_sel:[0,1,0] op_sel_hi:[1,1,0]")
+  } else {
+    SPDP_COLUMN2("op_sel_hi:[1,1,0]")
+  }
+}
+#undef SPDP_COLUMN2
+#undef SPDP_FMA2
+
+
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 // acc + lo(v) * lo(x) + hi(v) * hi(x) in fp32 (fp16 products are exact in fp32)
@@ -463,13 +504,22 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
         }
       }
     }
-    // 4. accumulate in fp32. One token: the words become EXEC around single
-    // FMAs (v_fma_mix, fp16 operands; no branch, no select). More tokens:
-    // lanes whose bit is clear are zeroed (v_cndmask on the word), the two
-    // columns of a pair are packed into one register, and one dot product
-    // per token (v_dot2_f32_f16 against the pair's two activations) adds
-    // both columns: NB/2 instructions per word instead of NB.
-    if constexpr (NB == 1) {
+    // 4. accumulate in fp32. One or two tokens: the words become EXEC around
+    // single FMAs (v_fma_mix, fp16 operands; no branch, no select), NB per
+    // word. More tokens: lanes whose bit is clear are zeroed (v_cndmask on
+    // the word), the two columns of a pair are packed into one register, and
+    // one dot product per token (v_dot2_f32_f16 against the pair's two
+    // activations) adds both columns: 1.5 + NB/2 instructions per word
+    // instead of NB, fewer from four tokens on.
+    if constexpr (NB == 2) {
+#pragma unroll
+      for (int pr = 0; pr < 2; ++pr) {
+        // the pair's dwords of tokens 0 and 1 (low half column 2pr)
+        const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
+        masked_fma_column2<WPC, false>(acc, vb[2 * pr], xq.x, xq.y, m[2 * pr]);
+        masked_fma_column2<WPC, true>(acc, vb[2 * pr + 1], xq.x, xq.y, m[2 * pr + 1]);
+      }
+    } else if constexpr (NB == 1) {
       const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[e0 + u0]);
 #pragma unroll
       for (int c = 0; c < kQuad; ++c) {
