@@ -218,6 +218,21 @@ __device__ __forceinline__ void masked_fma_column2(float (&acc)[WPC][2], const u
 
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
+// {a where word ma has the lane's bit, else 0} | {b likewise under mb} << 16,
+// for a and b zero-extended fp16 bits: two selects that each write one half
+// of the result (SDWA, the other half kept), the words as VCC.
+__device__ __forceinline__ uint32_t pair_under_words(uint32_t a, uint32_t b, uint64_t ma, uint64_t mb) {
+  uint32_t p;
+  asm("s_mov_b64 vcc, %[ma]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[a], vcc dst_sel:WORD_0 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0\n\t"
+      "s_mov_b64 vcc, %[mb]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[b], vcc dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0"
+      : [p] "=&v"(p)
+      : [a] "v"(a), [b] "v"(b), [ma] "s"(ma), [mb] "s"(mb)
+      : "vcc");
+  return p;
+}
+
 // acc + lo(v) * lo(x) + hi(v) * hi(x) in fp32 (fp16 products are exact in fp32)
 __device__ __forceinline__ float dot2(uint32_t v, uint32_t x, float acc) {
   return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, v), __builtin_bit_cast(half2_t, x), acc, false);
@@ -506,11 +521,11 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     }
     // 4. accumulate in fp32. One or two tokens: the words become EXEC around
     // single FMAs (v_fma_mix, fp16 operands; no branch, no select), NB per
-    // word. More tokens: lanes whose bit is clear are zeroed (v_cndmask on
-    // the word), the two columns of a pair are packed into one register, and
-    // one dot product per token (v_dot2_f32_f16 against the pair's two
-    // activations) adds both columns: 1.5 + NB/2 instructions per word
-    // instead of NB, fewer from four tokens on.
+    // word. More tokens: the two columns of a pair are selected into the
+    // halves of one register (zero where the bit is clear: one SDWA select
+    // per column word) and one dot product per token (v_dot2_f32_f16 against
+    // the pair's two activations) adds both columns: 1 + NB/2 instructions
+    // per word instead of NB, fewer from four tokens on.
     if constexpr (NB == 2) {
 #pragma unroll
       for (int pr = 0; pr < 2; ++pr) {
@@ -534,11 +549,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       for (int pr = 0; pr < 2; ++pr) {
         uint32_t pv[WPC];
 #pragma unroll
-        for (int w = 0; w < WPC; ++w) {
-          const uint32_t lo = __builtin_amdgcn_inverse_ballot_w64(m[2 * pr][w]) ? vb[2 * pr][w] : 0u;
-          const uint32_t hi = __builtin_amdgcn_inverse_ballot_w64(m[2 * pr + 1][w]) ? vb[2 * pr + 1][w] : 0u;
-          pv[w] = lo | (hi << 16);
-        }
+        for (int w = 0; w < WPC; ++w) pv[w] = pair_under_words(vb[2 * pr][w], vb[2 * pr + 1][w], m[2 * pr][w], m[2 * pr + 1][w]);
         const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
 #pragma unroll
         for (int b = 0; b < NB; ++b) {
