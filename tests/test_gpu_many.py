@@ -66,6 +66,33 @@ def test_many_matches_oracle_and_single_calls(shapes, tile, sw, p, batch, share_
         m.close()
 
 
+def test_many_mixes_early_and_plain_first_batches(monkeypatch):
+    """One token: a product of at most 1024 workgroups requests each wave's
+    first batch before the list is built, a larger one does not; in one
+    launch both forms run, and each product still gives the bits of its
+    single call. 64 segments make the 4200-row product 17 x 64 = 1088
+    workgroups."""
+    monkeypatch.setenv("SPDP_SPLITK", "64")
+    dev = _dev()
+    prods = _products([(4200, 4096), (512, 1024), (1300, 4096)], 0.6, 0.5, 1, 1234)
+    mats = [spdp.encode(w, (256, 16)) for w, _, _ in prods]
+    Xs = [_to_dev(x) for _, x, _ in prods]
+    Yg = [torch.full((1, m.rows), float("nan"), dtype=torch.float16, device=dev) for m in mats]
+    print("[gpu] many: mixed first-batch forms", flush=True)
+    spdp.spmspv_many(mats, Xs, [t for _, _, t in prods], Yg)
+    torch.cuda.synchronize()
+    for i, ((w, x, t), m, X, Y) in enumerate(zip(prods, mats, Xs, Yg)):
+        y = Y.cpu().numpy().astype(np.float64)
+        y64, s64, _ = oracle.spmspv(w, x, t)
+        _assert_close(y, y64, s64, f"product {i}")
+        Ys = torch.full_like(Y, float("nan"))
+        m.spmspv_into(X, t, Ys)
+        torch.cuda.synchronize()
+        assert torch.equal(Ys, Y), f"product {i}: grouped result differs from the single call"
+    for m in mats:
+        m.close()
+
+
 def test_many_repeated_and_graph_replayed():
     """Grouped calls back to back, then captured and replayed with eager calls
     in between: every result equals the first eager one."""
