@@ -118,12 +118,20 @@ def dropped_fraction(x16: np.ndarray, code: int) -> float:
     return float(1.0 - ((mag > code) & (mag <= 0x7C00)).mean()) if mag.size else 0.0
 
 
-def kernel_source_sha() -> str:
-    h = hashlib.sha256()
-    for f in ("spdp.hip",):
-        with open(os.path.join(ROOT, "paper_2607_21985_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
+def _code_only(src: str) -> str:
+    """Source text without comments and with whitespace collapsed, so that a
+    comment edit does not count as a kernel change."""
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
+def kernel_source_sha(src: str | None = None) -> str:
+    """Hash of the kernel source's code (comments and layout ignored)."""
+    if src is None:
+        with open(os.path.join(ROOT, "paper_2607_21985_amd", "csrc", "spdp.hip")) as fh:
+            src = fh.read()
+    return hashlib.sha256(_code_only(src).encode()).hexdigest()[:16]
 
 
 def read_traffic(workload: str, group: str):

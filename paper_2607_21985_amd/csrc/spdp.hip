@@ -18,20 +18,25 @@
 //      streams its batches through a two-slot ring in LDS with global->LDS
 //      DMA (16-byte loads of the padded values, two columns per instruction,
 //      plus the batch's bitmap words), so loads in flight hold no registers;
+//      on small one-token products each wave first requests a batch of its
+//      own first active columns, before the list is built;
 //   3. bitmap decode (HAD-SMBD, Sec. 4.2.1): the bitmap words come from
 //      scalar loads (their lines are in L2 once the batch's DMA has landed);
 //      lane i of word w reads its value at the word's masked popcount below
 //      bit i (v_mbcnt_lo/hi, the paper's MaskedPopcount) plus the popcount of
 //      the column's earlier words;
-//   4. accumulate in fp32 on the vector ALUs with fp16 operands (v_fma_mix
-//      under EXEC = the bitmap word: rows without a nonzero do nothing), no
-//      matrix cores (Sec. 3.3 challenge 2, Sec. 4.2 step 5);
+//   4. accumulate in fp32 on the vector ALUs with fp16 operands: one or two
+//      tokens, v_fma_mix under EXEC = the bitmap word (rows without a nonzero
+//      do nothing); more tokens, the two columns of a pair selected into the
+//      halves of one register and one v_dot2_f32_f16 per token; no matrix
+//      cores (Sec. 3.3 challenge 2, Sec. 4.2 step 5);
 //   5. split-K (Sec. 4.2.3): each workgroup reduces its 4 waves in LDS and
 //      stores its fp32 partial sums to the product's workspace, each value
 //      paired with the stripe's phase number in one 8-byte store; the
 //      stripe's last segments gather the partials until every one carries
 //      the current phase, add them in a fixed order, write fp16 Y (round to
-//      nearest even) and advance the stripe's phase for the next call. No
+//      nearest even), and the first of them advances the stripe's phase for
+//      the next call. No
 //      counter, no fence, no host-side state: a partial is usable as soon as
 //      its own store has landed, and a captured graph replays correctly.
 

@@ -44,3 +44,9 @@ def test_call_flops_matches_oracle(rows, cols, tile, sw, p, batch):
     t = float(oracle.threshold_for(x, p))
     f = spdp.encode_host(w, tile).format()
     assert bench.call_flops(f, x, spdp.threshold_code(t)) == oracle.useful_flops(w, x, t)
+
+
+def test_kernel_hash_ignores_comments_and_layout():
+    src = "int f(int a) { // one\n  return a + 1; /* two\n three */ }\n"
+    assert bench.kernel_source_sha(src) == bench.kernel_source_sha("int f(int a) {\n return a + 1; }")
+    assert bench.kernel_source_sha(src) != bench.kernel_source_sha("int f(int a) { return a + 2; }")
