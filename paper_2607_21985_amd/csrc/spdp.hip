@@ -728,23 +728,28 @@ int hip_fail(hipError_t e, const char* what) {
 
 // Split-K heuristic. Each wave tests and streams a K range of wave_cols
 // columns (a multiple of 16); a product's grid is stripes x segments with
-// segments = ceil(cols / (4 wave_cols)). Measured on the Llama shapes, about
-// 48 columns per wave is fastest as long as the product has between 512 (two
-// per CU) and 1792 (the seven per CU that fit at once) workgroups; outside
-// that band the range moves in steps of 16 columns (at most kMaxWaveCols,
-// and at most kMaxSegments segments, which the gather reads per row).
-// This gives 4096x4096: 32 segments, 11008x4096: 22, 13824x5120: 27,
-// 28672x8192: 16 (each the fastest of a sweep). SPDP_SPLITK overrides the
-// number of segments (for tuning).
-constexpr int kPreferredWaveCols = 48;
+// segments = ceil(cols / (4 wave_cols)). Measured on the Llama shapes (sweeps
+// of the segment count): 48 columns per wave; then the range widens in steps
+// of 16 columns (to at most kMaxWaveCols) while there are more segments than
+// one gather round reads at batch 1 (four waves x 12 partials in flight: a
+// second round is a second device-scope round trip, about 1.5 us) or more
+// than 1792 workgroups (the seven per CU that fit at once), and narrows
+// while there are fewer than 512 (two per CU). This gives 4096x4096: 32
+// segments, 5120x5120: 27, 4096x11008: 43, 5120x13824: 44, 11008x4096: 22,
+// 13824x5120: 27, 28672x8192: 16. The split is a property of the product
+// alone (it fixes the summation order), so a grouped launch adds up the
+// products' workgroups: 40 segments would make a lone 5120x5120 product 6 %
+// faster but three of them (q, k, v) in one launch 5 % slower.
+// SPDP_SPLITK overrides the number of segments (for tuning).
+constexpr int kWaveCols = 48;
+constexpr int64_t kOneRoundSegments = 48;
 constexpr int64_t kMinWorkgroups = 512;
 constexpr int64_t kMaxWorkgroups = 1792;
-constexpr int64_t kMaxSegments = 64;
 void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   const int64_t cols = std::max<int64_t>(1, m->cols);
   const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
   auto segs = [&](int64_t wc) { return (cols + kWaves * wc - 1) / (kWaves * wc); };
-  int64_t wc = kPreferredWaveCols;
+  int64_t wc = kWaveCols;
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1) {
@@ -754,8 +759,8 @@ void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
       return;
     }
   }
-  while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kMaxSegments) && wc < kMaxWaveCols) wc += 16;
-  while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kMaxSegments) wc -= 16;
+  while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kOneRoundSegments) && wc < kMaxWaveCols) wc += 16;
+  while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kOneRoundSegments) wc -= 16;
   *wave_cols = (int)wc;
   *segments = (int)segs(wc);
 }
