@@ -102,7 +102,13 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
  * must stay valid until the stream passes the work. The handle's workspace
  * is reused by every call, so one handle must not run on two streams at
  * once. The first call with a larger batch than before grows the workspace
- * (a device allocation); spdp_reserve does that ahead of time.
+ * (a device allocation); spdp_reserve does that ahead of time, after which
+ * calls allocate nothing and may be captured into a HIP graph (replays are
+ * exact: the call keeps no host-side state).
+ *
+ * Deterministic: the fp32 summation order depends only on the matrix's
+ * shape and the batch, so equal inputs give equal bits on every call, and a
+ * product gives the same bits alone and inside spdp_spmspv_many.
  */
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
                 float threshold, uint16_t* Y, void* stream);
