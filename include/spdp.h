@@ -106,9 +106,11 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
  * calls allocate nothing and may be captured into a HIP graph (replays are
  * exact: the call keeps no host-side state).
  *
- * Deterministic: the fp32 summation order depends only on the matrix's
- * shape and the batch, so equal inputs give equal bits on every call, and a
- * product gives the same bits alone and inside spdp_spmspv_many.
+ * Deterministic: the fp32 summation order depends only on the matrix, the
+ * batch and which columns are active (and on the tuning variables
+ * SPDP_SPLITK and SPDP_EARLY_FIRST, when set), so equal inputs give equal
+ * bits on every call, and a product gives the same bits alone and inside
+ * spdp_spmspv_many.
  */
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
                 float threshold, uint16_t* Y, void* stream);
