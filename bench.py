@@ -72,6 +72,9 @@ def parse():
                          "definition); N > 0: each layer's threshold is the p-quantile of |x| over N "
                          "separately drawn calibration tokens of that layer, applied to the inputs "
                          "(offline calibration as in the paper's DP setup)")
+    ap.add_argument("--mask", choices=("token", "batch"), default="token",
+                    help="token: each token's own active columns (their union is read); batch: one "
+                         "column set for the batch, chosen by the batch's mean |x| (batched DP)")
     ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
                     help="graph: each step is one captured HIP graph of its calls (how a decode "
                          "loop runs them); stream: one host launch per call")
@@ -81,41 +84,70 @@ def parse():
 # ---------------------------------------------------------------------------
 # byte model (measurement code: computed from the handle's format arrays)
 
-def call_bytes(fmt: dict, x16: np.ndarray, code: int) -> tuple[int, float]:
-    """Algorithmic bytes of one call and the fraction of columns it reads."""
+def token_activity(x16: np.ndarray, code: int) -> np.ndarray:
+    """[batch, cols] column activity per token, the kernel's integer rule."""
+    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
+    return (mag > code) & (mag <= 0x7C00)
+
+
+def batch_scores(x16: np.ndarray) -> np.ndarray:
+    """Per-column fp32 running sum of |x| over the tokens (ascending)."""
+    s = np.zeros(x16.shape[1], dtype=np.float32)
+    with np.errstate(invalid="ignore", over="ignore"):
+        for b in range(x16.shape[0]):
+            s = (s + np.abs(x16[b].astype(np.float32))).astype(np.float32)
+    return s
+
+
+def batch_activity(x16: np.ndarray, t: float) -> np.ndarray:
+    """[batch, cols]: one shared column set, score > fp32(batch * fp32(t))."""
+    thr = np.float32(np.float64(np.float32(t)) * x16.shape[0])
+    with np.errstate(invalid="ignore"):
+        shared = batch_scores(x16) > thr
+    return np.broadcast_to(shared[None, :], x16.shape).copy()
+
+
+def batch_threshold_for(x16: np.ndarray, p: float) -> float:
+    """Threshold t that drops the fraction p of the columns by batch score
+    (the ceil(p K)-th smallest score over the batch size; p = 0 keeps all)."""
+    if p <= 0.0:
+        return -1.0
+    s = np.sort(batch_scores(x16))
+    return float(s[int(np.ceil(p * s.size)) - 1]) / x16.shape[0]
+
+
+def call_bytes(fmt: dict, act: np.ndarray) -> tuple[int, float]:
+    """Algorithmic bytes of one call and the fraction of columns it reads,
+    given the [batch, cols] activity."""
     R, C, tk, tm = fmt["n_stripes"], fmt["n_colblocks"], fmt["tile_k"], fmt["tile_m"]
     K, M = fmt["cols"], fmt["rows"]
-    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
-    act = ((mag > code) & (mag <= 0x7C00)).any(axis=0)            # [K]
+    union = act.any(axis=0)                                       # [K]
     actp = np.zeros(C * tk, dtype=bool)
-    actp[:K] = act
+    actp[:K] = union
     nnz = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64)
     padded = (nnz + 7) // 8 * 8
     per_col = 4 + tm // 8 + 2 * padded                           # [R, C*tk]
     total = int((per_col * actp[None, :]).sum())
     touched = actp.reshape(C, tk).any(axis=1).sum()
     total += 4 * int(touched) * R
-    b = x16.shape[0]
+    b = act.shape[0]
     total += 2 * b * K + 2 * b * M
-    return total, float(act.mean())
+    return total, float(union.mean())
 
 
-def call_flops(fmt: dict, x16: np.ndarray, code: int) -> int:
+def call_flops(fmt: dict, act: np.ndarray) -> int:
     """Useful flops of one call: 2 x the (token, nonzero weight of an active
     column) products, the work the method cannot avoid."""
     R, C, tk = fmt["n_stripes"], fmt["n_colblocks"], fmt["tile_k"]
     K = fmt["cols"]
     nnz_col = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64).sum(axis=0)[:K]
-    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
-    act = (mag > code) & (mag <= 0x7C00)                          # [B, K]
     return int(2 * (act * nnz_col[None, :]).sum())
 
 
-def dropped_fraction(x16: np.ndarray, code: int) -> float:
-    """Fraction of the entries (all tokens) the threshold drops: the realized
-    dynamic sparsity, decided by the kernel's integer rule."""
-    mag = (x16.view(np.uint16) & 0x7FFF).astype(np.int64)
-    return float(1.0 - ((mag > code) & (mag <= 0x7C00)).mean()) if mag.size else 0.0
+def dropped_fraction(act: np.ndarray) -> float:
+    """Fraction of the entries (all tokens) the rule drops: the realized
+    dynamic sparsity."""
+    return float(1.0 - act.mean()) if act.size else 0.0
 
 
 def _code_only(src: str) -> str:
@@ -150,7 +182,7 @@ def read_traffic(workload: str, group: str):
 
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(points, budget_s=20.0):
+def cpu_baseline(points, mask="token", budget_s=20.0):
     """Time the CPU oracle on a bounded sample of the same calls."""
     import oracle
     try:
@@ -164,11 +196,11 @@ def cpu_baseline(points, budget_s=20.0):
     t_total, b_total = 0.0, 0
     t_start = time.perf_counter()
     for pt in points:
-        oracle.spmspv(pt["w"], pt["x"], pt["t"])  # warm-up
+        oracle.spmspv(pt["w"], pt["x"], pt["t"], mask)  # warm-up
         reps = []
         for _ in range(3):
             t0 = time.perf_counter()
-            oracle.spmspv(pt["w"], pt["x"], pt["t"])
+            oracle.spmspv(pt["w"], pt["x"], pt["t"], mask)
             reps.append(time.perf_counter() - t0)
         t_total += float(np.median(reps))
         b_total += pt["bytes"]
@@ -235,7 +267,18 @@ def main():
         for p in wl["act_sparsity"]:
             for proj in wl["projections"]:
                 x = xs[proj.name]
-                if cal:
+                if args.mask == "batch":
+                    if cal:
+                        # the calibration tokens in batches of this size,
+                        # their column scores pooled
+                        cs = cal[(proj.x_seed, proj.x_kind, proj.cols)]
+                        n = cs.shape[0] // batch * batch
+                        groups = cs[:n].reshape(-1, batch, cs.shape[1])
+                        sc = np.sort(np.concatenate([batch_scores(g) for g in groups]))
+                        t = -1.0 if p <= 0 else float(sc[int(np.ceil(p * sc.size)) - 1]) / batch
+                    else:
+                        t = batch_threshold_for(x, p)
+                elif cal:
                     t = spdp.calibrate_threshold(cal[(proj.x_seed, proj.x_kind, proj.cols)], p)
                 else:
                     t = spdp.calibrate_threshold(x, p)
@@ -250,9 +293,11 @@ def main():
     copies = [copy0] + [[spdp.encode(pt["w"], tile) for pt in points] for _ in range(n_copies - 1)]
     for pt, m in zip(points, copy0):
         f = m.format()
-        pt["bytes"], pt["active_frac"] = call_bytes(f, pt["x"], spdp.threshold_code(pt["t"]))
-        pt["dropped"] = dropped_fraction(pt["x"], spdp.threshold_code(pt["t"]))
-        pt["flops"] = call_flops(f, pt["x"], spdp.threshold_code(pt["t"]))
+        act = (batch_activity(pt["x"], pt["t"]) if args.mask == "batch"
+               else token_activity(pt["x"], spdp.threshold_code(pt["t"])))
+        pt["bytes"], pt["active_frac"] = call_bytes(f, act)
+        pt["dropped"] = dropped_fraction(act)
+        pt["flops"] = call_flops(f, act)
         pt["rows"], pt["cols"] = f["rows"], f["cols"]
         del f
     # one device copy of each distinct input per rotation copy (grouped
@@ -292,10 +337,10 @@ def main():
     def launch_calls(c, units):
         for u in units:
             if len(u) == 1:
-                copies[c][u[0]].spmspv_into(X[c][u[0]], points[u[0]]["t"], Y[c][u[0]])
+                copies[c][u[0]].spmspv_into(X[c][u[0]], points[u[0]]["t"], Y[c][u[0]], mask=args.mask)
             else:
                 spdp.spmspv_many([copies[c][j] for j in u], [X[c][j] for j in u],
-                                 [points[j]["t"] for j in u], [Y[c][j] for j in u])
+                                 [points[j]["t"] for j in u], [Y[c][j] for j in u], mask=args.mask)
 
     all_idx = list(range(len(points)))
     grouped = args.group == "decoder"
@@ -472,7 +517,7 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(points)
+        cpu = cpu_baseline(points, args.mask)
 
     traffic = read_traffic(args.workload, args.group)
     n_launch = len(step_units)
@@ -499,6 +544,7 @@ def main():
             "batch": batch, "tile": list(tile), "calls_per_step": len(points),
             "launches_per_step": n_launch, "grouping": args.group,
             "rotation_copies": n_copies, "accumulate": "f32",
+            "mask": args.mask,
             "threshold": ({"rule": "offline calibration", "calibration_tokens": args.calibration,
                            "how": "p-quantile of |x| over separately drawn tokens of each layer input"}
                           if args.calibration > 0 else

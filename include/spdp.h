@@ -142,6 +142,34 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count,
                      const uint16_t* const* X, int32_t batch,
                      const float* thresholds, uint16_t* const* Y, void* stream);
 
+/*
+ * spdp_spmspv_many_mask -- spdp_spmspv_many with a choice of how the batch's
+ * activations select columns (batched dynamic pruning, which the paper
+ * leaves to future work in Sec. 4.3 and Sec. 7):
+ *
+ *   SPDP_MASK_TOKEN  per-token masks, the rule of spdp_spmspv: column k takes
+ *                    part for token b iff |X[b,k]| > threshold; the columns
+ *                    read are the union over the batch, which grows as
+ *                    1 - p^batch and reaches every column by batch 4-8.
+ *   SPDP_MASK_BATCH  one column set for the whole batch: column k takes part
+ *                    for every token iff the fp32 running sum of |X[b,k]|
+ *                    over b = 0, 1, ... (each addition rounded to nearest
+ *                    even) exceeds fp32(batch * threshold), i.e. the batch's
+ *                    mean magnitude exceeds the threshold; in that column
+ *                    every token's activation is used as it is. The set keeps
+ *                    the per-token rule's size at any batch; at batch 1 the
+ *                    two rules are the same.
+ *
+ * Other arguments, ownership and errors are those of spdp_spmspv_many; a
+ * mask other than the two values is SPDP_ERR_INVALID_ARG (nothing is
+ * launched).
+ */
+enum { SPDP_MASK_TOKEN = 0, SPDP_MASK_BATCH = 1 };
+int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count,
+                          const uint16_t* const* X, int32_t batch,
+                          const float* thresholds, int32_t mask,
+                          uint16_t* const* Y, void* stream);
+
 /* spdp_reserve -- size the handle's workspace for batches up to max_batch. */
 int spdp_reserve(spdp_handle_t h, int32_t max_batch);
 

@@ -20,7 +20,9 @@ Functions and the passages of the paper they follow:
   empirical distribution of |x| (Sec. 5.1, ECDF quantile calibration).
 * ``active_mask`` / ``masked_activations`` -- dynamic pruning: a column k is
   kept for a token iff |x_k| exceeds the threshold (Sec. 2.2 DP definition,
-  Sec. 4.2 step (3)).
+  Sec. 4.2 step (3)); or, batched DP (future work in Sec. 4.3 and Sec. 7,
+  read here as one column set shared by the batch), kept for every token
+  iff the batch's fp32 score ``batch_score`` exceeds ``batch_threshold``.
 * ``encode`` / ``decode`` -- the Tiled-CBC format (Sec. 4.1, Tiling Design
   and Storage Structure; 16-byte column padding from Sec. 4.2.3).
 * ``spmspv`` / ``spmspv_rows`` -- the masked product
@@ -58,6 +60,9 @@ __all__ = [
     "calibrated_threshold",
     "realized_sparsity",
     "active_mask",
+    "batch_score",
+    "batch_threshold",
+    "MASKS",
     "masked_activations",
     "encode",
     "encode_brute",
@@ -167,20 +172,52 @@ def realized_sparsity(x: np.ndarray, t: float) -> float:
     return float(1.0 - active_mask(x.reshape(1, -1), t).mean())
 
 
-def active_mask(x: np.ndarray, t: float) -> np.ndarray:
-    """Per-token column activity: ``|x[b, k]| > t`` (strict), float64 compare.
+MASKS = ("token", "batch")
 
-    NaN activations are never active (the comparison is false).
+
+def batch_score(x: np.ndarray) -> np.ndarray:
+    """Per-column score of a batch: ``s_k = sum_b |x[b, k]|`` in float32,
+    tokens added in ascending order, each addition rounded to nearest even
+    (the first one exact). NaN entries make the score NaN."""
+    x = np.atleast_2d(np.asarray(x, dtype=np.float16))
+    s = np.zeros(x.shape[1], dtype=np.float32)
+    with np.errstate(invalid="ignore", over="ignore"):
+        for b in range(x.shape[0]):
+            s = (s + np.abs(x[b].astype(np.float32))).astype(np.float32)
+    return s
+
+
+def batch_threshold(t: float, batch: int) -> np.float32:
+    """The score threshold ``T = fp32(batch * fp32(t))`` (one rounding)."""
+    return np.float32(np.float64(np.float32(t)) * batch)
+
+
+def active_mask(x: np.ndarray, t: float, mask: str = "token") -> np.ndarray:
+    """Column activity per token, ``[batch, cols]`` booleans.
+
+    ``mask="token"`` (the DP definition, Sec. 2.2): ``|x[b, k]| > t``
+    (strict), float64 compare. ``mask="batch"`` (batched DP, one column set
+    shared by the batch; the paper leaves batched DP to future work, this is
+    the reading built here): column k is active for every token iff its batch
+    score exceeds ``batch_threshold(t, batch)``, i.e. the batch's mean |x|
+    exceeds t; at batch 1 the two rules coincide. NaN activations are never
+    active (a NaN makes the comparison false).
     """
-    x = np.asarray(x, dtype=np.float16)
-    with np.errstate(invalid="ignore"):
-        return np.abs(x.astype(np.float64)) > np.float64(np.float32(t))
+    x = np.atleast_2d(np.asarray(x, dtype=np.float16))
+    if mask == "token":
+        with np.errstate(invalid="ignore"):
+            return np.abs(x.astype(np.float64)) > np.float64(np.float32(t))
+    if mask == "batch":
+        with np.errstate(invalid="ignore"):
+            shared = batch_score(x) > batch_threshold(t, x.shape[0])
+        return np.broadcast_to(shared[None, :], x.shape).copy()
+    raise ValueError(f"unknown mask {mask!r}")
 
 
-def masked_activations(x: np.ndarray, t: float) -> np.ndarray:
+def masked_activations(x: np.ndarray, t: float, mask: str = "token") -> np.ndarray:
     """``xm[b, k] = x[b, k]`` where active, else +0; stays fp16 (exact)."""
-    x = np.asarray(x, dtype=np.float16)
-    return np.where(active_mask(x, t), x, np.float16(0.0)).astype(np.float16)
+    x = np.atleast_2d(np.asarray(x, dtype=np.float16))
+    return np.where(active_mask(x, t, mask), x, np.float16(0.0)).astype(np.float16)
 
 
 # --------------------------------------------------------------------------
@@ -404,7 +441,7 @@ def storage_bytes(rows: int, cols: int, tile_m: int, tile_k: int, nnz: int) -> i
 # The masked product (Sec. 2.2; inactive columns contribute nothing, Sec. 4.2)
 # --------------------------------------------------------------------------
 
-def spmspv(w_sp: np.ndarray, x: np.ndarray, t: float):
+def spmspv(w_sp: np.ndarray, x: np.ndarray, t: float, mask: str = "token"):
     """``y[b, m] = sum_k W_sp[m, k] * xm[b, k]`` in float64.
 
     Returns ``(y64, s64, y16)``: the float64 result, the magnitude sum
@@ -412,17 +449,17 @@ def spmspv(w_sp: np.ndarray, x: np.ndarray, t: float):
     and ``y64`` rounded once to fp16 (round to nearest even).
     """
     w64 = np.asarray(w_sp, dtype=np.float16).astype(np.float64)
-    xm = masked_activations(np.atleast_2d(x), t).astype(np.float64)
+    xm = masked_activations(np.atleast_2d(x), t, mask).astype(np.float64)
     y64 = xm @ w64.T
     s64 = np.abs(xm) @ np.abs(w64).T
     return y64, s64, y64.astype(np.float16)
 
 
-def spmspv_rows(w_sp: np.ndarray, x: np.ndarray, t: float, rows):
+def spmspv_rows(w_sp: np.ndarray, x: np.ndarray, t: float, rows, mask: str = "token"):
     """The same product for selected output rows only (one dot product each)."""
     rows = np.asarray(rows, dtype=np.int64)
     w64 = np.asarray(w_sp, dtype=np.float16)[rows].astype(np.float64)
-    xm = masked_activations(np.atleast_2d(x), t).astype(np.float64)
+    xm = masked_activations(np.atleast_2d(x), t, mask).astype(np.float64)
     return xm @ w64.T, np.abs(xm) @ np.abs(w64).T
 
 
@@ -463,7 +500,7 @@ def combined_sparsity(sp: float, dp: float):
 # What one call must move and compute
 # --------------------------------------------------------------------------
 
-def algorithmic_bytes(f: TiledCBC, x: np.ndarray, t: float) -> int:
+def algorithmic_bytes(f: TiledCBC, x: np.ndarray, t: float, mask: str = "token") -> int:
     """Bytes a call must read/write given the active columns (union over tokens).
 
     For every row stripe and every active column: its ColInfo word (4 B), its
@@ -472,7 +509,7 @@ def algorithmic_bytes(f: TiledCBC, x: np.ndarray, t: float) -> int:
     activations (2 B K) and the outputs (2 B M) per token.
     """
     x = np.atleast_2d(np.asarray(x, dtype=np.float16))
-    act = active_mask(x, t).any(axis=0)
+    act = active_mask(x, t, mask).any(axis=0)
     total = 0
     for r in range(f.n_stripes):
         touched = set()
@@ -487,9 +524,9 @@ def algorithmic_bytes(f: TiledCBC, x: np.ndarray, t: float) -> int:
     return total + 2 * b * f.cols + 2 * b * f.rows
 
 
-def useful_flops(w_sp: np.ndarray, x: np.ndarray, t: float) -> int:
+def useful_flops(w_sp: np.ndarray, x: np.ndarray, t: float, mask: str = "token") -> int:
     """2 x the number of (token, nonzero weight, active column) products."""
     x = np.atleast_2d(np.asarray(x, dtype=np.float16))
-    act = active_mask(x, t)
+    act = active_mask(x, t, mask)
     nnz_col = ((_bits(np.asarray(w_sp, dtype=np.float16)) & 0x7FFF) != 0).sum(axis=0)
     return int(2 * (act * nnz_col[None, :]).sum())

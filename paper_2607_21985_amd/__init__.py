@@ -29,6 +29,7 @@ __all__ = [
     "encode",
     "encode_host",
     "spmspv_many",
+    "MASKS",
     "prune_magnitude",
     "calibrate_threshold",
     "threshold_code",
@@ -39,7 +40,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_NAME = "libspdp.so"
 
 EXPORTED_SYMBOLS = (
-    "spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_reserve", "spdp_free",
+    "spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_spmspv_many_mask",
+    "spdp_reserve", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
 )
@@ -97,6 +99,9 @@ def lib() -> ctypes.CDLL:
     L.spdp_spmspv_many.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_void_p),
                                    ctypes.c_void_p]
+    L.spdp_spmspv_many_mask.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
+                                        ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(ctypes.c_void_p),
+                                        ctypes.c_void_p]
     L.spdp_reserve.argtypes = [H, i32]
     L.spdp_free.argtypes = [H]
     L.spdp_free.restype = None
@@ -108,7 +113,8 @@ def lib() -> ctypes.CDLL:
     L.spdp_strerror.restype = ctypes.c_char_p
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = ctypes.c_char_p
-    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_reserve",
+    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_spmspv_many_mask",
+                 "spdp_reserve",
                  "spdp_format",
                  "spdp_prune_magnitude", "spdp_calibrate_threshold", "spdp_threshold_code"):
         getattr(L, name).restype = ctypes.c_int
@@ -177,8 +183,12 @@ class Matrix:
     def reserve(self, max_batch: int) -> None:
         _check(lib().spdp_reserve(self._h, int(max_batch)))
 
-    def spmspv_into(self, x, threshold: float, y, stream=None) -> None:
-        """Enqueue ``y = W_sp . mask(x)`` on ``stream`` (torch stream, or the current one)."""
+    def spmspv_into(self, x, threshold: float, y, stream=None, mask: str = "token") -> None:
+        """Enqueue ``y = W_sp . mask(x)`` on ``stream`` (torch stream, or the current one).
+
+        ``mask``: "token" (each token's own columns) or "batch" (one column
+        set for the batch, by its fp32 sum of magnitudes; see
+        ``spmspv_many``)."""
         import torch
         if x.dtype != torch.float16 or y.dtype != torch.float16:
             raise TypeError("x and y must be torch.float16")
@@ -190,14 +200,22 @@ class Matrix:
         if not (x.is_cuda and y.is_cuda):
             raise ValueError("x and y must be device tensors")
         s = stream if stream is not None else torch.cuda.current_stream(x.device)
-        _check(lib().spdp_spmspv(self._h, ctypes.c_void_p(x.data_ptr()), int(b),
-                                 ctypes.c_float(threshold), ctypes.c_void_p(y.data_ptr()),
-                                 ctypes.c_void_p(s.cuda_stream)))
+        if mask == "token":
+            _check(lib().spdp_spmspv(self._h, ctypes.c_void_p(x.data_ptr()), int(b),
+                                     ctypes.c_float(threshold), ctypes.c_void_p(y.data_ptr()),
+                                     ctypes.c_void_p(s.cuda_stream)))
+        else:
+            hs = (ctypes.c_void_p * 1)(self._h)
+            xp = (ctypes.c_void_p * 1)(x.data_ptr())
+            yp = (ctypes.c_void_p * 1)(y.data_ptr())
+            ts = (ctypes.c_float * 1)(float(threshold))
+            _check(lib().spdp_spmspv_many_mask(hs, 1, xp, int(b), ts, _mask_code(mask), yp,
+                                               ctypes.c_void_p(s.cuda_stream)))
 
-    def __call__(self, x, threshold: float, stream=None):
+    def __call__(self, x, threshold: float, stream=None, mask: str = "token"):
         import torch
         y = torch.empty((x.shape[0], self.rows), dtype=torch.float16, device=x.device)
-        self.spmspv_into(x, threshold, y, stream)
+        self.spmspv_into(x, threshold, y, stream, mask)
         return y
 
     def close(self) -> None:
@@ -252,12 +270,25 @@ def encode(w: np.ndarray, tile=(256, 16)) -> Matrix:
     return Matrix(h)
 
 
-def spmspv_many(mats, xs, thresholds, ys, stream=None) -> None:
+MASKS = {"token": 0, "batch": 1}  # SPDP_MASK_TOKEN, SPDP_MASK_BATCH
+
+
+def _mask_code(mask: str) -> int:
+    if mask not in MASKS:
+        raise ValueError(f"mask must be one of {sorted(MASKS)}")
+    return MASKS[mask]
+
+
+def spmspv_many(mats, xs, thresholds, ys, stream=None, mask: str = "token") -> None:
     """Enqueue ``ys[i] = W_i . mask(xs[i])`` for every i in one launch.
 
     ``mats`` are encoded matrices with one tile height, ``xs``/``ys`` torch
     fp16 device tensors ``[batch, cols_i]`` / ``[batch, rows_i]`` (one batch
     for all), ``thresholds`` one float per product. Inputs may be shared.
+    ``mask="token"``: column k takes part for token b iff |x[b, k]| > t;
+    ``mask="batch"``: one column set for the batch, column k taking part for
+    every token iff the fp32 running sum of |x[b, k]| over the tokens exceeds
+    fp32(batch * t) (the batch's mean magnitude exceeds t).
     """
     import torch
     n = len(mats)
@@ -279,7 +310,8 @@ def spmspv_many(mats, xs, thresholds, ys, stream=None) -> None:
     xp = (ctypes.c_void_p * n)(*[x.data_ptr() for x in xs])
     yp = (ctypes.c_void_p * n)(*[y.data_ptr() for y in ys])
     ts = (ctypes.c_float * n)(*[float(t) for t in thresholds])
-    _check(lib().spdp_spmspv_many(hs, n, xp, int(xs[0].shape[0]), ts, yp, ctypes.c_void_p(s.cuda_stream)))
+    _check(lib().spdp_spmspv_many_mask(hs, n, xp, int(xs[0].shape[0]), ts, _mask_code(mask), yp,
+                                       ctypes.c_void_p(s.cuda_stream)))
 
 
 def encode_host(w: np.ndarray, tile=(256, 16)) -> Matrix:

@@ -95,6 +95,10 @@ struct MatArgs {
   // built (a property of the product and the batch, never of the launch, so
   // that grouping does not change the summation order)
   int early_first;
+  // with the batch's shared column set (the kernel's BMASK form): a column
+  // is active iff the fp32 running sum of |x[b, k]| over the tokens exceeds
+  // batch_thr = fp32(batch * t), every token's activation kept there
+  float batch_thr;
 };
 
 // A launch runs up to kMaxGroup independent products (same tile height and
@@ -280,7 +284,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
 // column (tile_m / 64).
-template <int NB, int WPC, bool EARLY>
+template <int NB, int WPC, bool EARLY, bool BMASK>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
@@ -306,6 +310,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const uint32_t n_seg0 = (uint32_t)A->segments;
   const int batch = L->batch;
   const int early_first = EARLY ? A->early_first : 0;
+  const float batch_thr = BMASK ? A->batch_thr : 0.0f;
   const int tk_log2 = A->tk_log2;
   const int n_colblocks = A->n_colblocks;
   const int code = A->code;
@@ -320,7 +325,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const uint32_t zero_col = A->zero_col;
   asm volatile("" ::"s"(n_seg0), "s"(batch), "s"(tk_log2), "s"(n_colblocks), "s"(code), "s"(cols),
                "s"(wave_cols), "s"(phase_p), "s"(col_info_p), "s"(tile_offset_p), "s"(x_p), "s"(values),
-               "s"(bitmap), "s"(zero_col), "s"(early_first));
+               "s"(bitmap), "s"(zero_col), "s"(early_first), "s"(batch_thr));
   if (local >= n_wg) return;  // the whole workgroup: no barrier has been reached
   const int r = (int)(local / n_seg0);
   const int seg = (int)(local - (uint32_t)r * n_seg0);
@@ -366,24 +371,35 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // list is built; a scalar load would share the LDS wait counter, and the
   // compiler would wait for it at the first LDS barrier.
   const uint32_t phase_lane = __hip_atomic_load(phase_p + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  // activity (union over the tokens)
+  // activity: the union of the tokens' sets, or the batch's shared set
   uint64_t actm[kChunks];
   int n_w = 0;
 #pragma unroll
   for (int c = 0; c < kChunks; ++c) {
     const bool in = 64 * c + lane < range;
     uint64_t act = 0;
+    if constexpr (BMASK) {
+      // fp32 running sum of |x| over the tokens in ascending order (NaN
+      // makes it NaN, never active)
+      float score = 0.0f;
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int mag = (int)(xb[c][b] & 0x7FFFu);
-      act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
+      for (int b = 0; b < NB; ++b)
+        if (b < batch) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
+      act = __builtin_amdgcn_ballot_w64(in && score > batch_thr);
+    } else {
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        const int mag = (int)(xb[c][b] & 0x7FFFu);
+        act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
+      }
     }
     actm[c] = act;
     n_w += __builtin_popcountll(act);
   }
   // list entry p of this lane's column of chunk c, with its masked
-  // activations (pair-interleaved: entries 2j and 2j+1 share a dword per
-  // token); entries of the all-zero column pad a batch: they read the
+  // activations (every token's under the batch's shared set; pair-
+  // interleaved: entries 2j and 2j+1 share a dword per token); entries of
+  // the all-zero column pad a batch: they read the
   // bitmap array's zeroed tail and the first 16 bytes of the values, and
   // decode to nothing
   auto put = [&](int c, int p) __attribute__((always_inline)) {
@@ -392,7 +408,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int mag = (int)(xb[c][b] & 0x7FFFu);
-      const bool on = b < batch && mag > code && mag <= 0x7C00;
+      const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
       xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
     }
   };
@@ -832,26 +848,33 @@ int upload(const std::vector<T>& v, void** dst) {
 }
 
 template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, bool early, dim3 grid, hipStream_t stream) {
-  // only the one-token kernel has the early-first-batch form (no product with
-  // more tokens asks for it)
+hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, dim3 grid, hipStream_t stream) {
+  // the one-token kernel has the early-first-batch form (no product with
+  // more tokens asks for it); the kernels for more tokens have the shared
+  // batch mask form (at one token the two masks are the same rule, and the
+  // host sends such calls to the per-token kernel)
   if constexpr (NB == 1) {
     if (early) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false>), grid, dim3(kThreads), 0, stream, args);
+      return hipGetLastError();
+    }
+  } else {
+    if (bmask) {
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false>), grid, dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, bool early, dim3 grid, hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, dim3 grid, hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, early, grid, stream);
-    case 2: return launch_one<NB, 2>(args, early, grid, stream);
-    case 3: return launch_one<NB, 3>(args, early, grid, stream);
-    default: return launch_one<NB, 4>(args, early, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, bmask, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, bmask, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, bmask, grid, stream);
+    default: return launch_one<NB, 4>(args, early, bmask, grid, stream);
   }
 }
 
@@ -872,7 +895,7 @@ int early_first(int batch, int64_t workgroups) {
 
 // Validates one product of a call and fills its kernel arguments (sizing
 // the handle's workspace for the batch if needed).
-int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, uint16_t* Y, int dev,
+int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, int32_t mask, uint16_t* Y, int dev,
             MatArgs* out, int64_t* n_wg) {
   if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
   if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
@@ -918,6 +941,7 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   *n_wg = (int64_t)segments * h->n_stripes;
   a.n_wg = (int)*n_wg;
   a.early_first = early_first(batch, *n_wg);
+  a.batch_thr = mask == SPDP_MASK_BATCH ? (float)((double)threshold * (double)batch) : 0.0f;
   return SPDP_OK;
 }
 
@@ -1001,10 +1025,13 @@ int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
   return ensure_workspace(h, max_batch, segments);
 }
 
-int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
-                     int32_t batch, const float* thresholds, uint16_t* const* Y, void* stream) {
+int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
+                          int32_t batch, const float* thresholds, int32_t mask, uint16_t* const* Y,
+                          void* stream) {
   spdp::clear_error();
   if (!handles || !X || !Y || !thresholds) return fail(SPDP_ERR_INVALID_ARG, "an argument array is NULL");
+  if (mask != SPDP_MASK_TOKEN && mask != SPDP_MASK_BATCH)
+    return fail(SPDP_ERR_INVALID_ARG, "mask must be SPDP_MASK_TOKEN or SPDP_MASK_BATCH");
   if (count < 1 || count > kMaxGroup) return fail(SPDP_ERR_INVALID_ARG, "count must lie in [1, 8]");
   if (batch < 1 || batch > kMaxBatch) return fail(SPDP_ERR_INVALID_ARG, "batch must lie in [1, 32]");
   for (int i = 0; i < count; ++i) {
@@ -1031,9 +1058,10 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t
   la.batch = batch;
   int64_t widest = 0;
   bool early = false;
+  const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
   for (int i = 0; i < count; ++i) {
     int64_t n_wg = 0;
-    const int st = prepare(handles[i], X[i], batch, thresholds[i], Y[i], dev, &la.m[i], &n_wg);
+    const int st = prepare(handles[i], X[i], batch, thresholds[i], mask, Y[i], dev, &la.m[i], &n_wg);
     if (st != SPDP_OK) return st;
     if (handles[i]->tile_m != handles[0]->tile_m)
       return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
@@ -1046,24 +1074,29 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t
   const dim3 grid((unsigned)widest, (unsigned)count);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (batch <= 1)
-    e = launch<1>(la, wpc, early, grid, s);
+    e = launch<1>(la, wpc, early, bmask, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, early, grid, s);
+    e = launch<2>(la, wpc, early, bmask, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, early, grid, s);
+    e = launch<4>(la, wpc, early, bmask, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, early, grid, s);
+    e = launch<8>(la, wpc, early, bmask, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, early, grid, s);
+    e = launch<16>(la, wpc, early, bmask, grid, s);
   else
-    e = launch<32>(la, wpc, early, grid, s);
+    e = launch<32>(la, wpc, early, bmask, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }
 
+int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
+                     int32_t batch, const float* thresholds, uint16_t* const* Y, void* stream) {
+  return spdp_spmspv_many_mask(handles, count, X, batch, thresholds, SPDP_MASK_TOKEN, Y, stream);
+}
+
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold,
                 uint16_t* Y, void* stream) {
-  return spdp_spmspv_many(&h, 1, &X, batch, &threshold, &Y, stream);
+  return spdp_spmspv_many_mask(&h, 1, &X, batch, &threshold, SPDP_MASK_TOKEN, &Y, stream);
 }
 
 void spdp_free(spdp_handle_t h) {

@@ -138,5 +138,14 @@ def test_spmspv_many_argument_errors():
     # host-only handles are rejected before any device work
     assert L.spdp_spmspv_many(hs, 2, xs, 1, ts, ys, None) == ERR_INVALID
     assert b"device" in L.spdp_last_error()
+    # the mask choice: only the two declared values
+    for mask in (-1, 2, 7):
+        assert L.spdp_spmspv_many_mask(hs, 2, xs, 1, ts, mask, ys, None) == ERR_INVALID
+        assert b"mask" in L.spdp_last_error()
+    for mask in (0, 1):  # valid masks reach the same device check
+        assert L.spdp_spmspv_many_mask(hs, 2, xs, 1, ts, mask, ys, None) == ERR_INVALID
+        assert b"device" in L.spdp_last_error()
+    with pytest.raises(ValueError):
+        spdp._mask_code("mean")
     a.close()
     b.close()

@@ -93,6 +93,33 @@ def test_many_mixes_early_and_plain_first_batches(monkeypatch):
         m.close()
 
 
+def test_many_batch_mask_matches_oracle_and_single_calls():
+    """The batch-shared mask in a grouped launch: every product against the
+    oracle and bit-identical to its single call."""
+    dev = _dev()
+    prods = _products([(700, 1500), (300, 1500), (1300, 900)], 0.6, 0.5, 6, 4321)
+    ts = []
+    for _, x, _ in prods:
+        sc = np.sort(oracle.batch_score(x))
+        ts.append(float(sc[int(np.ceil(0.5 * sc.size)) - 1]) / x.shape[0])
+    mats = [spdp.encode(w, (256, 16)) for w, _, _ in prods]
+    Xs = [_to_dev(x) for _, x, _ in prods]
+    Yg = [torch.full((6, m.rows), float("nan"), dtype=torch.float16, device=dev) for m in mats]
+    print("[gpu] many: batch mask", flush=True)
+    spdp.spmspv_many(mats, Xs, ts, Yg, mask="batch")
+    torch.cuda.synchronize()
+    for i, ((w, x, _), t, m, X, Y) in enumerate(zip(prods, ts, mats, Xs, Yg)):
+        y = Y.cpu().numpy().astype(np.float64)
+        y64, s64, _ = oracle.spmspv(w, x, t, "batch")
+        _assert_close(y, y64, s64, f"product {i}")
+        Ys = torch.full_like(Y, float("nan"))
+        m.spmspv_into(X, t, Ys, mask="batch")
+        torch.cuda.synchronize()
+        assert torch.equal(Ys, Y), f"product {i}: grouped result differs from the single call"
+    for m in mats:
+        m.close()
+
+
 def test_many_repeated_and_graph_replayed():
     """Grouped calls back to back, then captured and replayed with eager calls
     in between: every result equals the first eager one."""

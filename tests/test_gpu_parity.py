@@ -42,13 +42,13 @@ def _to_dev(x16: np.ndarray):
     return t.to(_dev())
 
 
-def _run_gpu(m, x16, t, y_init=None):
+def _run_gpu(m, x16, t, y_init=None, mask="token"):
     X = _to_dev(x16)
     if y_init is None:
         Y = torch.full((x16.shape[0], m.rows), float("nan"), dtype=torch.float16, device=X.device)
     else:
         Y = y_init
-    m.spmspv_into(X, t, Y)
+    m.spmspv_into(X, t, Y, mask=mask)
     torch.cuda.synchronize()
     return Y.cpu().numpy().astype(np.float64)
 
@@ -374,3 +374,65 @@ def test_full_size_sampled(name, proj):
         x = proj.activations(b)
         t = float(oracle.threshold_for(x, p))
         _check_sampled(w, x, t, wl["tile"], f"{name}/{proj.name} {proj.rows}x{proj.cols} sw={sw} p={p} B={b}")
+
+
+# ---------------------------------------------------------------------------
+# Batched DP with one column set shared by the batch (mask="batch"): column k
+# is read for every token iff the fp32 running sum of |x[b, k]| exceeds
+# fp32(batch * t).
+
+def _batch_t(x, p):
+    """t dropping the fraction p of the columns by batch score (oracle side)."""
+    s = np.sort(oracle.batch_score(x))
+    return -1.0 if p <= 0 else float(s[int(np.ceil(p * s.size)) - 1]) / x.shape[0]
+
+
+BATCH_MASK = [
+    # rows, cols, tile, sw, p, batch
+    (333, 517, (256, 16), 0.5, 0.5, 1),
+    (513, 1000, (256, 16), 0.6, 0.4, 2),
+    (256, 4096, (256, 16), 0.7, 0.5, 3),
+    (700, 900, (128, 8), 0.5, 0.3, 4),
+    (300, 2048, (64, 1), 0.5, 0.5, 8),
+    (1000, 1536, (256, 256), 0.5, 0.6, 13),
+    (129, 300, (128, 64), 0.5, 0.5, 17),
+    (512, 1111, (256, 16), 0.6, 0.7, 32),
+]
+
+
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch", BATCH_MASK)
+def test_batch_mask_against_oracle(rows, cols, tile, sw, p, batch):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows * 3 + cols), sw)
+    x = synth.laplace_activations(batch, cols, cols + 5 * batch)
+    t = _batch_t(x, p)
+    label = f"batch mask {rows}x{cols} tile={tile} sw={sw} p={p} B={batch}"
+    print(f"[gpu] {label}", flush=True)
+    m = spdp.encode(w, tile)
+    y = _run_gpu(m, x, t, mask="batch")
+    y64, s64, _ = oracle.spmspv(w, x, t, "batch")
+    _assert_close(y, y64, s64, label)
+    if batch == 1:  # the two rules coincide at one token, bit for bit
+        assert np.array_equal(y, _run_gpu(m, x, t, mask="token"))
+    m.close()
+
+
+def test_batch_mask_edge_cases():
+    w = oracle.magnitude_prune(synth.weights(300, 700, 91), 0.5)
+    x = synth.laplace_activations(5, 700, 92)
+    m = spdp.encode(w, (256, 16))
+    # nothing active: exact zeros
+    y = _run_gpu(m, x, float(np.abs(x.astype(np.float64)).max()) * 2, mask="batch")
+    assert np.array_equal(y, np.zeros_like(y))
+    # a negative threshold keeps every column: the plain product
+    y = _run_gpu(m, x, -1.0, mask="batch")
+    y64, s64, _ = oracle.spmspv(w, x, -1.0, "batch")
+    _assert_close(y, y64, s64, "batch mask, t < 0")
+    # a NaN in one token drops its column for the whole batch
+    xn = x.copy()
+    xn[2, 10] = np.float16(np.nan)
+    t = _batch_t(x, 0.3)
+    y = _run_gpu(m, xn, t, mask="batch")
+    y64, s64, _ = oracle.spmspv(w, xn, t, "batch")
+    assert not oracle.active_mask(xn, t, "batch")[0, 10]
+    _assert_close(y, y64, s64, "batch mask, NaN token")
+    m.close()

@@ -470,3 +470,66 @@ def test_useful_flops_counts_products():
                 if act[b, k] and (wb[m, k] & 0x7FFF):
                     cnt += 1
     assert oracle.useful_flops(w, x, t) == 2 * cnt
+
+
+# ---------------------------------------------------------------------------
+# Batched DP with one column set shared by the batch (the paper leaves
+# batched DP to future work, Sec. 4.3 and Sec. 7; the reading built here):
+# column k is kept for every token iff the fp32 score sum_b |x[b, k]|
+# (tokens in ascending order) exceeds T = fp32(B * t).
+
+@pytest.mark.parametrize("t", [-1.0, 0.0, 6e-8, 0.5, 1.0, 65504.0])
+def test_batch_mask_at_batch_one_is_the_token_rule(t):
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    x = bits.view(np.float16).reshape(1, -1)
+    assert np.array_equal(oracle.active_mask(x, t, "batch"), oracle.active_mask(x, t, "token"))
+
+
+def test_batch_mask_hand_worked():
+    x = np.array([[1.0, 0.5, -2.0, 0.0], [0.5, 0.25, 0.0, 0.0]], dtype=np.float16)
+    # scores 1.5, 0.75, 2.0, 0; T = fp32(2 * 0.7) = 1.4 (to fp32)
+    assert oracle.batch_score(x).tolist() == [1.5, 0.75, 2.0, 0.0]
+    act = oracle.active_mask(x, 0.7, "batch")
+    assert act.tolist() == [[True, False, True, False]] * 2
+    xm = oracle.masked_activations(x, 0.7, "batch")
+    # token 1 keeps its 0.5 in column 0 although 0.5 < t: the set is shared
+    assert xm.astype(np.float64).tolist() == [[1.0, 0.0, -2.0, 0.0], [0.5, 0.0, 0.0, 0.0]]
+    # the per-token rule differs: each token keeps only its own entries above t
+    assert oracle.masked_activations(x, 0.7, "token").astype(np.float64).tolist() == [[1.0, 0.0, -2.0, 0.0],
+                                                                                      [0.0, 0.0, 0.0, 0.0]]
+
+
+def test_batch_score_is_an_fp32_running_sum():
+    # 65504 + 2^-14 is not representable in fp32 near 65504 (spacing 2^-8):
+    # the running sum stays 65504, so with T = 65504 the column is inactive,
+    # where an exact (or float64) sum would make it active
+    x = np.array([[65504.0], [2.0 ** -14]], dtype=np.float16)
+    assert oracle.batch_score(x)[0] == np.float32(65504.0)
+    assert oracle.batch_threshold(32752.0, 2) == np.float32(65504.0)
+    assert not oracle.active_mask(x, 32752.0, "batch")[0, 0]
+    # order matters for the rounding: small terms first accumulate
+    y = np.array([[2.0 ** -10]] * 3 + [[2048.0]], dtype=np.float16)
+    assert oracle.batch_score(y)[0] == np.float32(np.float32(3 * 2.0 ** -10) + np.float32(2048.0))
+
+
+def test_batch_mask_special_values():
+    x = np.array([[np.nan, np.inf, 0.0, 1.0], [1.0, 1.0, 0.0, 1.0]], dtype=np.float16)
+    act = oracle.active_mask(x, 0.5, "batch")[0]
+    assert act.tolist() == [False, True, False, True]       # NaN never, inf always
+    assert oracle.active_mask(x[:, 2:], -1.0, "batch").all()  # negative t keeps every column
+    with pytest.raises(ValueError):
+        oracle.active_mask(x, 0.5, "mean")
+
+
+def test_batch_mask_bytes_and_flops_brute_force():
+    w = oracle.magnitude_prune(synth.weights(70, 40, 3), 0.5)
+    x = synth.laplace_activations(3, 40, 4)
+    t = float(oracle.threshold_for(x, 0.6))
+    act = oracle.active_mask(x, t, "batch")[0]
+    nnz = ((w.view(np.uint16) & 0x7FFF) != 0).sum(axis=0)
+    assert oracle.useful_flops(w, x, t, "batch") == 2 * 3 * int(nnz[act].sum())
+    f = oracle.encode(w, 64, 8)
+    per_col = [sum(4 + 8 + 2 * ((f.column(r, k)[1] + 7) // 8 * 8) for r in range(f.n_stripes)) for k in range(40)]
+    touched = len({k // 8 for k in range(40) if act[k]}) * f.n_stripes
+    expect = sum(c for c, a in zip(per_col, act) if a) + 4 * touched + 2 * 3 * (40 + 70)
+    assert oracle.algorithmic_bytes(f, x, t, "batch") == expect
