@@ -241,22 +241,26 @@ def test_graph_replay_matches_eager():
     in between) gives the eager result."""
     dev = _dev()
     cases = [_case(900, 2100, (256, 16), 0.5, p, b, 71 + i, 81 + i) for i, (p, b) in enumerate([(0.5, 1), (0.0, 3)])]
+    # a third call with the batch-shared column set
+    wb, xb, _ = _case(900, 2100, (256, 16), 0.5, 0.5, 5, 74, 84)
+    cases.append((wb, xb, _batch_t(xb, 0.5)))
+    masks = ["token", "token", "batch"]
     mats = [spdp.encode(w, (256, 16)) for w, _, _ in cases]
     for m, (_, x, _) in zip(mats, cases):
         m.reserve(x.shape[0])
     Xs = [_to_dev(x) for _, x, _ in cases]
     Ys = [torch.zeros((x.shape[0], m.rows), dtype=torch.float16, device=dev) for (_, x, _), m in zip(cases, mats)]
     eager = []
-    for m, X, Y, (_, _, t) in zip(mats, Xs, Ys, cases):
-        m.spmspv_into(X, t, Y)
+    for m, X, Y, (_, _, t), mk in zip(mats, Xs, Ys, cases, masks):
+        m.spmspv_into(X, t, Y, mask=mk)
         eager.append(Y.clone())
     torch.cuda.synchronize()
     s = torch.cuda.Stream(device=dev)
     s.wait_stream(torch.cuda.current_stream(dev))
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=s):
-        for m, X, Y, (_, _, t) in zip(mats, Xs, Ys, cases):
-            m.spmspv_into(X, t, Y)
+        for m, X, Y, (_, _, t), mk in zip(mats, Xs, Ys, cases, masks):
+            m.spmspv_into(X, t, Y, mask=mk)
     torch.cuda.synchronize()
     for rep in range(4):
         print(f"[gpu] graph replay {rep}", flush=True)
@@ -267,11 +271,11 @@ def test_graph_replay_matches_eager():
         for i, (Y, E) in enumerate(zip(Ys, eager)):
             assert torch.equal(Y, E), f"replay {rep}, call {i}: differs from the eager result"
         # eager calls on the same handles between replays
-        for m, X, (_, _, t) in zip(mats, Xs, cases):
-            m(X, t)
+        for m, X, (_, _, t), mk in zip(mats, Xs, cases, masks):
+            m(X, t, mask=mk)
         torch.cuda.synchronize()
-    for (w, x, t), E in zip(cases, eager):
-        y64, s64, _ = oracle.spmspv(w, x, t)
+    for (w, x, t), E, mk in zip(cases, eager, masks):
+        y64, s64, _ = oracle.spmspv(w, x, t, mk)
         _assert_close(E.cpu().numpy().astype(np.float64), y64, s64, "graph eager reference")
     del g
     for m in mats:
