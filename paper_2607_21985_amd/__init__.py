@@ -30,6 +30,7 @@ __all__ = [
     "encode_host",
     "spmspv_many",
     "MASKS",
+    "Chain",
     "prune_magnitude",
     "calibrate_threshold",
     "threshold_code",
@@ -346,3 +347,62 @@ def threshold_code(t: float) -> int:
     c = ctypes.c_int32()
     _check(lib().spdp_threshold_code(ctypes.c_float(t), ctypes.byref(c)))
     return int(c.value)
+
+
+class Chain:
+    """A decoder layer's projections issued as one HIP graph.
+
+    ``add`` records one launch: a list of products that read one input
+    (q, k and v; gate and up) goes out as one grouped launch, a single
+    product as a plain call. ``capture`` sizes every matrix's workspace for
+    the batches recorded, issues the launches once eagerly and records them
+    into a graph on a side stream; ``replay`` re-issues the whole chain on
+    the current stream with one host call. Between replays the caller
+    rewrites the input tensors in place (and the thresholds are fixed at
+    capture); the calls keep no host-side state, so every replay computes on
+    the tensors' current contents.
+    """
+
+    def __init__(self):
+        self._calls = []
+        self._graph = None
+
+    def add(self, mats, xs, thresholds, ys, mask: str = "token") -> "Chain":
+        if self._graph is not None:
+            raise RuntimeError("the chain is captured already")
+        if isinstance(mats, Matrix):
+            mats, xs, thresholds, ys = [mats], [xs], [thresholds], [ys]
+        _mask_code(mask)
+        self._calls.append((list(mats), list(xs), [float(t) for t in thresholds], list(ys), mask))
+        return self
+
+    def _issue(self):
+        for mats, xs, ts, ys, mask in self._calls:
+            if len(mats) == 1:
+                mats[0].spmspv_into(xs[0], ts[0], ys[0], mask=mask)
+            else:
+                spmspv_many(mats, xs, ts, ys, mask=mask)
+
+    def capture(self) -> "Chain":
+        import torch
+        if not self._calls:
+            raise RuntimeError("nothing to capture")
+        for mats, xs, _, _, _ in self._calls:
+            for m, x in zip(mats, xs):
+                m.reserve(int(x.shape[0]))
+        dev = self._calls[0][1][0].device
+        self._issue()  # eager once: every workspace and phase in place
+        torch.cuda.synchronize(dev)
+        s = torch.cuda.Stream(device=dev)
+        s.wait_stream(torch.cuda.current_stream(dev))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            self._issue()
+        torch.cuda.current_stream(dev).wait_stream(s)
+        self._graph = g
+        return self
+
+    def replay(self) -> None:
+        if self._graph is None:
+            raise RuntimeError("capture() first")
+        self._graph.replay()

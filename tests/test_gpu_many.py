@@ -186,3 +186,43 @@ def test_many_argument_errors_on_device():
     torch.cuda.synchronize()
     for m in (a, b, c):
         m.close()
+
+
+def test_decoder_layer_chain_in_one_graph():
+    """A small decoder layer (q/k/v grouped, o, gate/up grouped, down) as one
+    captured graph: every replay, with fresh inputs written in place between
+    replays, matches the oracle on those inputs."""
+    dev = _dev()
+    d, f = 768, 2048
+    shapes = {"q": (d, d), "k": (d, d), "v": (d, d), "o": (d, d), "gate": (f, d), "up": (f, d), "down": (d, f)}
+    ws = {n: oracle.magnitude_prune(synth.weights(r, c, 700 + i), 0.6) for i, (n, (r, c)) in enumerate(shapes.items())}
+    mats = {n: spdp.encode(w, (256, 16)) for n, w in ws.items()}
+    batch = 2
+    inputs = {"qkv": d, "o": d, "gu": d, "down": f}
+    X = {k: torch.zeros((batch, c), dtype=torch.float16, device=dev) for k, c in inputs.items()}
+    Y = {n: torch.zeros((batch, r), dtype=torch.float16, device=dev) for n, (r, _) in shapes.items()}
+    t = 0.6
+    chain = spdp.Chain()
+    chain.add([mats["q"], mats["k"], mats["v"]], [X["qkv"]] * 3, [t] * 3, [Y["q"], Y["k"], Y["v"]])
+    chain.add(mats["o"], X["o"], t, Y["o"])
+    chain.add([mats["gate"], mats["up"]], [X["gu"]] * 2, [t] * 2, [Y["gate"], Y["up"]], mask="batch")
+    chain.add(mats["down"], X["down"], t, Y["down"], mask="batch")
+    chain.capture()
+    src = {"q": "qkv", "k": "qkv", "v": "qkv", "o": "o", "gate": "gu", "up": "gu", "down": "down"}
+    mask = {"q": "token", "k": "token", "v": "token", "o": "token", "gate": "batch", "up": "batch", "down": "batch"}
+    for rep in range(3):
+        print(f"[gpu] chain replay {rep}", flush=True)
+        xs = {k: synth.laplace_activations(batch, c, 900 + 10 * rep + i) for i, (k, c) in enumerate(inputs.items())}
+        for k, x in xs.items():
+            X[k].copy_(torch.from_numpy(x.view(np.int16)).view(torch.float16).to(dev))
+        for yv in Y.values():
+            yv.fill_(float("nan"))
+        chain.replay()
+        torch.cuda.synchronize()
+        for n in shapes:
+            y = Y[n].cpu().numpy().astype(np.float64)
+            y64, s64, _ = oracle.spmspv(ws[n], xs[src[n]], t, mask[n])
+            _assert_close(y, y64, s64, f"chain replay {rep}, {n}")
+    del chain
+    for m in mats.values():
+        m.close()
