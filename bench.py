@@ -11,9 +11,11 @@ Calls are issued the way a decoder issues them: projections of one sweep
 point that read the same layer input (q, k and v; gate and up) go out as one
 grouped launch (spdp_spmspv_many), the others (o, down) as single launches;
 --group none issues every product as its own launch, and the JSON line
-reports that rate too. By default each step is replayed as one captured HIP
-graph of its launches (the kernel keeps no host-side state between calls, so
-replays are exact); --launch stream issues one host launch per call instead.
+reports that rate too. By default the steps are replayed from captured HIP
+graphs of their launches, a whole rotation cycle of steps per graph, as a
+decoder replays a token's pass over all its layers as one graph (the kernel
+keeps no host-side state between calls, so replays are exact); --launch
+stream issues one host launch per call instead.
 
 Prints one JSON line. ``value`` is the whole step's algorithmic bytes over its
 time (GB/s). Algorithmic bytes per call = for every row stripe and every
@@ -365,6 +367,32 @@ def main():
         else:
             launch_calls(c, units if units is not None else step_units)
 
+    def capture_cycle(key, units):
+        # one rotation cycle (the steps of copies 0 .. n_copies-1, in order)
+        # as one graph: a decoder replays a whole token's pass over all its
+        # layers as one graph, so the graph's own start-up is paid once per
+        # many launches, not once per layer
+        s = torch.cuda.Stream(device=dev)
+        s.wait_stream(torch.cuda.current_stream(dev))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            for c in range(n_copies):
+                launch_calls(c, units)
+        torch.cuda.current_stream(dev).wait_stream(s)
+        graphs[(key, "cycle")] = g
+
+    def run_steps(first, n, mode, key="step", units=None):
+        # steps first .. first+n-1; in graph mode whole rotation cycles are
+        # one replay, the steps outside a whole cycle one replay each
+        i, end = first, first + n
+        while i < end:
+            if mode == "graph" and i % n_copies == 0 and i + n_copies <= end:
+                graphs[(key, "cycle")].replay()
+                i += n_copies
+            else:
+                step(i, mode, key, units)
+                i += 1
+
     def timed(fn, n):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -382,11 +410,12 @@ def main():
         for c in range(n_copies):
             capture(("step", c), c, step_units)
             capture(("single", c), c, single_units)
+        capture_cycle("step", step_units)
+        capture_cycle("single", single_units)
         torch.cuda.synchronize(dev)
-    for i in range(args.warmup):
-        step(i, args.launch)
+    run_steps(0, args.warmup, args.launch)
     torch.cuda.synchronize(dev)
-    total_ms = timed(lambda i: step(args.warmup + i, args.launch), args.steps)
+    total_ms = timed(lambda _: run_steps(args.warmup, args.steps, args.launch), 1)
     if args.calib_copy_mib:
         n = args.calib_copy_mib * (1 << 20)
         src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
@@ -408,8 +437,8 @@ def main():
     # the same steps with one host launch per call, and with every product
     # as its own launch, for comparison
     stream_ms = timed(lambda i: step(args.warmup + i, "stream"), args.steps) / args.steps
-    single_ms = timed(lambda i: step(args.warmup + i, args.launch, "single", single_units),
-                      args.steps) / args.steps
+    single_ms = timed(lambda _: run_steps(args.warmup, args.steps, args.launch, "single", single_units),
+                      1) / args.steps
 
     # ---- duration per sweep point: the point's calls run back to back (as a
     # captured graph in graph mode), so HIP events around a run of them
@@ -476,25 +505,33 @@ def main():
         torch.cuda.synchronize(dev)
         dgraphs = []
         if args.launch == "graph":
-            for c in range(n_dc):
+            # per copy, and one rotation cycle as one graph, as for spMspV
+            for cs in [[c] for c in range(n_dc)] + [list(range(n_dc))]:
                 s_cap = torch.cuda.Stream(device=dev)
                 s_cap.wait_stream(torch.cuda.current_stream(dev))
                 g = torch.cuda.CUDAGraph()
                 with torch.cuda.graph(g, stream=s_cap):
-                    dcalls(c)
+                    for c in cs:
+                        dcalls(c)
                 torch.cuda.current_stream(dev).wait_stream(s_cap)
                 dgraphs.append(g)
 
-        def dstep(i):
-            if dgraphs:
-                dgraphs[i % n_dc].replay()
-            else:
-                dcalls(i % n_dc)
+        def drun(first, n):
+            i, end = first, first + n
+            while i < end:
+                if dgraphs and i % n_dc == 0 and i + n_dc <= end:
+                    dgraphs[n_dc].replay()
+                    i += n_dc
+                else:
+                    if dgraphs:
+                        dgraphs[i % n_dc].replay()
+                    else:
+                        dcalls(i % n_dc)
+                    i += 1
 
-        for i in range(args.warmup):
-            dstep(i)
+        drun(0, args.warmup)
         torch.cuda.synchronize(dev)
-        d_us = timed(dstep, args.steps) * 1e3 / (args.steps * len(names))
+        d_us = timed(lambda _: drun(args.warmup, args.steps), 1) * 1e3 / (args.steps * len(names))
         del dgraphs
         dense = {"us_per_call": d_us,
                  "gbs": (w_bytes / len(names) + 2 * batch * (wl["projections"][0].rows + wl["projections"][0].cols)) / (d_us * 1e-6) / 1e9}
@@ -571,7 +608,7 @@ def main():
             "kernel": "spmspv_kernel",
             "kernel_us_per_launch": round(kernel_us, 3),
             "duration_source": "HIP events around the timed steps on the launch stream "
-                               f"({'captured graph per step' if args.launch == 'graph' else 'back-to-back launches'})",
+                               f"({'one captured graph per rotation cycle of steps' if args.launch == 'graph' else 'back-to-back launches'})",
             "algorithmic_bytes_per_launch": int(step_bytes / n_launch),
         },
         "cpu_baseline": cpu,
