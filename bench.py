@@ -336,13 +336,15 @@ def main():
     prep_s = time.perf_counter() - t_prep
     stream = torch.cuda.current_stream(dev)
 
-    def launch_calls(c, units):
+    def launch_calls(c, units, t_all=None):
+        # t_all: one threshold for every call instead of the points' own
+        th = (lambda j: points[j]["t"]) if t_all is None else (lambda j: t_all)
         for u in units:
             if len(u) == 1:
-                copies[c][u[0]].spmspv_into(X[c][u[0]], points[u[0]]["t"], Y[c][u[0]], mask=args.mask)
+                copies[c][u[0]].spmspv_into(X[c][u[0]], th(u[0]), Y[c][u[0]], mask=args.mask)
             else:
                 spdp.spmspv_many([copies[c][j] for j in u], [X[c][j] for j in u],
-                                 [points[j]["t"] for j in u], [Y[c][j] for j in u], mask=args.mask)
+                                 [th(j) for j in u], [Y[c][j] for j in u], mask=args.mask)
 
     all_idx = list(range(len(points)))
     grouped = args.group == "decoder"
@@ -367,7 +369,7 @@ def main():
         else:
             launch_calls(c, units if units is not None else step_units)
 
-    def capture_cycle(key, units):
+    def capture_cycle(key, units, t_all=None):
         # one rotation cycle (the steps of copies 0 .. n_copies-1, in order)
         # as one graph: a decoder replays a whole token's pass over all its
         # layers as one graph, so the graph's own start-up is paid once per
@@ -377,7 +379,7 @@ def main():
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=s):
             for c in range(n_copies):
-                launch_calls(c, units)
+                launch_calls(c, units, t_all)
         torch.cuda.current_stream(dev).wait_stream(s)
         graphs[(key, "cycle")] = g
 
@@ -437,6 +439,16 @@ def main():
     # the same steps with one host launch per call, and with every product
     # as its own launch, for comparison
     stream_ms = timed(lambda i: step(args.warmup + i, "stream"), args.steps) / args.steps
+    # the latency floor: the same launches with a threshold of +inf, so that
+    # no column is active and every step but the value stream runs (launch,
+    # set-up loads, activity test, list, split-K exchange, output)
+    floor_ms = None
+    if args.launch == "graph":
+        capture_cycle("floor", step_units, float("inf"))
+        run_steps(0, n_copies, "graph", "floor")
+        torch.cuda.synchronize(dev)
+        floor_ms = timed(lambda _: run_steps(0, args.steps // n_copies * n_copies or n_copies, "graph", "floor"),
+                         1) / (args.steps // n_copies * n_copies or n_copies)
     single_ms = timed(lambda _: run_steps(args.warmup, args.steps, args.launch, "single", single_units),
                       1) / args.steps
 
@@ -611,6 +623,10 @@ def main():
                                f"({'one captured graph per rotation cycle of steps' if args.launch == 'graph' else 'back-to-back launches'})",
             "algorithmic_bytes_per_launch": int(step_bytes / n_launch),
         },
+        "latency_floor": ({"us_per_launch": round(floor_ms * 1e3 / n_launch, 3),
+                           "frac_of_launch": round(floor_ms / kern_ms, 4),
+                           "how": "the same launches with threshold +inf: no column active, every step "
+                                  "but the value stream runs"} if floor_ms is not None else None),
         "cpu_baseline": cpu,
         "dense_gemv": dense,
         "speedup_vs_dense": round(dense["us_per_call"] / us_per_call, 3) if dense else None,
