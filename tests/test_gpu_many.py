@@ -226,3 +226,23 @@ def test_decoder_layer_chain_in_one_graph():
     del chain
     for m in mats.values():
         m.close()
+
+
+def test_many_nothing_active_gives_exact_zeros():
+    """A threshold of +inf leaves no column active (the bench's latency-floor
+    launches): every product of a grouped launch comes out exactly 0, at one
+    token and with both masks at several."""
+    dev = _dev()
+    shapes = [(4096, 4096), (1000, 4096), (300, 4096)]
+    ws = [oracle.magnitude_prune(synth.weights(r, c, 1200 + i), 0.5) for i, (r, c) in enumerate(shapes)]
+    mats = [spdp.encode(w, (256, 16)) for w in ws]
+    for batch, mask in ((1, "token"), (3, "token"), (3, "batch")):
+        print(f"[gpu] many, nothing active: batch {batch}, mask {mask}", flush=True)
+        X = _to_dev(synth.laplace_activations(batch, 4096, 1300 + batch))
+        Ys = [torch.full((batch, m.rows), float("nan"), dtype=torch.float16, device=dev) for m in mats]
+        spdp.spmspv_many(mats, [X] * len(mats), [float("inf")] * len(mats), Ys, mask=mask)
+        torch.cuda.synchronize()
+        for i, Y in enumerate(Ys):
+            assert torch.count_nonzero(Y).item() == 0 and not torch.isnan(Y).any().item(), f"product {i}"
+    for m in mats:
+        m.close()
