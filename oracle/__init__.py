@@ -35,6 +35,12 @@ Functions and the passages of the paper they follow:
 * ``algorithmic_bytes`` / ``useful_flops`` -- the bytes a call must move
   (active-column metadata + values + touched TileOffset entries + x + y)
   and the multiply-adds it must do.
+* ``rtn_quantize`` / ``encode_codes`` / ``decode_codes`` / ``spmspv_rtn``
+  -- low-bit Values: round-to-nearest weight-only quantization of the pruned
+  matrix (Sec. 5.1's quantization setup: pruning first, then quantization,
+  then dynamic pruning at inference), the same format with one byte per
+  code (Sec. 7: Values are stored apart from the sparsity metadata), and
+  the masked product with the dequantized weights.
 
 Readings where the paper is silent (bit order, array order, padding value,
 ColInfo offset unit, zero test, ragged shapes, threshold tie rule, batch>1
@@ -78,6 +84,12 @@ __all__ = [
     "combined_sparsity",
     "algorithmic_bytes",
     "useful_flops",
+    "rtn_quantize",
+    "rtn_dequantize",
+    "encode_codes",
+    "decode_codes",
+    "spmspv_rtn",
+    "algorithmic_bytes_codes",
 ]
 
 
@@ -530,3 +542,159 @@ def useful_flops(w_sp: np.ndarray, x: np.ndarray, t: float, mask: str = "token")
     act = active_mask(x, t, mask)
     nnz_col = ((_bits(np.asarray(w_sp, dtype=np.float16)) & 0x7FFF) != 0).sum(axis=0)
     return int(2 * (act * nnz_col[None, :]).sum())
+
+
+# --------------------------------------------------------------------------
+# Low-bit Values (Sec. 5.1 quantization setup; Sec. 7 on low-precision Values)
+# --------------------------------------------------------------------------
+
+def rtn_quantize(w_sp: np.ndarray, bits: int = 4):
+    """Round-to-nearest weight-only quantization of a pruned fp16 matrix.
+
+    The paper quantizes after pruning and before dynamic pruning, with 4-bit
+    round-to-nearest, and gives no further detail. Reading: symmetric, one
+    fp32 scale per output row, no zero point:
+
+        s_m = fp32(max_k |W_sp[m, k]|) / fp32(2^(bits-1) - 1)   (fp32 division)
+        q[m, k] = clamp(rint_even(fp32(W_sp[m, k]) / s_m), -qmax, qmax)
+
+    with the division in fp32 and ties to even. The sparsity pattern is the
+    pruning's: an entry is stored iff its magnitude bits are nonzero, also
+    when its code rounds to 0; pruned entries have code 0 and are not
+    stored. A row with no stored entry has scale 0. Non-finite weights are
+    rejected. Returns ``(codes int8 [M, K], scales float32 [M], pattern bool
+    [M, K])``.
+    """
+    if not (2 <= int(bits) <= 8):
+        raise ValueError("bits must be in [2, 8]")
+    wb = _bits(np.asarray(w_sp))
+    w32 = wb.view(np.float16).astype(np.float32)  # exact
+    if not np.all(np.isfinite(w32)):
+        raise ValueError("weights must be finite")
+    pattern = (wb & 0x7FFF) != 0
+    qmax = np.float32(2 ** (int(bits) - 1) - 1)
+    amax = np.where(pattern, np.abs(w32), np.float32(0)).max(axis=1).astype(np.float32)
+    scales = (amax / qmax).astype(np.float32)
+    codes = np.zeros(wb.shape, dtype=np.int8)
+    live = scales > 0
+    q = np.rint(w32[live] / scales[live, None]).astype(np.float32)
+    q = np.clip(q, -qmax, qmax)
+    codes[live] = np.where(pattern[live], q, 0).astype(np.int8)
+    return codes, scales, pattern
+
+
+def rtn_dequantize(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """The weights the quantized format stands for, in float64: s_m * q[m, k]."""
+    return np.asarray(scales, dtype=np.float64)[:, None] * np.asarray(codes, dtype=np.float64)
+
+
+def _pad16(n: int) -> int:
+    return (n + 15) // 16 * 16
+
+
+def encode_codes(codes: np.ndarray, pattern: np.ndarray, tile_m: int, tile_k: int) -> TiledCBC:
+    """Tiled-CBC with one byte per value: the layout of ``encode`` (same
+    GTile and column order, same bitmaps from the sparsity pattern), the
+    Values array holding the codes as two's-complement bytes, each column
+    padded with 0 to a multiple of 16 codes (16 bytes), and TileOffset and
+    the ColInfo offsets counted in codes.
+    """
+    _check_tile(tile_m, tile_k)
+    codes = np.asarray(codes, dtype=np.int8)
+    pattern = np.asarray(pattern, dtype=bool)
+    rows, cols = codes.shape
+    R = -(-rows // tile_m)
+    C = -(-cols // tile_k)
+    wpc = tile_m // 64
+    pc = np.zeros((R * tile_m, C * tile_k), dtype=np.int8)
+    pp = np.zeros((R * tile_m, C * tile_k), dtype=bool)
+    pc[:rows, :cols] = codes
+    pp[:rows, :cols] = pattern
+    tile_offset = np.zeros(R * C + 1, dtype=np.uint64)
+    col_info = np.zeros(R * C * tile_k, dtype=np.uint32)
+    bitmap = np.zeros(R * C * tile_k * wpc, dtype=np.uint64)
+    chunks = []
+    weights_of_bit = np.left_shift(np.uint64(1), np.arange(64, dtype=np.uint64))
+    total = 0
+    for r in range(R):
+        for c in range(C):
+            g = r * C + c
+            off = 0
+            for j in range(tile_k):
+                col = pc[r * tile_m:(r + 1) * tile_m, c * tile_k + j]
+                nz = pp[r * tile_m:(r + 1) * tile_m, c * tile_k + j]
+                for wi in range(wpc):
+                    seg = nz[64 * wi:64 * (wi + 1)]
+                    bitmap[(g * tile_k + j) * wpc + wi] = np.bitwise_or.reduce(
+                        np.where(seg, weights_of_bit, np.uint64(0)))
+                vals = col[nz]
+                nnz = int(vals.size)
+                padn = _pad16(nnz)
+                chunks.append(vals)
+                if padn > nnz:
+                    chunks.append(np.zeros(padn - nnz, dtype=np.int8))
+                col_info[g * tile_k + j] = (off << 16) | nnz
+                off += padn
+            total += off
+            tile_offset[g + 1] = total
+    if total > 0xFFFFFFFF:
+        raise ValueError("encoded matrix exceeds 2^32 - 1 values")
+    values = np.concatenate(chunks) if chunks else np.zeros(0, dtype=np.int8)
+    return TiledCBC(rows, cols, tile_m, tile_k, tile_offset.astype(np.uint32),
+                    col_info, bitmap, values.astype(np.int8).view(np.uint8))
+
+
+def decode_codes(f: TiledCBC):
+    """Rebuild ``(codes int8 [M, K], pattern bool [M, K])`` from a one-byte-per-value Tiled-CBC."""
+    R, C, wpc = f.n_stripes, f.n_colblocks, f.words_per_column
+    vals = np.asarray(f.values, dtype=np.uint8).view(np.int8)
+    codes = np.zeros((R * f.tile_m, C * f.tile_k), dtype=np.int8)
+    pattern = np.zeros((R * f.tile_m, C * f.tile_k), dtype=bool)
+    for r in range(R):
+        for c in range(C):
+            g = r * C + c
+            for j in range(f.tile_k):
+                ci = int(f.col_info[g * f.tile_k + j])
+                base = int(f.tile_offset[g]) + (ci >> 16)
+                rank = 0
+                for wi in range(wpc):
+                    word = int(f.bitmap[(g * f.tile_k + j) * wpc + wi])
+                    for i in range(64):
+                        if (word >> i) & 1:
+                            codes[r * f.tile_m + 64 * wi + i, c * f.tile_k + j] = vals[base + rank]
+                            pattern[r * f.tile_m + 64 * wi + i, c * f.tile_k + j] = True
+                            rank += 1
+                if rank != (ci & 0xFFFF):
+                    raise ValueError("bitmap popcount disagrees with ColInfo nnz")
+    return codes[:f.rows, :f.cols], pattern[:f.rows, :f.cols]
+
+
+def spmspv_rtn(codes: np.ndarray, scales: np.ndarray, x: np.ndarray, t: float, mask: str = "token"):
+    """The masked product with the dequantized weights, in float64:
+    ``y[b, m] = sum_k (s_m q[m, k]) xm[b, k]``. Returns ``(y64, s64, y16)``
+    as ``spmspv`` does, with ``S[b, m] = sum_k |s_m q[m, k]| |xm[b, k]|``.
+    """
+    wq = rtn_dequantize(codes, scales)
+    xm = masked_activations(np.atleast_2d(x), t, mask).astype(np.float64)
+    y64 = xm @ wq.T
+    s64 = np.abs(xm) @ np.abs(wq).T
+    return y64, s64, y64.astype(np.float16)
+
+
+def algorithmic_bytes_codes(f: TiledCBC, x: np.ndarray, t: float, mask: str = "token") -> int:
+    """``algorithmic_bytes`` for one byte per value: padded codes (pad16(nnz)
+    bytes) instead of fp16 values, plus the row scales (4 B per row)."""
+    x = np.atleast_2d(np.asarray(x, dtype=np.float16))
+    act = active_mask(x, t, mask).any(axis=0)
+    total = 0
+    for r in range(f.n_stripes):
+        touched = set()
+        for k in range(f.cols):
+            if not act[k]:
+                continue
+            _, nnz, _ = f.column(r, k)
+            total += 4 + f.tile_m // 8 + _pad16(nnz)
+            touched.add(k // f.tile_k)
+        total += 4 * len(touched)
+    b = x.shape[0]
+    return total + 2 * b * f.cols + 2 * b * f.rows + 4 * f.rows

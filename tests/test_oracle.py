@@ -533,3 +533,155 @@ def test_batch_mask_bytes_and_flops_brute_force():
     touched = len({k // 8 for k in range(40) if act[k]}) * f.n_stripes
     expect = sum(c for c, a in zip(per_col, act) if a) + 4 * touched + 2 * 3 * (40 + 70)
     assert oracle.algorithmic_bytes(f, x, t, "batch") == expect
+
+
+# ---------------------------------------------------------------------------
+# Low-bit Values: round-to-nearest quantization after pruning
+
+def test_rtn_hand_worked():
+    """Row 0: max |w| = 0.875, s = 0.875 / 7 = 0.125 exactly; 0.1875 / s = 1.5
+    and 0.3125 / s = 2.5 are ties (to even: 2 and 2); 0.0625 / s = 0.5 ties to
+    0 and stays stored (code 0); the pruned 0 and -0 are not stored. Row 1
+    has nothing stored: scale 0."""
+    w = np.array([[0.875, -0.1875, 0.0, 0.3125, 0.0625, -0.0],
+                  [0.0, 0.0, 0.0, 0.0, 0.0, 0.0]], dtype=np.float16)
+    codes, scales, pattern = oracle.rtn_quantize(w, 4)
+    assert scales.dtype == np.float32 and list(scales) == [0.125, 0.0]
+    assert codes.tolist() == [[7, -2, 0, 2, 0, 0], [0, 0, 0, 0, 0, 0]]
+    assert pattern.tolist() == [[True, True, False, True, True, False], [False] * 6]
+    f = oracle.encode_codes(codes, pattern, 64, 2)
+    # GTile 0 (columns 0, 1): {7}, {-2}, each padded to 16 codes; GTile 1
+    # (columns 2, 3): {}, {2}; GTile 2 (columns 4, 5): {0}, {}
+    assert f.tile_offset.tolist() == [0, 32, 48, 64]
+    assert f.col_info.tolist() == [1, (16 << 16) | 1, 0, 1, 1, 16 << 16]
+    v = f.values.view(np.int8)
+    assert v[0] == 7 and v[16] == -2 and v[32] == 2 and v[48] == 0 and len(v) == 64
+    assert [int(b) for b in f.bitmap] == [1, 1, 0, 1, 1, 0]
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+def test_rtn_exact_when_representable(bits):
+    """Weights that are s * q for integer q with |q| <= qmax and each row
+    reaching +-qmax come back exactly."""
+    rng = np.random.default_rng(bits)
+    qmax = 2 ** (bits - 1) - 1
+    q = rng.integers(-qmax, qmax + 1, size=(40, 70))
+    q[q == 0] = 1
+    q[:, 3] = qmax * np.where(rng.random(40) < 0.5, -1, 1)
+    s = 2.0 ** rng.integers(-9, -3, size=40)
+    w = (s[:, None] * q).astype(np.float16)
+    assert np.array_equal(w.astype(np.float64), s[:, None] * q)  # exactly fp16
+    codes, scales, pattern = oracle.rtn_quantize(w, bits)
+    assert pattern.all()
+    assert np.array_equal(codes, q) and np.array_equal(scales.astype(np.float64), s)
+    assert np.array_equal(oracle.rtn_dequantize(codes, scales), w.astype(np.float64))
+
+
+@pytest.mark.parametrize("bits", [2, 4, 6, 8])
+def test_rtn_error_bound_and_range(bits):
+    w = oracle.magnitude_prune(synth.weights(120, 300, 40 + bits), 0.6)
+    codes, scales, pattern = oracle.rtn_quantize(w, bits)
+    qmax = 2 ** (bits - 1) - 1
+    w64 = w.astype(np.float64)
+    assert np.all(np.abs(codes) <= qmax)
+    assert np.all(codes[~pattern] == 0)
+    # every row with a stored entry reaches +-qmax at its largest magnitude
+    for m in range(w.shape[0]):
+        if pattern[m].any():
+            k = int(np.argmax(np.where(pattern[m], np.abs(w64[m]), -1)))
+            assert abs(int(codes[m, k])) == qmax and np.sign(codes[m, k]) == np.sign(w64[m, k])
+    # round to nearest: within half a step, plus the fp32 rounding of the
+    # quotient w / s (relative 2^-24 of a quotient of at most qmax steps)
+    err = np.abs(oracle.rtn_dequantize(codes, scales) - np.where(pattern, w64, 0))
+    assert np.all(err <= scales.astype(np.float64)[:, None] * (0.5 + (qmax + 1) * 2.0 ** -24))
+    # the sign of a nonzero code is the weight's
+    nz = codes != 0
+    assert np.all(np.sign(codes[nz]) == np.sign(w64[nz]))
+
+
+def test_rtn_matches_scalar_loop():
+    """Element-by-element fp32 arithmetic in plain Python (NumPy scalars)."""
+    w = oracle.magnitude_prune(synth.weights(9, 23, 77), 0.4)
+    codes, scales, pattern = oracle.rtn_quantize(w, 4)
+    wb = w.view(np.uint16)
+    for m in range(9):
+        amax = np.float32(0)
+        for k in range(23):
+            if wb[m, k] & 0x7FFF:
+                amax = max(amax, np.float32(abs(float(w[m, k]))))
+        s = np.float32(amax / np.float32(7))
+        assert scales[m] == s
+        for k in range(23):
+            if not (wb[m, k] & 0x7FFF) or s == 0:
+                assert codes[m, k] == 0
+                continue
+            qv = float(np.float32(np.float32(float(w[m, k])) / s))
+            r = math.floor(qv)
+            frac = qv - r
+            q = r + 1 if frac > 0.5 or (frac == 0.5 and r % 2 == 1) else r
+            assert codes[m, k] == max(-7, min(7, q)), (m, k)
+
+
+def test_rtn_rejects_bad_input():
+    with pytest.raises(ValueError):
+        oracle.rtn_quantize(np.ones((2, 2), dtype=np.float16), 1)
+    with pytest.raises(ValueError):
+        oracle.rtn_quantize(np.ones((2, 2), dtype=np.float16), 9)
+    w = np.ones((2, 2), dtype=np.float16)
+    w[0, 1] = np.inf
+    with pytest.raises(ValueError):
+        oracle.rtn_quantize(w, 4)
+
+
+@pytest.mark.parametrize("rows,cols,tile", [(300, 200, (128, 16)), (70, 33, (64, 4)), (256, 64, (256, 64)), (5, 1, (64, 1))])
+def test_encode_codes_shares_the_pattern_of_encode(rows, cols, tile):
+    """Same bitmaps and nonzero counts as the fp16 encoding of the pruned
+    matrix; offsets are the running sums of pad16(nnz); decoding gives the
+    codes and the pattern back."""
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows + cols), 0.5)
+    codes, scales, pattern = oracle.rtn_quantize(w, 4)
+    f16 = oracle.encode(w, *tile)
+    fq = oracle.encode_codes(codes, pattern, *tile)
+    assert np.array_equal(fq.bitmap, f16.bitmap)
+    assert np.array_equal(fq.col_info & 0xFFFF, f16.col_info & 0xFFFF)
+    nnz = (fq.col_info & 0xFFFF).astype(np.int64).reshape(-1, tile[1])
+    pad = (nnz + 15) // 16 * 16
+    assert np.array_equal(fq.col_info >> 16, (np.cumsum(pad, axis=1) - pad).reshape(-1).astype(np.uint32))
+    assert np.array_equal(fq.tile_offset[1:], np.cumsum(pad.sum(axis=1)).astype(np.uint32))
+    assert fq.values.dtype == np.uint8 and len(fq.values) == int(fq.tile_offset[-1])
+    c2, p2 = oracle.decode_codes(fq)
+    assert np.array_equal(c2, codes) and np.array_equal(p2, pattern)
+
+
+def test_spmspv_rtn_exact_on_tiny_input():
+    """Exact rational arithmetic: y = sum_k s_m q[m,k] xm[k]."""
+    w = oracle.magnitude_prune(synth.weights(5, 11, 3), 0.3)
+    x = synth.laplace_activations(2, 11, 4)
+    t = float(oracle.threshold_for(x, 0.4))
+    codes, scales, _ = oracle.rtn_quantize(w, 4)
+    y64, s64, _ = oracle.spmspv_rtn(codes, scales, x, t)
+    xm = oracle.masked_activations(x, t)
+    for b in range(2):
+        for m in range(5):
+            exact = sum(Fraction(float(scales[m])) * int(codes[m, k]) * Fraction(float(xm[b, k])) for k in range(11))
+            mag = sum(abs(Fraction(float(scales[m])) * int(codes[m, k]) * Fraction(float(xm[b, k]))) for k in range(11))
+            assert abs(Fraction(y64[b, m]) - exact) <= Fraction(1, 2 ** 40) * (mag + 1)
+            assert abs(Fraction(s64[b, m]) - mag) <= Fraction(1, 2 ** 40) * (mag + 1)
+
+
+def test_algorithmic_bytes_codes_brute():
+    w = oracle.magnitude_prune(synth.weights(130, 40, 8), 0.5)
+    x = synth.laplace_activations(1, 40, 9)
+    t = float(oracle.threshold_for(x, 0.5))
+    codes, scales, pattern = oracle.rtn_quantize(w, 4)
+    f = oracle.encode_codes(codes, pattern, 64, 8)
+    act = oracle.active_mask(x, t).any(axis=0)
+    total = 0
+    for r in range(f.n_stripes):
+        for k in range(40):
+            if act[k]:
+                nnz = int(pattern[64 * r:64 * (r + 1), k].sum())
+                total += 4 + 8 + (nnz + 15) // 16 * 16
+        total += 4 * len({k // 8 for k in range(40) if act[k]})
+    total += 2 * 40 + 2 * 130 + 4 * 130
+    assert oracle.algorithmic_bytes_codes(f, x, t) == total
