@@ -199,9 +199,48 @@ typedef struct spdp_format {
   const void* d_bitmap;
   const void* d_values;
   int32_t device; /* HIP device ordinal of the copies, -1 if host-only */
+  /* 16 for fp16 values; 2..8 for a handle from spdp_encode_rtn, whose
+     Values are codes (then `values` is NULL, n_values counts codes, and
+     tile_offset and the ColInfo offsets count codes) */
+  int32_t value_bits;
+  const int8_t* codes;  /* host, n_values, or NULL */
+  const float* scales;  /* host, rows, or NULL */
+  const void* d_scales; /* device copy (or NULL) */
 } spdp_format_t;
 
 int spdp_format(spdp_handle_t h, spdp_format_t* out);
+
+/*
+ * spdp_encode_rtn -- low-bit Values (Sec. 5.1's quantization setup: the
+ * weights are quantized after pruning, and dynamic pruning runs on top at
+ * inference; Sec. 7: Values are stored apart from the sparsity metadata).
+ * W (already pruned, as for spdp_encode) is quantized to `bits`-bit
+ * round-to-nearest codes, symmetric, one fp32 scale per row:
+ *     s[m] = fp32(max over the row's nonzeros of |W[m,k]|) / (2^(bits-1) - 1)
+ *     q[m,k] = clamp(rint(fp32(W[m,k]) / s[m]), -(2^(bits-1)-1), 2^(bits-1)-1)
+ * (fp32 division, ties to even; a row without nonzeros has s = 0). The
+ * Tiled-CBC layout is that of spdp_encode -- the same GTiles, column order,
+ * bitmaps and nonzero counts (the pruning's pattern: a nonzero whose code is
+ * 0 stays stored) -- with one two's-complement byte per code in Values,
+ * each column padded with 0 to a multiple of 16 codes (16 bytes), and
+ * tile_offset / ColInfo offsets counted in codes. spdp_spmspv* on such a
+ * handle computes y[b,m] = fp16(s[m] * sum_k q[m,k] xm[b,k]) (fp32
+ * accumulation, the scale applied once per row, one rounding to fp16).
+ *
+ *   bits     2..8 (the paper uses 4); otherwise SPDP_ERR_INVALID_ARG.
+ *   Non-finite weights: SPDP_ERR_INVALID_ARG. Other arguments, ownership
+ *   and errors as spdp_encode. Products of one spdp_spmspv_many call must
+ *   all be fp16 or all be codes.
+ */
+int spdp_encode_rtn(const uint16_t* W, int64_t rows, int64_t cols,
+                    int32_t tile_m, int32_t tile_k, int32_t bits,
+                    spdp_handle_t* out);
+/* spdp_encode_rtn_host -- the same without a device copy (host-only handle,
+ * for spdp_format; spdp_spmspv on it is SPDP_ERR_INVALID_ARG). */
+int spdp_encode_rtn_host(const uint16_t* W, int64_t rows, int64_t cols,
+                         int32_t tile_m, int32_t tile_k, int32_t bits,
+                         spdp_handle_t* out);
+
 
 /*
  * Offline preparation helpers (host only, no device work).

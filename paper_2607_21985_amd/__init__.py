@@ -28,6 +28,8 @@ __all__ = [
     "lib_path",
     "encode",
     "encode_host",
+    "encode_rtn",
+    "encode_rtn_host",
     "spmspv_many",
     "MASKS",
     "Chain",
@@ -45,6 +47,7 @@ EXPORTED_SYMBOLS = (
     "spdp_reserve", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
+    "spdp_encode_rtn", "spdp_encode_rtn_host",
 )
 
 SPDP_OK = 0
@@ -73,6 +76,10 @@ class _Format(ctypes.Structure):
         ("d_tile_offset", ctypes.c_void_p), ("d_col_info", ctypes.c_void_p),
         ("d_bitmap", ctypes.c_void_p), ("d_values", ctypes.c_void_p),
         ("device", ctypes.c_int32),
+        ("value_bits", ctypes.c_int32),
+        ("codes", ctypes.POINTER(ctypes.c_int8)),
+        ("scales", ctypes.POINTER(ctypes.c_float)),
+        ("d_scales", ctypes.c_void_p),
     ]
 
 
@@ -96,6 +103,8 @@ def lib() -> ctypes.CDLL:
     H = ctypes.c_void_p
     L.spdp_encode.argtypes = [u16p, i64, i64, i32, i32, ctypes.POINTER(H)]
     L.spdp_encode_host.argtypes = [u16p, i64, i64, i32, i32, ctypes.POINTER(H)]
+    L.spdp_encode_rtn.argtypes = [u16p, i64, i64, i32, i32, i32, ctypes.POINTER(H)]
+    L.spdp_encode_rtn_host.argtypes = [u16p, i64, i64, i32, i32, i32, ctypes.POINTER(H)]
     L.spdp_spmspv.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
     L.spdp_spmspv_many.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_void_p),
@@ -167,14 +176,22 @@ class Matrix:
                 return np.zeros(0, dtype=dt)
             return np.ctypeslib.as_array(p, shape=(n,)).astype(dt, copy=True)
 
-        return {
+        out = {
             "rows": int(f.rows), "cols": int(f.cols), "tile_m": tm, "tile_k": tk,
             "n_stripes": int(f.n_stripes), "n_colblocks": int(f.n_colblocks), "n_gtiles": ngt,
             "tile_offset": arr(f.tile_offset, ngt + 1, np.uint32),
             "col_info": arr(f.col_info, ngt * tk, np.uint32),
             "bitmap": arr(f.bitmap, ngt * tk * tm // 64, np.uint64),
-            "values": arr(f.values, int(f.n_values), np.uint16),
+            "value_bits": int(f.value_bits),
         }
+        if f.value_bits < 16:
+            # one byte per code; "values" holds the codes' bytes
+            out["codes"] = arr(f.codes, int(f.n_values), np.int8)
+            out["values"] = out["codes"].view(np.uint8)
+            out["scales"] = arr(f.scales, int(f.rows), np.float32)
+        else:
+            out["values"] = arr(f.values, int(f.n_values), np.uint16)
+        return out
 
     def device_pointers(self) -> dict:
         f = self._fmt()
@@ -313,6 +330,30 @@ def spmspv_many(mats, xs, thresholds, ys, stream=None, mask: str = "token") -> N
     ts = (ctypes.c_float * n)(*[float(t) for t in thresholds])
     _check(lib().spdp_spmspv_many_mask(hs, n, xp, int(xs[0].shape[0]), ts, _mask_code(mask), yp,
                                        ctypes.c_void_p(s.cuda_stream)))
+
+
+def encode_rtn(w: np.ndarray, tile=(256, 16), bits: int = 4) -> Matrix:
+    """Quantize a pruned fp16 matrix to ``bits``-bit round-to-nearest codes
+    (one scale per row), encode it with one byte per code and upload it."""
+    wb = _u16(w)
+    if wb.ndim != 2:
+        raise ValueError("w must be 2-D")
+    _free_deferred()
+    h = ctypes.c_void_p()
+    _check(lib().spdp_encode_rtn(_ptr(wb), wb.shape[0], wb.shape[1], int(tile[0]), int(tile[1]),
+                                 int(bits), ctypes.byref(h)))
+    return Matrix(h)
+
+
+def encode_rtn_host(w: np.ndarray, tile=(256, 16), bits: int = 4) -> Matrix:
+    """``encode_rtn`` without touching any device."""
+    wb = _u16(w)
+    if wb.ndim != 2:
+        raise ValueError("w must be 2-D")
+    h = ctypes.c_void_p()
+    _check(lib().spdp_encode_rtn_host(_ptr(wb), wb.shape[0], wb.shape[1], int(tile[0]), int(tile[1]),
+                                      int(bits), ctypes.byref(h)))
+    return Matrix(h)
 
 
 def encode_host(w: np.ndarray, tile=(256, 16)) -> Matrix:

@@ -77,8 +77,9 @@ void clear_error() { g_last_error.clear(); }
 // the bitmap words, ColInfo entries and the packed, 8-element-padded values.
 // A serial prefix sum over GTile sizes gives TileOffset, and the per-stripe
 // value runs are then copied into place in parallel.
-int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
-                       int32_t tile_m, int32_t tile_k, spdp_matrix* m) {
+namespace {
+
+int check_shape(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m, int32_t tile_k) {
   if (!W) return fail(SPDP_ERR_INVALID_ARG, "W is NULL");
   if (rows < 1 || cols < 1) return fail(SPDP_ERR_INVALID_ARG, "rows and cols must be >= 1");
   if (!valid_tile(tile_m, tile_k)) {
@@ -87,13 +88,25 @@ int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
     return fail(SPDP_ERR_INVALID_ARG,
                 "tile_m must be a multiple of 64 in [64, 256] and tile_k a power of two in [1, 256]");
   }
+  if ((rows + tile_m - 1) / tile_m > 65535) return fail(SPDP_ERR_UNSUPPORTED, "more than 65535 row stripes");
+  if ((cols + tile_k - 1) / tile_k * tile_k > (int64_t)1 << 31) return fail(SPDP_ERR_UNSUPPORTED, "too many columns");
+  return SPDP_OK;
+}
+
+// The stripe walk for either value type: T = uint16_t (fp16 bits, columns
+// padded to 8 elements) or int8_t (codes, padded to 16); both pads are 16
+// bytes. value_of(row, h) is the element stored for the nonzero of `row`
+// whose fp16 bits are h (it is also called, and its result discarded, for
+// zeros and for the padding rows past the last one).
+template <typename T, typename ValueOf>
+int walk(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m, int32_t tile_k, ValueOf value_of,
+         spdp_matrix* m, std::vector<T>* values) {
+  constexpr uint32_t kPad = 16 / sizeof(T);
   const int64_t R = (rows + tile_m - 1) / tile_m;
   const int64_t C = (cols + tile_k - 1) / tile_k;
   const int64_t NGT = R * C;
   const int wpc = tile_m / 64;
   const int64_t kpad = C * tile_k;
-  if (R > 65535) return fail(SPDP_ERR_UNSUPPORTED, "more than 65535 row stripes");
-  if (kpad > (int64_t)1 << 31) return fail(SPDP_ERR_UNSUPPORTED, "too many columns");
 
   try {
     m->col_info.assign((size_t)(NGT * tile_k), 0u);
@@ -102,12 +115,13 @@ int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
   } catch (const std::bad_alloc&) {
     return fail(SPDP_ERR_OOM, "host allocation for the format arrays failed");
   }
-  std::vector<std::vector<uint16_t>> stripe_vals((size_t)R);
+  std::vector<std::vector<T>> stripe_vals((size_t)R);
   std::vector<uint64_t> gtile_size((size_t)NGT, 0);
   std::atomic<bool> oom{false};
 
   parallel_for(R, [&](int64_t r) {
-    std::vector<uint16_t> colbuf, vals;
+    std::vector<uint16_t> colbuf;
+    std::vector<T> vals;
     try {
       colbuf.assign((size_t)(kpad * tile_m), 0);
       vals.resize((size_t)(kpad * tile_m));
@@ -139,13 +153,13 @@ int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
             const uint16_t h = col[64 * w + i];
             const uint64_t nz = (h & 0x7FFF) != 0;
             word |= nz << i;
-            vals[pos] = h;
+            vals[pos] = value_of(m0 + 64 * w + i, h);
             pos += nz;
           }
           m->bitmap[(size_t)((g * tile_k + j) * wpc + w)] = word;
           nnz += (uint32_t)__builtin_popcountll(word);
         }
-        const uint32_t padded = (nnz + 7u) & ~7u;
+        const uint32_t padded = (nnz + kPad - 1) & ~(kPad - 1);
         for (uint32_t z = nnz; z < padded; ++z) vals[pos++] = 0;
         m->col_info[(size_t)(g * tile_k + j)] = (off << 16) | nnz;
         off += padded;
@@ -166,15 +180,14 @@ int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
     m->tile_offset[(size_t)(g + 1)] = (uint32_t)total;
   }
   try {
-    m->values.resize((size_t)total);
+    values->resize((size_t)total);
   } catch (const std::bad_alloc&) {
     return fail(SPDP_ERR_OOM, "host allocation for values failed");
   }
   parallel_for(R, [&](int64_t r) {
     const auto& v = stripe_vals[(size_t)r];
     if (!v.empty())
-      std::memcpy(m->values.data() + m->tile_offset[(size_t)(r * C)], v.data(),
-                  v.size() * sizeof(uint16_t));
+      std::memcpy(values->data() + m->tile_offset[(size_t)(r * C)], v.data(), v.size() * sizeof(T));
   });
   m->rows = rows;
   m->cols = cols;
@@ -184,6 +197,58 @@ int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
   m->n_colblocks = C;
   m->n_gtiles = NGT;
   return SPDP_OK;
+}
+
+}  // namespace
+
+int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
+                       int32_t tile_m, int32_t tile_k, spdp_matrix* m) {
+  const int st = check_shape(W, rows, cols, tile_m, tile_k);
+  if (st != SPDP_OK) return st;
+  m->value_bits = 16;
+  return walk<uint16_t>(W, rows, cols, tile_m, tile_k, [](int64_t, uint16_t h) { return h; }, m, &m->values);
+}
+
+// Round-to-nearest quantization after pruning (Sec. 5.1 quantization setup:
+// symmetric, one scale per row): s = fp32(max |w| of the row's nonzeros) /
+// (2^(bits-1) - 1), code = clamp(rint(fp32(w) / s)) with fp32 division and
+// ties to even; the sparsity pattern stays the pruning's (a nonzero whose
+// code is 0 is still stored), and a row with no nonzero has scale 0.
+int encode_host_arrays_rtn(const uint16_t* W, int64_t rows, int64_t cols,
+                           int32_t tile_m, int32_t tile_k, int32_t bits, spdp_matrix* m) {
+  int st = check_shape(W, rows, cols, tile_m, tile_k);
+  if (st != SPDP_OK) return st;
+  if (bits < 2 || bits > 8) return fail(SPDP_ERR_INVALID_ARG, "bits must be in [2, 8]");
+  const float qmax = (float)((1 << (bits - 1)) - 1);
+  try {
+    m->scales.assign((size_t)rows, 0.0f);
+  } catch (const std::bad_alloc&) {
+    return fail(SPDP_ERR_OOM, "host allocation for the scales failed");
+  }
+  std::atomic<bool> non_finite{false};
+  parallel_for(rows, [&](int64_t r) {
+    float amax = 0.0f;
+    for (int64_t k = 0; k < cols; ++k) {
+      const uint16_t h = W[r * cols + k];
+      if ((h & 0x7FFF) == 0) continue;
+      if ((h & 0x7C00) == 0x7C00) {
+        non_finite = true;
+        return;
+      }
+      amax = std::max(amax, (float)std::fabs(half_value(h)));
+    }
+    m->scales[(size_t)r] = amax / qmax;
+  });
+  if (non_finite) return fail(SPDP_ERR_INVALID_ARG, "weights must be finite (inf or NaN found)");
+  const float* sc = m->scales.data();
+  auto code = [sc, rows, qmax](int64_t row, uint16_t h) -> int8_t {
+    const float s = sc[std::min(row, rows - 1)];
+    if ((h & 0x7FFF) == 0 || !(s > 0.0f)) return 0;
+    const float q = std::nearbyint((float)half_value(h) / s);
+    return (int8_t)std::min(std::max(q, -qmax), qmax);
+  };
+  m->value_bits = bits;
+  return walk<int8_t>(W, rows, cols, tile_m, tile_k, code, m, &m->codes);
 }
 
 }  // namespace spdp
@@ -224,6 +289,22 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
   return SPDP_OK;
 }
 
+int spdp_encode_rtn_host(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m, int32_t tile_k,
+                         int32_t bits, spdp_handle_t* out) {
+  spdp::clear_error();
+  if (!out) return fail(SPDP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  spdp_matrix* m = new (std::nothrow) spdp_matrix();
+  if (!m) return fail(SPDP_ERR_OOM, "host allocation failed");
+  const int st = spdp::encode_host_arrays_rtn(W, rows, cols, tile_m, tile_k, bits, m);
+  if (st != SPDP_OK) {
+    delete m;
+    return st;
+  }
+  *out = m;
+  return SPDP_OK;
+}
+
 int spdp_format(spdp_handle_t h, spdp_format_t* out) {
   spdp::clear_error();
   if (!h || !out) return fail(SPDP_ERR_INVALID_ARG, "handle or out is NULL");
@@ -234,16 +315,21 @@ int spdp_format(spdp_handle_t h, spdp_format_t* out) {
   out->n_stripes = h->n_stripes;
   out->n_colblocks = h->n_colblocks;
   out->n_gtiles = h->n_gtiles;
-  out->n_values = (int64_t)h->values.size();
+  const bool q = h->value_bits < 16;
+  out->n_values = (int64_t)(q ? h->codes.size() : h->values.size());
   out->tile_offset = h->tile_offset.data();
   out->col_info = h->col_info.data();
   out->bitmap = h->bitmap.data();
-  out->values = h->values.data();
+  out->values = q ? nullptr : h->values.data();
   out->d_tile_offset = h->d_tile_offset;
   out->d_col_info = h->d_col_info;
   out->d_bitmap = h->d_bitmap;
   out->d_values = h->d_values;
   out->device = h->device;
+  out->value_bits = h->value_bits;
+  out->codes = q ? h->codes.data() : nullptr;
+  out->scales = q ? h->scales.data() : nullptr;
+  out->d_scales = h->d_scales;
   return SPDP_OK;
 }
 

@@ -17,13 +17,19 @@ struct spdp_matrix {
   std::vector<uint32_t> tile_offset;
   std::vector<uint32_t> col_info;
   std::vector<uint64_t> bitmap;
-  std::vector<uint16_t> values;
+  std::vector<uint16_t> values;  // fp16 bits (value_bits == 16)
+  // value_bits 2..8: round-to-nearest codes, one byte each, in place of
+  // `values`, and one fp32 scale per row
+  int32_t value_bits = 16;
+  std::vector<int8_t> codes;
+  std::vector<float> scales;
 
   int device = -1;  // -1: host-only handle
   void* d_tile_offset = nullptr;
   void* d_col_info = nullptr;
   void* d_bitmap = nullptr;
-  void* d_values = nullptr;
+  void* d_values = nullptr;  // fp16 values or codes
+  void* d_scales = nullptr;
 
   // Split-K workspace: {fp32 partial sum, phase} pairs
   // [segments - 1][batch][n_stripes*tile_m], and each row stripe's phase
@@ -42,5 +48,9 @@ void clear_error();
 // Validates shape/tile arguments and fills the host arrays of `m`.
 int encode_host_arrays(const uint16_t* W, int64_t rows, int64_t cols,
                        int32_t tile_m, int32_t tile_k, spdp_matrix* m);
+// The same with the weights quantized to `bits`-bit round-to-nearest codes
+// (one fp32 scale per row) and stored one byte per code.
+int encode_host_arrays_rtn(const uint16_t* W, int64_t rows, int64_t cols,
+                           int32_t tile_m, int32_t tile_k, int32_t bits, spdp_matrix* m);
 
 }  // namespace spdp

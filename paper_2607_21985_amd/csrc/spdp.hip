@@ -78,7 +78,8 @@ struct MatArgs {
   const uint32_t* tile_offset;
   const uint32_t* col_info;
   const uint64_t* bitmap;
-  const uint16_t* values;
+  const uint16_t* values;  // fp16 values, or one-byte codes (the kernel's Q form)
+  const float* scales;     // Q form: one scale per row
   const uint16_t* x;
   uint16_t* y;
   // [segments][batch][n_stripes * tile_m]: {fp32 bits, phase} pairs
@@ -283,8 +284,9 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
-// column (tile_m / 64).
-template <int NB, int WPC, bool EARLY, bool BMASK>
+// column (tile_m / 64); Q: Values are one-byte round-to-nearest codes with a
+// scale per row (else fp16).
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
@@ -403,8 +405,9 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // bitmap array's zeroed tail and the first 16 bytes of the values, and
   // decode to nothing
   auto put = [&](int c, int p) __attribute__((always_inline)) {
-    const uint32_t chunks = ((ci[c] & 0xFFFFu) + 7u) >> 3;
-    ent_s[p] = make_uint2(2u * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
+    // 16-byte chunks of the column's padded values (8 fp16 or 16 codes each)
+    const uint32_t chunks = Q ? ((ci[c] & 0xFFFFu) + 15u) >> 4 : ((ci[c] & 0xFFFFu) + 7u) >> 3;
+    ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int mag = (int)(xb[c][b] & 0x7FFFu);
@@ -532,11 +535,22 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       uint32_t sb = lds_addr(slot + (u0 + c) * kSlotBytes);
 #pragma unroll
       for (int w = 0; w < WPC; ++w) {
-        const uint32_t a = sb + 2u * mbcnt64(m[c][w]);
-        vb[c][w] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)a;
-        if (w + 1 < WPC) {
-          const uint32_t pop = (uint32_t)__builtin_popcountll(m[c][w]);
-          asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+        if constexpr (Q) {
+          // a code is one byte: no shift in the address (an add instead:
+          // the mbcnt cannot take both the mask and the base from scalar
+          // registers); the signed code becomes an fp16 integer (exact for
+          // |q| <= 127), and the rest of the decode is that of fp16 values
+          const uint32_t a = sb + mbcnt64(m[c][w]);
+          const int q = *(const __attribute__((address_space(3))) int8_t*)(uintptr_t)a;
+          vb[c][w] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)(int16_t)q);
+          if (w + 1 < WPC) sb += (uint32_t)__builtin_popcountll(m[c][w]);
+        } else {
+          const uint32_t a = sb + 2u * mbcnt64(m[c][w]);
+          vb[c][w] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)a;
+          if (w + 1 < WPC) {
+            const uint32_t pop = (uint32_t)__builtin_popcountll(m[c][w]);
+            asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+          }
         }
       }
     }
@@ -674,6 +688,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     const int m = r * ka->tile_m + 64 * w + lane;
     const bool live = m < rows;
     const unsigned long long* src = ka->partials + (live ? m : 0);
+    // Q form: the row's scale, requested ahead of the partials
+    const float row_scale = Q ? (live ? ka->scales[m] : 0.0f) : 1.0f;
     float sums[NB];
 #pragma unroll
     for (int b = 0; b < NB; ++b) sums[b] = 0.0f;
@@ -724,7 +740,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
         red[wave * 64 + lane] = sums[b];
         __syncthreads();
         if (wave == 0 && live) {
-          const float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
+          float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
+          if constexpr (Q) t *= row_scale;  // y = s * sum q x, rounded once to fp16
           ka->y[(size_t)b * rows + m] = __half_as_ushort(__float2half_rn(t));
         }
       }
@@ -818,10 +835,10 @@ void release_device(spdp_matrix* m) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
-  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_partials, m->d_phase};
+  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_scales, m->d_partials, m->d_phase};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
-  m->d_tile_offset = m->d_col_info = m->d_bitmap = m->d_values = nullptr;
+  m->d_tile_offset = m->d_col_info = m->d_bitmap = m->d_values = m->d_scales = nullptr;
   m->d_partials = nullptr;
   m->d_phase = nullptr;
   m->partial_floats = 0;
@@ -851,34 +868,40 @@ int upload(const std::vector<T>& v, void** dst) {
   return SPDP_OK;
 }
 
-template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, dim3 grid, hipStream_t stream) {
+template <int NB, int WPC, bool Q>
+hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, dim3 grid, hipStream_t stream) {
   // the one-token kernel has the early-first-batch form (no product with
   // more tokens asks for it); the kernels for more tokens have the shared
   // batch mask form (at one token the two masks are the same rule, and the
   // host sends such calls to the per-token kernel)
   if constexpr (NB == 1) {
     if (early) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   } else {
     if (bmask) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false>), grid, dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
+template <int NB, int WPC>
+hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool q, dim3 grid, hipStream_t stream) {
+  return q ? launch_form<NB, WPC, true>(args, early, bmask, grid, stream)
+           : launch_form<NB, WPC, false>(args, early, bmask, grid, stream);
+}
+
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, dim3 grid, hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool q, dim3 grid, hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, early, bmask, grid, stream);
-    case 2: return launch_one<NB, 2>(args, early, bmask, grid, stream);
-    case 3: return launch_one<NB, 3>(args, early, bmask, grid, stream);
-    default: return launch_one<NB, 4>(args, early, bmask, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, bmask, q, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, bmask, q, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, bmask, q, grid, stream);
+    default: return launch_one<NB, 4>(args, early, bmask, q, grid, stream);
   }
 }
 
@@ -928,6 +951,7 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   a.col_info = static_cast<const uint32_t*>(h->d_col_info);
   a.bitmap = static_cast<const uint64_t*>(h->d_bitmap);
   a.values = static_cast<const uint16_t*>(h->d_values);
+  a.scales = static_cast<const float*>(h->d_scales);
   a.x = X;
   a.y = Y;
   a.partials = h->d_partials;
@@ -954,22 +978,10 @@ bool overlap(const void* p, size_t pn, const void* q, size_t qn) {
   return a0 < b0 + qn && b0 < a0 + pn;
 }
 
-}  // namespace
-
-extern "C" {
-
-int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
-                int32_t tile_k, spdp_handle_t* out) {
-  spdp::clear_error();
-  if (!out) return fail(SPDP_ERR_INVALID_ARG, "out is NULL");
-  *out = nullptr;
-  spdp_matrix* m = new (std::nothrow) spdp_matrix();
-  if (!m) return fail(SPDP_ERR_OOM, "host allocation failed");
-  int st = spdp::encode_host_arrays(W, rows, cols, tile_m, tile_k, m);
-  if (st != SPDP_OK) {
-    delete m;
-    return st;
-  }
+// Uploads the host arrays of a freshly encoded matrix to the current device
+// and sizes its workspace for one token; on failure frees what it made and
+// the matrix itself.
+int finish_device(spdp_matrix* m, spdp_handle_t* out) {
   // the kernel packs a GTile column index (the all-zero padding column
   // included) into 26 bits and addresses values and bitmaps with 32-bit
   // byte offsets
@@ -977,7 +989,8 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
     delete m;
     return fail(SPDP_ERR_UNSUPPORTED, "more than 2^26 - 2 GTile columns (row stripes x padded columns)");
   }
-  if ((uint64_t)m->values.size() * 2 + kTailBytes >= (uint64_t(1) << 32)) {
+  const uint64_t value_bytes = m->value_bits < 16 ? (uint64_t)m->codes.size() : (uint64_t)m->values.size() * 2;
+  if (value_bytes + kTailBytes >= (uint64_t(1) << 32)) {
     delete m;
     return fail(SPDP_ERR_UNSUPPORTED, "more than 4 GiB of padded values");
   }
@@ -988,10 +1001,11 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
     return hip_fail(e, "hipGetDevice");
   }
   m->device = dev;
-  st = upload(m->tile_offset, &m->d_tile_offset);
+  int st = upload(m->tile_offset, &m->d_tile_offset);
   if (st == SPDP_OK) st = upload(m->col_info, &m->d_col_info);
   if (st == SPDP_OK) st = upload(m->bitmap, &m->d_bitmap);
-  if (st == SPDP_OK) st = upload(m->values, &m->d_values);
+  if (st == SPDP_OK) st = m->value_bits < 16 ? upload(m->codes, &m->d_values) : upload(m->values, &m->d_values);
+  if (st == SPDP_OK && m->value_bits < 16) st = upload(m->scales, &m->d_scales);
   if (st == SPDP_OK) {
     // every stripe starts in phase 1
     std::vector<uint32_t> ones((size_t)m->n_stripes, 1u);
@@ -1016,6 +1030,40 @@ int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
   }
   *out = m;
   return SPDP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int spdp_encode(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
+                int32_t tile_k, spdp_handle_t* out) {
+  spdp::clear_error();
+  if (!out) return fail(SPDP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  spdp_matrix* m = new (std::nothrow) spdp_matrix();
+  if (!m) return fail(SPDP_ERR_OOM, "host allocation failed");
+  const int st = spdp::encode_host_arrays(W, rows, cols, tile_m, tile_k, m);
+  if (st != SPDP_OK) {
+    delete m;
+    return st;
+  }
+  return finish_device(m, out);
+}
+
+int spdp_encode_rtn(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m,
+                    int32_t tile_k, int32_t bits, spdp_handle_t* out) {
+  spdp::clear_error();
+  if (!out) return fail(SPDP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  spdp_matrix* m = new (std::nothrow) spdp_matrix();
+  if (!m) return fail(SPDP_ERR_OOM, "host allocation failed");
+  const int st = spdp::encode_host_arrays_rtn(W, rows, cols, tile_m, tile_k, bits, m);
+  if (st != SPDP_OK) {
+    delete m;
+    return st;
+  }
+  return finish_device(m, out);
 }
 
 int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
@@ -1069,6 +1117,8 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uin
     if (st != SPDP_OK) return st;
     if (handles[i]->tile_m != handles[0]->tile_m)
       return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
+    if ((handles[i]->value_bits < 16) != (handles[0]->value_bits < 16))
+      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must all hold fp16 values or all codes");
     if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
     widest = std::max(widest, n_wg);
     early = early || la.m[i].early_first;
@@ -1076,19 +1126,20 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uin
 
   const int wpc = handles[0]->tile_m / 64;
   const dim3 grid((unsigned)widest, (unsigned)count);
+  const bool q = handles[0]->value_bits < 16;
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (batch <= 1)
-    e = launch<1>(la, wpc, early, bmask, grid, s);
+    e = launch<1>(la, wpc, early, bmask, q, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, early, bmask, grid, s);
+    e = launch<2>(la, wpc, early, bmask, q, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, early, bmask, grid, s);
+    e = launch<4>(la, wpc, early, bmask, q, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, early, bmask, grid, s);
+    e = launch<8>(la, wpc, early, bmask, q, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, early, bmask, grid, s);
+    e = launch<16>(la, wpc, early, bmask, q, grid, s);
   else
-    e = launch<32>(la, wpc, early, bmask, grid, s);
+    e = launch<32>(la, wpc, early, bmask, q, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }

@@ -87,6 +87,34 @@ def test_spmspv_on_host_only_handle_is_rejected():
     m.close()
 
 
+def test_rtn_encode_argument_errors():
+    w = np.ones((64, 16), dtype=np.float16)
+    for bits in (0, 1, 9, 16):
+        with pytest.raises(spdp.SpdpError) as e:
+            spdp.encode_rtn_host(w, (64, 16), bits)
+        assert e.value.status == ERR_INVALID and "bits" in str(e.value)
+    w[3, 4] = np.inf
+    with pytest.raises(spdp.SpdpError) as e:
+        spdp.encode_rtn_host(w, (64, 16), 4)
+    assert e.value.status == ERR_INVALID and "finite" in str(e.value)
+    w[3, 4] = np.nan
+    with pytest.raises(spdp.SpdpError):
+        spdp.encode_rtn_host(w, (64, 16), 4)
+    with pytest.raises(spdp.SpdpError) as e:
+        spdp.encode_rtn_host(np.ones((64, 16), dtype=np.float16), (100, 16), 4)
+    assert e.value.status == ERR_INVALID
+    # a host-only code handle cannot run a product
+    m = spdp.encode_rtn_host(np.ones((64, 16), dtype=np.float16), (64, 16), 4)
+    L = spdp.lib()
+    x = np.zeros(64, dtype=np.uint16)
+    st = L.spdp_spmspv(m._h, ctypes.c_void_p(x.ctypes.data), 1, ctypes.c_float(0.0),
+                       ctypes.c_void_p(x.ctypes.data + 64), None)
+    assert st == ERR_INVALID
+    f = m.format()
+    assert f["value_bits"] == 4 and f["codes"].dtype == np.int8 and np.all(f["scales"] == np.float32(1.0 / 7.0))
+    m.close()
+
+
 def test_prune_and_calibrate_argument_errors():
     w = np.ones(10, dtype=np.float16)
     for bad in (-0.1, 1.5, float("nan")):

@@ -105,3 +105,54 @@ def test_threshold_code_decides_like_oracle_for_every_fp16():
         code = spdp.threshold_code(t)
         lib_act = (mag > code) & (mag <= 0x7C00)
         assert np.array_equal(lib_act, oracle.active_mask(x, t)[0]), t
+
+
+# ---------------------------------------------------------------------------
+# Low-bit Values: round-to-nearest codes, one byte each, one scale per row
+
+def _same_rtn(m, w, tile, bits):
+    f = m.format()
+    codes, scales, pattern = oracle.rtn_quantize(w, bits)
+    ref = oracle.encode_codes(codes, pattern, *tile)
+    _same_format(f, ref)
+    assert f["value_bits"] == bits
+    assert f["scales"].dtype == np.float32 and np.array_equal(f["scales"].view(np.uint32), scales.view(np.uint32))
+    assert np.array_equal(f["codes"], ref.values.view(np.int8))
+
+
+@pytest.mark.parametrize("rows,cols,tm,tk,sw,bits,seed", [
+    (1, 1, 64, 1, 0.0, 4, 1), (64, 16, 64, 16, 0.5, 4, 2), (130, 37, 64, 4, 0.6, 2, 3),
+    (200, 33, 128, 8, 0.3, 8, 4), (256, 40, 256, 16, 0.7, 4, 5), (70, 9, 192, 2, 0.9, 3, 6),
+    (513, 1000, 256, 16, 0.5, 4, 9), (777, 300, 128, 1, 0.95, 5, 10), (257, 129, 256, 128, 1.0, 4, 11),
+])
+def test_rtn_encoder_bit_exact(rows, cols, tm, tk, sw, bits, seed):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, seed), sw)
+    _same_rtn(spdp.encode_rtn_host(w, (tm, tk), bits), w, (tm, tk), bits)
+
+
+def test_rtn_encoder_ties_zero_rows_and_subnormals():
+    """The hand-worked tie rows of the oracle pins, rows with nothing stored,
+    -0 entries and subnormal weights (scales far below the fp16 range)."""
+    w = synth.weights(256, 64, 78)
+    wb = w.view(np.uint16).copy()
+    wb[3] = 0                       # a row with nothing stored: scale 0
+    wb[5] = 0x8000                  # -0 everywhere: also nothing stored
+    wb[7, :] = 0
+    wb[7, :4] = [0x0001, 0x0002, 0x0003, 0x8001]   # subnormals only
+    row = np.array([0.875, -0.1875, 0.0, 0.3125, 0.0625, -0.0] * 10 + [0.0] * 4, dtype=np.float16)
+    wb[9] = row.view(np.uint16)     # ties at 1.5, 2.5 and 0.5 steps
+    w2 = wb.view(np.float16)
+    for bits in (4, 8):
+        m = spdp.encode_rtn_host(w2, (256, 16), bits)
+        _same_rtn(m, w2, (256, 16), bits)
+        f = m.format()
+        assert f["scales"][3] == 0 and f["scales"][5] == 0
+    m = spdp.encode_rtn_host(w2, (256, 16), 4)
+    codes, _ = oracle.decode_codes(oracle.encode_codes(*oracle.rtn_quantize(w2, 4)[::2], 256, 16))
+    assert codes[9, :6].tolist() == [7, -2, 0, 2, 0, 0]
+
+
+@pytest.mark.slow
+def test_rtn_encoder_bit_exact_full_size():
+    w = spdp.prune_magnitude(synth.weights(4096, 4096, 201), 0.5)
+    _same_rtn(spdp.encode_rtn_host(w, (256, 16), 4), w, (256, 16), 4)
