@@ -77,6 +77,9 @@ def parse():
     ap.add_argument("--mask", choices=("token", "batch"), default="token",
                     help="token: each token's own active columns (their union is read); batch: one "
                          "column set for the batch, chosen by the batch's mean |x| (batched DP)")
+    ap.add_argument("--rtn-bits", type=int, default=0, metavar="B",
+                    help="0: fp16 Values; 2..8: the pruned weights quantized to B-bit round-to-nearest "
+                         "codes (one byte each, one scale per row; the paper's quantization setup uses 4)")
     ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
                     help="graph: each step is one captured HIP graph of its calls (how a decode "
                          "loop runs them); stream: one host launch per call")
@@ -127,13 +130,18 @@ def call_bytes(fmt: dict, act: np.ndarray) -> tuple[int, float]:
     actp = np.zeros(C * tk, dtype=bool)
     actp[:K] = union
     nnz = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64)
-    padded = (nnz + 7) // 8 * 8
-    per_col = 4 + tm // 8 + 2 * padded                           # [R, C*tk]
+    if fmt.get("value_bits", 16) < 16:
+        # one byte per code, columns padded to 16 codes; one fp32 scale per row
+        per_col = 4 + tm // 8 + (nnz + 15) // 16 * 16             # [R, C*tk]
+        extra = 4 * M
+    else:
+        per_col = 4 + tm // 8 + 2 * ((nnz + 7) // 8 * 8)
+        extra = 0
     total = int((per_col * actp[None, :]).sum())
     touched = actp.reshape(C, tk).any(axis=1).sum()
     total += 4 * int(touched) * R
     b = act.shape[0]
-    total += 2 * b * K + 2 * b * M
+    total += 2 * b * K + 2 * b * M + extra
     return total, float(union.mean())
 
 
@@ -184,8 +192,10 @@ def read_traffic(workload: str, group: str):
 
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(points, mask="token", budget_s=20.0):
-    """Time the CPU oracle on a bounded sample of the same calls."""
+def cpu_baseline(points, mask="token", budget_s=20.0, rtn_bits=0):
+    """Time the CPU oracle on a bounded sample of the same calls (with low-bit
+    Values: the oracle's product with the dequantized weights, the
+    quantization itself done before the timing, as the encoding is)."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
@@ -198,11 +208,16 @@ def cpu_baseline(points, mask="token", budget_s=20.0):
     t_total, b_total = 0.0, 0
     t_start = time.perf_counter()
     for pt in points:
-        oracle.spmspv(pt["w"], pt["x"], pt["t"], mask)  # warm-up
+        if rtn_bits:
+            codes, scales, _ = oracle.rtn_quantize(pt["w"], rtn_bits)
+            product = lambda: oracle.spmspv_rtn(codes, scales, pt["x"], pt["t"], mask)  # noqa: E731
+        else:
+            product = lambda: oracle.spmspv(pt["w"], pt["x"], pt["t"], mask)  # noqa: E731
+        product()  # warm-up
         reps = []
         for _ in range(3):
             t0 = time.perf_counter()
-            oracle.spmspv(pt["w"], pt["x"], pt["t"], mask)
+            product()
             reps.append(time.perf_counter() - t0)
         t_total += float(np.median(reps))
         b_total += pt["bytes"]
@@ -221,7 +236,8 @@ def cpu_baseline(points, mask="token", budget_s=20.0):
     return {
         "value": b_total / t_total / 1e9, "unit": "GB/s", "cores": int(cores), "kind": "oracle",
         "sample": f"{len(sample)} of the step's calls ({', '.join(sample[:4])}{', ...' if len(sample) > 4 else ''}), "
-                  f"median of 3 after 1 warm-up, float64 NumPy masked product; cpu={cpu}; blas={blas}",
+                  f"median of 3 after 1 warm-up, float64 NumPy masked product"
+                  f"{' with the dequantized weights' if rtn_bits else ''}; cpu={cpu}; blas={blas}",
         "us_per_call": t_total / len(sample) * 1e6,
     }
 
@@ -288,11 +304,15 @@ def main():
                                "w": pruned[(sw, proj.name)],
                                "label": f"{proj.name}@sw{sw:g}/p{p:g}"})
     t_enc = time.perf_counter()
-    copy0 = [spdp.encode(pt["w"], tile) for pt in points]
+    if args.rtn_bits:
+        enc = lambda w: spdp.encode_rtn(w, tile, args.rtn_bits)  # noqa: E731
+    else:
+        enc = lambda w: spdp.encode(w, tile)  # noqa: E731
+    copy0 = [enc(pt["w"]) for pt in points]
     enc_s = (time.perf_counter() - t_enc) / len(points)
-    dev_bytes = sum(len(m.format()["values"]) * 2 for m in copy0)
+    dev_bytes = sum(len(m.format()["values"]) * (1 if args.rtn_bits else 2) for m in copy0)
     n_copies = max(2, int(np.ceil(args.rotation_mb * 1e6 / max(dev_bytes, 1))) + 1)
-    copies = [copy0] + [[spdp.encode(pt["w"], tile) for pt in points] for _ in range(n_copies - 1)]
+    copies = [copy0] + [[enc(pt["w"]) for pt in points] for _ in range(n_copies - 1)]
     for pt, m in zip(points, copy0):
         f = m.format()
         act = (batch_activity(pt["x"], pt["t"]) if args.mask == "batch"
@@ -566,9 +586,10 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(points, args.mask)
+        cpu = cpu_baseline(points, args.mask, rtn_bits=args.rtn_bits)
 
-    traffic = read_traffic(args.workload, args.group)
+    # the committed counter summaries are of fp16 Values
+    traffic = None if args.rtn_bits else read_traffic(args.workload, args.group)
     n_launch = len(step_units)
     us_per_call = ms_per_step * 1e3 / len(points)
     kernel_us = kern_ms * 1e3 / n_launch
@@ -593,6 +614,8 @@ def main():
             "batch": batch, "tile": list(tile), "calls_per_step": len(points),
             "launches_per_step": n_launch, "grouping": args.group,
             "rotation_copies": n_copies, "accumulate": "f32",
+            "values": (f"rtn{args.rtn_bits}: {args.rtn_bits}-bit round-to-nearest codes, one byte each, one "
+                       "fp32 scale per row" if args.rtn_bits else "fp16"),
             "mask": args.mask,
             "threshold": ({"rule": "offline calibration", "calibration_tokens": args.calibration,
                            "how": "p-quantile of |x| over separately drawn tokens of each layer input"}

@@ -39,6 +39,11 @@
 //      the next call. No
 //      counter, no fence, no host-side state: a partial is usable as soon as
 //      its own store has landed, and a captured graph replays correctly.
+// With low-bit Values (spdp_encode_rtn, Sec. 5.1's quantization setup) the
+// same kernel reads one-byte codes: step 2 streams 16 codes per 16-byte
+// chunk, step 3 addresses bytes and turns each code into an fp16 integer
+// (exact), steps 4-5 are unchanged, and the row's scale multiplies the
+// gathered sum once before the fp16 rounding.
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>

@@ -24,6 +24,20 @@ def test_call_bytes_matches_oracle(rows, cols, tile, sw, p, batch):
     assert frac == pytest.approx(oracle.active_mask(x, t).any(axis=0).mean())
 
 
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch,bits", [
+    (1024, 1024, (64, 64), 0.5, 0.5, 1, 4), (700, 900, (256, 16), 0.6, 0.25, 1, 4),
+    (333, 517, (192, 4), 0.7, 0.5, 8, 8),
+])
+def test_call_bytes_of_codes_matches_oracle(rows, cols, tile, sw, p, batch, bits):
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows + cols), sw)
+    x = synth.laplace_activations(batch, cols, 5)
+    t = float(oracle.threshold_for(x, p))
+    f = spdp.encode_rtn_host(w, tile, bits).format()
+    got, _ = bench.call_bytes(f, bench.token_activity(x, spdp.threshold_code(t)))
+    codes, _, pattern = oracle.rtn_quantize(w, bits)
+    assert got == oracle.algorithmic_bytes_codes(oracle.encode_codes(codes, pattern, *tile), x, t)
+
+
 @pytest.mark.parametrize("p,batch,draw_t", [(0.5, 1, 0), (0.25, 4, 1), (0.7, 2, 1), (0.0, 1, 0)])
 def test_dropped_fraction_matches_oracle(p, batch, draw_t):
     """Realized dynamic sparsity as the bench reports it, with the threshold
