@@ -177,3 +177,16 @@ def test_spmspv_many_argument_errors():
         spdp._mask_code("mean")
     a.close()
     b.close()
+
+
+def test_chain_host_side_errors():
+    """Chain: nothing to capture, replay before capture, a bad mask name."""
+    ch = spdp.Chain()
+    with pytest.raises(RuntimeError):
+        ch.replay()
+    with pytest.raises(RuntimeError):
+        ch.capture()
+    m = spdp.encode_host(np.ones((64, 16), dtype=np.float16), (64, 16))
+    with pytest.raises(ValueError):
+        ch.add(m, None, 0.5, None, mask="rows")
+    m.close()
