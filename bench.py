@@ -245,7 +245,7 @@ def cpu_baseline(points, mask="token", budget_s=20.0, rtn_bits=0):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
+        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
     import torch
 

@@ -30,7 +30,7 @@ extern "C" {
 typedef enum spdp_status {
   SPDP_OK = 0,
   SPDP_ERR_INVALID_ARG = -1, /* a null pointer, a bad size, NaN, ... */
-  SPDP_ERR_UNSUPPORTED = -2, /* valid input this build does not handle */
+  SPDP_ERR_UNSUPPORTED = -2, /* valid input the library does not handle */
   SPDP_ERR_OOM = -3,         /* host or device allocation failed */
   SPDP_ERR_HIP = -4          /* a HIP runtime call failed (text in spdp_last_error) */
 } spdp_status;

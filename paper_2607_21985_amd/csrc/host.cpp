@@ -84,7 +84,7 @@ int check_shape(const uint16_t* W, int64_t rows, int64_t cols, int32_t tile_m, i
   if (rows < 1 || cols < 1) return fail(SPDP_ERR_INVALID_ARG, "rows and cols must be >= 1");
   if (!valid_tile(tile_m, tile_k)) {
     if (tile_m > 256 && tile_m <= 1024 && tile_m % 64 == 0)
-      return fail(SPDP_ERR_UNSUPPORTED, "tile_m above 256 is not supported by this build");
+      return fail(SPDP_ERR_UNSUPPORTED, "tile_m above 256 is not supported by this library");
     return fail(SPDP_ERR_INVALID_ARG,
                 "tile_m must be a multiple of 64 in [64, 256] and tile_k a power of two in [1, 256]");
   }
