@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   constexpr int kSlots = S::kSlots;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[S::kRingBytes];
   // the workgroup's active columns in activity order: {byte offset of the
-  // column's values, column index into ColInfo/bitmap << 6 | index of its
+  // column's values, the column's bitmap offset and the index of its
   // last 16-byte chunk}; padded to a whole batch with entries that load
   // nothing of use
   __shared__ uint2 ent_s[kMaxWgCols + kBatch];
@@ -409,10 +409,24 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // the all-zero column pad a batch: they read the
   // bitmap array's zeroed tail and the first 16 bytes of the values, and
   // decode to nothing
+  // An entry's second word: with tile_m a power of two (WPC 1, 2 or 4) the
+  // byte offset of the column's bitmap words, a multiple of WPC x 8, with
+  // the index of the column's last 16-byte chunk (< WPC x 8) in its low
+  // bits, so that both come out with one AND each; with 192-row tiles the
+  // column index << 6 and the chunk index.
+  constexpr bool kPow2 = (WPC & (WPC - 1)) == 0;
+  constexpr uint32_t kLow = kPow2 ? WPC * 8u - 1u : 63u;
+  auto ent_col = [&](uint32_t col, uint32_t chunk) __attribute__((always_inline)) {
+    return kPow2 ? col * (WPC * 8u) + chunk : (col << 6) | chunk;
+  };
+  auto ent_chunk = [&](uint32_t y) __attribute__((always_inline)) { return y & kLow; };
+  auto ent_bitmap = [&](uint32_t y) __attribute__((always_inline)) {
+    return kPow2 ? y & ~kLow : (y >> 6) * (WPC * 8u);
+  };
   auto put = [&](int c, int p) __attribute__((always_inline)) {
     // 16-byte chunks of the column's padded values (8 fp16 or 16 codes each)
     const uint32_t chunks = Q ? ((ci[c] & 0xFFFFu) + 15u) >> 4 : ((ci[c] & 0xFFFFu) + 7u) >> 3;
-    ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), (colx[c] << 6) | (chunks ? chunks - 1u : 0u));
+    ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), ent_col(colx[c], chunks ? chunks - 1u : 0u));
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
       const int mag = (int)(xb[c][b] & 0x7FFFu);
@@ -421,7 +435,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     }
   };
   auto put_zero = [&](int p) __attribute__((always_inline)) {
-    ent_s[p] = make_uint2(0u, zero_col << 6);
+    ent_s[p] = make_uint2(0u, ent_col(zero_col, 0u));
 #pragma unroll
     for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = 0;
   };
@@ -441,11 +455,11 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
 #pragma unroll
     for (int pr = 0; pr < kBatch / 2; ++pr) {
       const uint2 e = ent_s[e0 + 2 * pr + hsel];
-      dma16(values, e.x + (min((uint32_t)q, e.y & 63u) << 4), slot + pr * 2 * kSlotBytes);
+      dma16(values, e.x + (min((uint32_t)q, ent_chunk(e.y)) << 4), slot + pr * 2 * kSlotBytes);
     }
     if (lane < 2 * WPC * kBatch) {
       const uint2 e = ent_s[e0 + lane / (2 * WPC)];
-      dma4(bitmap, (e.y >> 6) * (WPC * 8u) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
+      dma4(bitmap, ent_bitmap(e.y) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
     }
   };
 
@@ -617,7 +631,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   uint64_t m[kQuad][WPC];
   auto masks_of = [&](int i) __attribute__((always_inline)) {
     // byte offsets of the batch's bitmaps: lane u < kBatch holds column u's
-    const uint32_t bo_v = (ent_s[entry0(i) + (lane & (kBatch - 1))].y >> 6) * (WPC * 8u);
+    const uint32_t bo_v = ent_bitmap(ent_s[entry0(i) + (lane & (kBatch - 1))].y);
     load_masks(m, bo_v, 0);
   };
   if (EARLY && n_mine > 0) masks_of(0);
