@@ -694,45 +694,55 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // not depend on timing. The workgroups of lower segments of the stripe were
   // dispatched before these, so the wait ends; a bound on the rounds still
   // makes every wave exit (the rows then read NaN).
-  const int n_red = min(n_seg, WPC);
+  // Reducers take units (64-row block w, token slice): a slice is every
+  // token up to 8 tokens, and 8 tokens beyond; unit u = w + WPC x slice goes
+  // to reducer u mod n_red. Splitting the tokens keeps several segments of
+  // a slice in flight per round at large batches (one segment per round for
+  // 16 or 32 tokens would cost a device-scope round trip per segment) and
+  // spreads the gather over more workgroups; the sum per token is the same.
+  constexpr int kTok = NB > 8 ? 8 : NB;
+  const int n_units = WPC * ((nb + kTok - 1) / kTok);
+  const int n_red = min(n_seg, n_units);
   const int jr = seg - (n_seg - n_red);
   if (jr < 0) return;
-  // A round requests kJ of the wave's segments for every token at once
-  // (about kGather partials in flight per lane).
-  constexpr int kGather = 12;
-  constexpr int kJ = NB >= kGather ? 1 : kGather / NB;
+  // A round requests kJ of the wave's segments for every token of the slice
+  // at once (about kGather partials in flight per lane).
+  constexpr int kGather = NB > 8 ? NB : 12;
+  constexpr int kJ = kGather / kTok >= 1 ? kGather / kTok : 1;
   constexpr int kMaxRounds = 1 << 22;
   const int rows = ka->rows;
-  for (int w = jr; w < WPC; w += n_red) {
+  for (int u = jr; u < n_units; u += n_red) {
+    const int w = u % WPC;
+    const int b0 = (u / WPC) * kTok;
     const int m = r * ka->tile_m + 64 * w + lane;
     const bool live = m < rows;
     const unsigned long long* src = ka->partials + (live ? m : 0);
     // Q form: the row's scale, requested ahead of the partials
     const float row_scale = Q ? (live ? ka->scales[m] : 0.0f) : 1.0f;
-    float sums[NB];
+    float sums[kTok];
 #pragma unroll
-    for (int b = 0; b < NB; ++b) sums[b] = 0.0f;
+    for (int b = 0; b < kTok; ++b) sums[b] = 0.0f;
     if (live) {
       bool lost = false;
       auto part = [&](int sg, int b) {
-        return __hip_atomic_load(src + ((size_t)sg * nb + b) * mpad, __ATOMIC_RELAXED,
+        return __hip_atomic_load(src + ((size_t)sg * nb + b0 + b) * mpad, __ATOMIC_RELAXED,
                                  __HIP_MEMORY_SCOPE_AGENT);
       };
       // this wave's segments: wave, wave + 4, ...
       for (int sg0 = wave; sg0 < n_seg; sg0 += kWaves * kJ) {
-        unsigned long long v[kJ][NB];
+        unsigned long long v[kJ][kTok];
 #pragma unroll
         for (int jj = 0; jj < kJ; ++jj)
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
-            if (b < nb) v[jj][b] = part(min(sg0 + kWaves * jj, n_seg - 1), b);
+          for (int b = 0; b < kTok; ++b)
+            if (b0 + b < nb) v[jj][b] = part(min(sg0 + kWaves * jj, n_seg - 1), b);
         for (int round = 0;; ++round) {
           bool ready = true;
 #pragma unroll
           for (int jj = 0; jj < kJ; ++jj)
 #pragma unroll
-            for (int b = 0; b < NB; ++b)
-              if (b < nb && sg0 + kWaves * jj < n_seg && (uint32_t)(v[jj][b] >> 32) != phase) {
+            for (int b = 0; b < kTok; ++b)
+              if (b0 + b < nb && sg0 + kWaves * jj < n_seg && (uint32_t)(v[jj][b] >> 32) != phase) {
                 ready = false;
                 v[jj][b] = part(sg0 + kWaves * jj, b);
               }
@@ -745,23 +755,23 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
 #pragma unroll
         for (int jj = 0; jj < kJ; ++jj)
 #pragma unroll
-          for (int b = 0; b < NB; ++b)
-            if (b < nb && sg0 + kWaves * jj < n_seg) sums[b] += __uint_as_float((uint32_t)v[jj][b]);
+          for (int b = 0; b < kTok; ++b)
+            if (b0 + b < nb && sg0 + kWaves * jj < n_seg) sums[b] += __uint_as_float((uint32_t)v[jj][b]);
       }
       if (lost)
 #pragma unroll
-        for (int b = 0; b < NB; ++b) sums[b] = __builtin_nanf("");
+        for (int b = 0; b < kTok; ++b) sums[b] = __builtin_nanf("");
     }
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      if (b < nb) {  // uniform over the workgroup
+    for (int b = 0; b < kTok; ++b) {
+      if (b0 + b < nb) {  // uniform over the workgroup
         __syncthreads();
         red[wave * 64 + lane] = sums[b];
         __syncthreads();
         if (wave == 0 && live) {
           float t = ((red[lane] + red[64 + lane]) + red[128 + lane]) + red[192 + lane];
           if constexpr (Q) t *= row_scale;  // y = s * sum q x, rounded once to fp16
-          ka->y[(size_t)b * rows + m] = __half_as_ushort(__float2half_rn(t));
+          ka->y[(size_t)(b0 + b) * rows + m] = __half_as_ushort(__float2half_rn(t));
         }
       }
     }

@@ -146,6 +146,11 @@ EARLY = [
     (300, 2048, (64, 1), 0.5, 0.5, 8, None),
     (512, 1111, (256, 16), 0.6, 0.4, 32, None),
     (1024, 8192, (256, 16), 0.5, 0.0, 1, 16),
+    # many tokens: the gather's (row block, 8-token slice) units outnumber
+    # the reducers, which then take several each
+    (512, 1111, (256, 16), 0.6, 0.4, 32, 1),
+    (300, 2048, (64, 1), 0.5, 0.5, 17, 3),
+    (700, 900, (128, 8), 0.5, 0.3, 16, 5),
 ]
 
 
