@@ -700,8 +700,9 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // a slice in flight per round at large batches (one segment per round for
   // 16 or 32 tokens would cost a device-scope round trip per segment) and
   // spreads the gather over more workgroups; the sum per token is the same.
-  constexpr int kTok = NB > 8 ? 8 : NB;
-  const int n_units = WPC * ((nb + kTok - 1) / kTok);
+  constexpr bool kSliced = NB > 8;
+  constexpr int kTok = kSliced ? 8 : NB;
+  const int n_units = kSliced ? WPC * ((nb + kTok - 1) / kTok) : WPC;
   const int n_red = min(n_seg, n_units);
   const int jr = seg - (n_seg - n_red);
   if (jr < 0) return;
@@ -712,8 +713,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   constexpr int kMaxRounds = 1 << 22;
   const int rows = ka->rows;
   for (int u = jr; u < n_units; u += n_red) {
-    const int w = u % WPC;
-    const int b0 = (u / WPC) * kTok;
+    const int w = kSliced ? u % WPC : u;
+    const int b0 = kSliced ? (u / WPC) * kTok : 0;
     const int m = r * ka->tile_m + 64 * w + lane;
     const bool live = m < rows;
     const unsigned long long* src = ka->partials + (live ? m : 0);
