@@ -708,7 +708,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   if (jr < 0) return;
   // A round requests kJ of the wave's segments for every token of the slice
   // at once (about kGather partials in flight per lane).
-  constexpr int kGather = NB > 8 ? NB : 12;
+  constexpr int kGather = NB > 8 ? NB : NB == 8 ? 16 : 12;
   constexpr int kJ = kGather / kTok >= 1 ? kGather / kTok : 1;
   constexpr int kMaxRounds = 1 << 22;
   const int rows = ka->rows;
