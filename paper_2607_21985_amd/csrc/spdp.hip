@@ -707,8 +707,10 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const int jr = seg - (n_seg - n_red);
   if (jr < 0) return;
   // A round requests kJ of the wave's segments for every token of the slice
-  // at once (about kGather partials in flight per lane).
-  constexpr int kGather = NB > 8 ? NB : NB == 8 ? 16 : 12;
+  // at once (about kGather partials in flight per lane: 16 where the
+  // kernel's occupancy is bound by LDS and the registers are free, 12 at
+  // one token, where they are not).
+  constexpr int kGather = NB > 8 ? NB : NB >= 2 ? 16 : 12;
   constexpr int kJ = kGather / kTok >= 1 ? kGather / kTok : 1;
   constexpr int kMaxRounds = 1 << 22;
   const int rows = ka->rows;
