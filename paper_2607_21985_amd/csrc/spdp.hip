@@ -620,8 +620,9 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
   // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
   // requested after i) loads outstanding". In the early-first-batch form
-  // (small products, few waves per CU to hide latency with) and at two to
-  // eight tokens (measured: 0-2.5 % faster on every shape) the bitmap words
+  // (small products, few waves per CU to hide latency with) and with more
+  // than one token (measured: 0-2.5 % faster at 2-8 tokens, -2 to +1 % at
+  // 16 and 32) the bitmap words
   // of batch i + 1 are requested as soon as batch i no longer needs their
   // registers, so that their round trip overlaps the wait for batch i + 1's
   // values; with many waves per CU, requesting them after that wait is
@@ -635,7 +636,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     const uint32_t bo_v = ent_bitmap(ent_s[entry0(i) + (lane & (kBatch - 1))].y);
     load_masks(m, bo_v, 0);
   };
-  constexpr bool kAhead = EARLY || (NB >= 2 && NB <= 8);
+  constexpr bool kAhead = EARLY || NB > 1;
   if (kAhead && n_mine > 0) masks_of(0);
   for (int i = 0; i < n_mine; ++i) {
     const int later = min(n_mine - 1 - i, kSlots - 1);
