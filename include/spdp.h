@@ -101,10 +101,14 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
  * Asynchronous: the call validates, enqueues one kernel and returns; X and Y
  * must stay valid until the stream passes the work. The handle's workspace
  * is reused by every call, so one handle must not run on two streams at
- * once. The first call with a larger batch than before grows the workspace
- * (a device allocation); spdp_reserve does that ahead of time, after which
- * calls allocate nothing and may be captured into a HIP graph (replays are
- * exact: the call keeps no host-side state).
+ * once. The first call with a larger batch than before grows the workspace:
+ * a device allocation, cleared on `stream` ahead of the kernel, with no wait
+ * for the device (the old workspace is kept until spdp_free, since work in
+ * flight or a captured graph may still use it). Growth is refused with
+ * SPDP_ERR_INVALID_ARG while `stream` is capturing. spdp_reserve sizes the
+ * workspace ahead of time, after which calls allocate nothing and may be
+ * captured into a HIP graph (replays are exact: the call keeps no host-side
+ * state).
  *
  * Deterministic: the fp32 summation order depends only on the matrix, the
  * batch and which columns are active (and on the tuning variables
@@ -213,7 +217,7 @@ int spdp_format(spdp_handle_t h, spdp_format_t* out);
 /*
  * spdp_encode_rtn -- low-bit Values (Sec. 5.1's quantization setup: the
  * weights are quantized after pruning, and dynamic pruning runs on top at
- * inference; Sec. 7: Values are stored apart from the sparsity metadata).
+ * inference; Sec. 6: Values are stored apart from the sparsity metadata).
  * W (already pruned, as for spdp_encode) is quantized to `bits`-bit
  * round-to-nearest codes, symmetric, one fp32 scale per row:
  *     s[m] = fp32(max over the row's nonzeros of |W[m,k]|) / (2^(bits-1) - 1)

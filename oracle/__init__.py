@@ -39,7 +39,7 @@ Functions and the passages of the paper they follow:
   -- low-bit Values: round-to-nearest weight-only quantization of the pruned
   matrix (Sec. 5.1's quantization setup: pruning first, then quantization,
   then dynamic pruning at inference), the same format with one byte per
-  code (Sec. 7: Values are stored apart from the sparsity metadata), and
+  code (Sec. 6: Values are stored apart from the sparsity metadata), and
   the masked product with the dequantized weights.
 
 Readings where the paper is silent (bit order, array order, padding value,
@@ -545,7 +545,7 @@ def useful_flops(w_sp: np.ndarray, x: np.ndarray, t: float, mask: str = "token")
 
 
 # --------------------------------------------------------------------------
-# Low-bit Values (Sec. 5.1 quantization setup; Sec. 7 on low-precision Values)
+# Low-bit Values (Sec. 5.1 quantization setup; Sec. 6 on low-precision Values)
 # --------------------------------------------------------------------------
 
 def rtn_quantize(w_sp: np.ndarray, bits: int = 4):

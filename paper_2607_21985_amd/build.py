@@ -26,8 +26,12 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libspdp)")
 
 
+PEAK_LIB = os.path.join(HERE, "libspdp_peak.so")
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source of the library; always rebuilds. Returns the .so path."""
+    """Compile every source of the library (and the benchmark's read-roof
+    kernel, libspdp_peak.so); always rebuilds. Returns the library's path."""
     cc = hipcc()
     objdir = os.path.join(HERE, "_build")
     os.makedirs(objdir, exist_ok=True)
@@ -57,6 +61,13 @@ def build(verbose: bool = False) -> str:
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(link)}\n{res.stdout}{res.stderr}")
     os.replace(tmp, LIB)
+    # the benchmark's streaming-read roof: its own small library
+    tmp = PEAK_LIB + ".tmp"
+    peak = [cc] + common + device + ["-shared", "-o", tmp, os.path.join(CSRC, "peak.hip")]
+    res = subprocess.run(peak, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"compile failed: {' '.join(peak)}\n{res.stdout}{res.stderr}")
+    os.replace(tmp, PEAK_LIB)
     return LIB
 
 

@@ -32,11 +32,14 @@ struct spdp_matrix {
   void* d_scales = nullptr;
 
   // Split-K workspace: {fp32 partial sum, phase} pairs
-  // [segments - 1][batch][n_stripes*tile_m], and each row stripe's phase
+  // [segments][batch][n_stripes*tile_m], and each row stripe's phase
   // (advanced on the device by every call).
   unsigned long long* d_partials = nullptr;
   size_t partial_floats = 0;  // capacity in pairs
   uint32_t* d_phase = nullptr;
+  // Workspaces replaced by a larger one: a HIP graph captured earlier still
+  // names them, so they live until the handle is freed.
+  std::vector<void*> retired;
 };
 
 namespace spdp {

@@ -837,29 +837,39 @@ void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
   *segments = (int)segs(wc);
 }
 
-// The workspace holds {fp32, phase} pairs for all segments; it
-// starts zeroed and phases are never 0, so nothing in it matches a call
-// before that call has written it.
-int ensure_workspace(spdp_matrix* m, int batch, int segments) {
+// The workspace holds {fp32, phase} pairs for all segments; it starts zeroed
+// and phases are never 0, so nothing in it matches a call before that call
+// has written it. Growing it never waits for the device and never frees: the
+// old workspace may still be read by work in flight or named by a captured
+// graph, so it is kept until spdp_free. On the call path (stream given) the
+// new one is cleared on the call's stream, ahead of the kernel; inside a
+// stream capture no allocation is made at all (the call is refused: size
+// the workspace with spdp_reserve before capturing).
+int ensure_workspace(spdp_matrix* m, int batch, int segments, bool on_call, hipStream_t stream) {
   const size_t need = (size_t)segments * batch * m->n_stripes * m->tile_m;
   if (need <= m->partial_floats) return SPDP_OK;
-  if (m->d_partials) {
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
-    (void)hipFree(m->d_partials);
-    m->d_partials = nullptr;
-    m->partial_floats = 0;
+  if (on_call) {
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(stream, &cs);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+    if (cs != hipStreamCaptureStatusNone)
+      return fail(SPDP_ERR_INVALID_ARG,
+                  "the split-K workspace is too small for this batch and the stream is capturing; "
+                  "call spdp_reserve(h, batch) before the capture");
   }
-  hipError_t e = hipMalloc(&m->d_partials, need * sizeof(unsigned long long));
-  if (e != hipSuccess) {
-    m->d_partials = nullptr;
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, need * sizeof(unsigned long long));
+  if (e != hipSuccess)
     return e == hipErrorOutOfMemory ? fail(SPDP_ERR_OOM, "hipMalloc of the split-K workspace failed")
                                     : hip_fail(e, "hipMalloc");
+  e = on_call ? hipMemsetAsync(p, 0, need * sizeof(unsigned long long), stream)
+              : hipMemset(p, 0, need * sizeof(unsigned long long));
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_fail(e, "hipMemset");
   }
-  e = hipMemset(m->d_partials, 0, need * sizeof(unsigned long long));
-  if (e != hipSuccess) return hip_fail(e, "hipMemset");
-  e = hipDeviceSynchronize();
-  if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+  if (m->d_partials) m->retired.push_back(m->d_partials);
+  m->d_partials = static_cast<unsigned long long*>(p);
   m->partial_floats = need;
   return SPDP_OK;
 }
@@ -873,6 +883,8 @@ void release_device(spdp_matrix* m) {
   void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_scales, m->d_partials, m->d_phase};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
+  for (void* p : m->retired) (void)hipFree(p);
+  m->retired.clear();
   m->d_tile_offset = m->d_col_info = m->d_bitmap = m->d_values = m->d_scales = nullptr;
   m->d_partials = nullptr;
   m->d_phase = nullptr;
@@ -958,7 +970,7 @@ int early_first(int batch, int64_t workgroups) {
 // Validates one product of a call and fills its kernel arguments (sizing
 // the handle's workspace for the batch if needed).
 int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, int32_t mask, uint16_t* Y, int dev,
-            MatArgs* out, int64_t* n_wg) {
+            hipStream_t stream, MatArgs* out, int64_t* n_wg) {
   if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
   if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
   if (!X || !Y) return fail(SPDP_ERR_INVALID_ARG, "X or Y is NULL");
@@ -978,7 +990,7 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
 
   int segments = 1, wave_cols = 16;
   choose_split(h, &segments, &wave_cols);
-  st = ensure_workspace(h, batch, segments);
+  st = ensure_workspace(h, batch, segments, true, stream);
   if (st != SPDP_OK) return st;
 
   MatArgs& a = *out;
@@ -1056,7 +1068,7 @@ int finish_device(spdp_matrix* m, spdp_handle_t* out) {
   if (st == SPDP_OK) {
     int segments = 1, wave_cols = 16;
     choose_split(m, &segments, &wave_cols);
-    st = ensure_workspace(m, 1, segments);
+    st = ensure_workspace(m, 1, segments, false, nullptr);
   }
   if (st != SPDP_OK) {
     release_device(m);
@@ -1109,7 +1121,7 @@ int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
     return fail(SPDP_ERR_INVALID_ARG, "max_batch must lie in [1, 32]");
   int segments = 1, wave_cols = 16;
   choose_split(h, &segments, &wave_cols);
-  return ensure_workspace(h, max_batch, segments);
+  return ensure_workspace(h, max_batch, segments, false, nullptr);
 }
 
 int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
@@ -1148,7 +1160,8 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uin
   const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
   for (int i = 0; i < count; ++i) {
     int64_t n_wg = 0;
-    const int st = prepare(handles[i], X[i], batch, thresholds[i], mask, Y[i], dev, &la.m[i], &n_wg);
+    const int st = prepare(handles[i], X[i], batch, thresholds[i], mask, Y[i], dev, static_cast<hipStream_t>(stream),
+                           &la.m[i], &n_wg);
     if (st != SPDP_OK) return st;
     if (handles[i]->tile_m != handles[0]->tile_m)
       return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");

@@ -287,6 +287,55 @@ def test_graph_replay_matches_eager():
         m.close()
 
 
+def test_workspace_growth_keeps_captured_graphs_valid():
+    """A call with a larger batch grows the handle's workspace without waiting
+    for the device; the old workspace stays allocated, so a graph captured
+    before the growth still replays correctly. Growth while the stream is
+    capturing is refused and launches nothing."""
+    dev = _dev()
+    w, x1, t = _case(1000, 3000, (256, 16), 0.5, 0.5, 1, 91, 92)
+    m = spdp.encode(w, (256, 16))
+    X1 = _to_dev(x1)
+    Y1 = torch.zeros((1, m.rows), dtype=torch.float16, device=dev)
+    m.spmspv_into(X1, t, Y1)
+    torch.cuda.synchronize()
+    ref1 = Y1.clone()
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        m.spmspv_into(X1, t, Y1)
+    torch.cuda.synchronize()
+    # grow: 8 tokens (a new workspace, the captured one retired but alive)
+    x8 = synth.laplace_activations(8, 3000, 93)
+    t8 = float(oracle.threshold_for(x8, 0.5))
+    y8 = _run_gpu(m, x8, t8)
+    y64, s64, _ = oracle.spmspv(w, x8, t8)
+    _assert_close(y8, y64, s64, "after growth, 8 tokens")
+    for rep in range(3):
+        Y1.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y1, ref1), f"replay {rep} after the workspace grew"
+        _assert_close(_run_gpu(m, x1, t), *oracle.spmspv(w, x1, t)[:2], f"eager one token, rep {rep}")
+    # a batch beyond the workspace inside a capture: refused, nothing launched
+    x16 = synth.laplace_activations(16, 3000, 94)
+    X16 = _to_dev(x16)
+    Y16 = torch.zeros((16, m.rows), dtype=torch.float16, device=dev)
+    g2 = torch.cuda.CUDAGraph()
+    err = None
+    s.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.graph(g2, stream=s):
+        try:
+            m.spmspv_into(X16, 0.5, Y16)
+        except spdp.SpdpError as e:
+            err = e
+    torch.cuda.synchronize()
+    assert err is not None and err.status == -1 and "spdp_reserve" in str(err)
+    del g, g2
+    m.close()
+
+
 @pytest.mark.parametrize("splitk", ["1", "2", "3", "7", "64", "1000"])
 def test_split_k_settings(splitk, monkeypatch):
     monkeypatch.setenv("SPDP_SPLITK", splitk)
@@ -351,38 +400,47 @@ def test_argument_errors_on_device():
 
 
 # ---------------------------------------------------------------------------
-# Full-size workloads, same launch configuration as bench.py, sampled rows.
+# Full-size workloads, same launch configuration as bench.py, every row: the
+# oracle runs in row blocks. One shape per distinct projection of each
+# workload, at its highest (sw, p) point, at 50/0 (no dynamic sparsity), and
+# for the 70B layer also at 80/70; batch 1 and the workload's largest batch.
 
-def _check_sampled(w, x, t, tile, label, n_rows=192, seed=0):
+def _check_all_rows(m, w, x, t, label, block=2048):
     print(f"[gpu] {label}", flush=True)
-    m = spdp.encode(w, tile)
     y = _run_gpu(m, x, t)
-    m.close()
     assert np.all(np.isfinite(y)), label
-    rng = np.random.default_rng(seed)
-    rows = np.unique(np.concatenate([[0, w.shape[0] - 1], rng.choice(w.shape[0], n_rows, replace=False)]))
-    y64, s64 = oracle.spmspv_rows(w, x, t, rows)
-    _assert_close(y[:, rows], y64, s64, label)
+    for r0 in range(0, w.shape[0], block):
+        rows = np.arange(r0, min(w.shape[0], r0 + block))
+        y64, s64 = oracle.spmspv_rows(w, x, t, rows)
+        _assert_close(y[:, rows], y64, s64, f"{label} rows {rows[0]}..{rows[-1]}")
 
 
 FULL = []
 for name in ("llama7b-attn", "llama7b-mlp", "llama13b-layer", "llama70b-layer"):
     wl = synth.workload(name)
+    seen = set()
     for proj in wl["projections"]:
-        FULL.append((name, proj))
+        if (proj.rows, proj.cols, proj.x_kind) not in seen:
+            seen.add((proj.rows, proj.cols, proj.x_kind))
+            FULL.append((name, proj))
 
 
 @pytest.mark.parametrize("name,proj", FULL, ids=[f"{n}-{p.name}" for n, p in FULL])
-def test_full_size_sampled(name, proj):
+def test_full_size_all_rows(name, proj):
     wl = synth.workload(name)
-    sw = max(wl["weight_sparsity"])
-    p = max(wl["act_sparsity"])
-    batch = max(wl["batch"]) if name != "llama70b-layer" else 32
-    w = oracle.magnitude_prune(proj.weight(), sw)
-    for b in sorted({1, batch}):
-        x = proj.activations(b)
-        t = float(oracle.threshold_for(x, p))
-        _check_sampled(w, x, t, wl["tile"], f"{name}/{proj.name} {proj.rows}x{proj.cols} sw={sw} p={p} B={b}")
+    points = [(max(wl["weight_sparsity"]), max(wl["act_sparsity"])), (0.5, 0.0)]
+    if name == "llama70b-layer":
+        points.append((0.8, 0.7))
+    batch = max(wl["batch"])
+    w0 = proj.weight()
+    for sw, p in sorted(set(points)):
+        w = oracle.magnitude_prune(w0, sw)
+        m = spdp.encode(w, wl["tile"])
+        for b in sorted({1, batch}):
+            x = proj.activations(b)
+            t = float(oracle.threshold_for(x, p))
+            _check_all_rows(m, w, x, t, f"{name}/{proj.name} {proj.rows}x{proj.cols} sw={sw} p={p} B={b}")
+        m.close()
 
 
 # ---------------------------------------------------------------------------

@@ -140,19 +140,18 @@ def test_rtn_edge_cases():
 
 
 @pytest.mark.parametrize("rows,cols,sw,p", [(4096, 4096, 0.5, 0.5), (28672, 8192, 0.7, 0.5), (8192, 28672, 0.7, 0.5)])
-def test_rtn_full_size_sampled(rows, cols, sw, p):
+def test_rtn_full_size_all_rows(rows, cols, sw, p):
     w = oracle.magnitude_prune(synth.weights(rows, cols, rows // 7 + cols), sw)
     codes, scales, _ = oracle.rtn_quantize(w, 4)
     m = spdp.encode_rtn(w, (256, 16), 4)
-    rng = np.random.default_rng(rows + cols)
-    sel = np.unique(np.concatenate([[0, rows - 1], rng.choice(rows, 192, replace=False)]))
-    wq = oracle.rtn_dequantize(codes[sel], scales[sel])
     for b in (1, 8):
         x = synth.laplace_activations(b, cols, cols + b)
         t = float(oracle.threshold_for(x, p))
         print(f"[gpu] rtn full size {rows}x{cols} sw={sw} p={p} B={b}", flush=True)
         y = _run(m, x, t)
         assert np.all(np.isfinite(y))
-        xm = oracle.masked_activations(x, t).astype(np.float64)
-        _assert_close(y[:, sel], xm @ wq.T, np.abs(xm) @ np.abs(wq).T, f"{rows}x{cols} B={b}")
+        for r0 in range(0, rows, 2048):
+            r1 = min(rows, r0 + 2048)
+            y64, s64, _ = oracle.spmspv_rtn(codes[r0:r1], scales[r0:r1], x, t)
+            _assert_close(y[:, r0:r1], y64, s64, f"{rows}x{cols} B={b} rows {r0}..{r1 - 1}")
     m.close()
