@@ -120,6 +120,30 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
                 float threshold, uint16_t* Y, void* stream);
 
 /*
+ * spdp_spmspv_noalloc -- spdp_spmspv that allocates nothing, for callers that
+ * cannot call hipMalloc (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Same arguments, semantics, summation
+ * order and bits as spdp_spmspv; the split-K partials live in one static
+ * workspace of the library per device (SPDP_NOALLOC_PARTIAL_BYTES bytes,
+ * held until the process ends) instead of the handle's own.
+ *
+ *   A product needing more than SPDP_NOALLOC_PARTIAL_BYTES of partials
+ *   (8 bytes x K segments x batch x rows rounded up to tile_m) returns
+ *   SPDP_ERR_UNSUPPORTED and launches nothing: a 4096 x 4096 product fits
+ *   at every batch up to 32, the largest Llama-70B projections (28672 x
+ *   8192, 8192 x 28672) up to batch 9.
+ *   The workspace is shared by every call on one GPU and keeps the last
+ *   call's contents (tagged with a device-wide call epoch, so a call never
+ *   reads another's partials): calls that overlap on one GPU (two streams,
+ *   or two host threads) race and must not be issued.
+ *   The first call on a device looks up the workspace's address
+ *   (hipGetSymbolAddress); no call allocates, frees or waits for the device.
+ */
+#define SPDP_NOALLOC_PARTIAL_BYTES ((size_t)32 << 20)
+int spdp_spmspv_noalloc(spdp_handle_t h, const uint16_t* X, int32_t batch,
+                        float threshold, uint16_t* Y, void* stream);
+
+/*
  * spdp_spmspv_many -- several independent products in one launch:
  * Y[i] = W_i . mask(X[i]) with threshold thresholds[i], for i < count. This
  * is how a decoder issues the projections that read the same layer input

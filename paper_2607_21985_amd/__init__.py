@@ -47,7 +47,7 @@ EXPORTED_SYMBOLS = (
     "spdp_reserve", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
-    "spdp_encode_rtn", "spdp_encode_rtn_host",
+    "spdp_encode_rtn", "spdp_encode_rtn_host", "spdp_spmspv_noalloc",
 )
 
 SPDP_OK = 0
@@ -106,6 +106,7 @@ def lib() -> ctypes.CDLL:
     L.spdp_encode_rtn.argtypes = [u16p, i64, i64, i32, i32, i32, ctypes.POINTER(H)]
     L.spdp_encode_rtn_host.argtypes = [u16p, i64, i64, i32, i32, i32, ctypes.POINTER(H)]
     L.spdp_spmspv.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    L.spdp_spmspv_noalloc.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
     L.spdp_spmspv_many.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_void_p),
                                    ctypes.c_void_p]
@@ -123,7 +124,8 @@ def lib() -> ctypes.CDLL:
     L.spdp_strerror.restype = ctypes.c_char_p
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = ctypes.c_char_p
-    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_spmspv_many_mask",
+    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_noalloc", "spdp_spmspv_many",
+                 "spdp_spmspv_many_mask",
                  "spdp_reserve",
                  "spdp_format",
                  "spdp_prune_magnitude", "spdp_calibrate_threshold", "spdp_threshold_code"):
@@ -229,6 +231,25 @@ class Matrix:
             ts = (ctypes.c_float * 1)(float(threshold))
             _check(lib().spdp_spmspv_many_mask(hs, 1, xp, int(b), ts, _mask_code(mask), yp,
                                                ctypes.c_void_p(s.cuda_stream)))
+
+    def spmspv_noalloc_into(self, x, threshold: float, y, stream=None) -> None:
+        """``spmspv_into`` through ``spdp_spmspv_noalloc``: the split-K partials
+        go to the library's static workspace, so the call allocates nothing
+        (per-token mask; calls on one GPU must not overlap)."""
+        import torch
+        if x.dtype != torch.float16 or y.dtype != torch.float16:
+            raise TypeError("x and y must be torch.float16")
+        if x.dim() != 2 or x.shape[1] != self.cols or not x.is_contiguous():
+            raise ValueError(f"x must be a contiguous [batch, {self.cols}] tensor")
+        b = x.shape[0]
+        if tuple(y.shape) != (b, self.rows) or not y.is_contiguous():
+            raise ValueError(f"y must be a contiguous [{b}, {self.rows}] tensor")
+        if not (x.is_cuda and y.is_cuda):
+            raise ValueError("x and y must be device tensors")
+        s = stream if stream is not None else torch.cuda.current_stream(x.device)
+        _check(lib().spdp_spmspv_noalloc(self._h, ctypes.c_void_p(x.data_ptr()), int(b),
+                                         ctypes.c_float(threshold), ctypes.c_void_p(y.data_ptr()),
+                                         ctypes.c_void_p(s.cuda_stream)))
 
     def __call__(self, x, threshold: float, stream=None, mask: str = "token"):
         import torch

@@ -51,7 +51,9 @@
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
+#include <string>
 
 #include "internal.h"
 
@@ -89,7 +91,16 @@ struct MatArgs {
   uint16_t* y;
   // [segments][batch][n_stripes * tile_m]: {fp32 bits, phase} pairs
   unsigned long long* partials;
-  uint32_t* phase;     // [n_stripes], never 0 (the workspace starts zeroed)
+  // the tag of this call's partials, never 0 (the workspace starts zeroed).
+  // A handle's own workspace has one phase per stripe (phase_step 1,
+  // epoch_done NULL): the tag is phase[r], and the stripe's first reducer
+  // advances it. The library's static workspace, shared by every handle, has
+  // one device-wide epoch (phase_step 0): the tag is *phase + 1 (0 skipped);
+  // each stripe's first reducer counts itself in *epoch_done, and the last
+  // stripe's stores the tag as the new epoch and clears the count.
+  uint32_t* phase;
+  uint32_t* epoch_done;
+  int phase_step;
   int rows, cols;
   int tile_m, tk_log2, n_colblocks, n_stripes;
   int code;       // threshold code: active iff code < (x & 0x7fff) <= 0x7c00
@@ -377,7 +388,8 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // them does not wait for it (loads return in order), waited for after the
   // list is built; a scalar load would share the LDS wait counter, and the
   // compiler would wait for it at the first LDS barrier.
-  const uint32_t phase_lane = __hip_atomic_load(phase_p + r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+  const uint32_t phase_lane =
+      __hip_atomic_load(phase_p + r * A->phase_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
   // activity: the union of the tokens' sets, or the batch's shared set
   uint64_t actm[kChunks];
   int n_w = 0;
@@ -471,7 +483,11 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // the only vector load the compiler tracks and must be complete before the
   // first DMA: the compiler does not see those loads, so a wait it placed
   // for a load of its own among them would count them and drain the ring.
-  const uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
+  // the static workspace's epoch starts at 0 (static storage), the value
+  // its zeroed partials carry: a call's tag is the stored epoch plus one
+  // (0 skipped), and the call stores its tag back when it is done
+  uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
+  if (A->phase_step == 0) phase = phase + 1u == 0u ? 1u : phase + 1u;
   asm volatile("" ::"s"(phase));
   const bool has_first = EARLY && early_first && n_w > 0;
   const int e_first = kFirstList + kBatch * wave;
@@ -788,8 +804,20 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   // its barriers every workgroup of the stripe has published, and so has
   // read the phase; the next call starts after this kernel ends: advance the
   // tag (0 is skipped, the workspace's initial contents). The other reducers
-  // keep their own copies of the phase.
-  if (jr == 0 && threadIdx.x == 0) ka->phase[r] = phase + 1 == 0 ? 1u : phase + 1;
+  // keep their own copies of the phase. With the device-wide epoch the same
+  // holds for every stripe once each stripe's first reducer has counted
+  // itself: the last of them stores this call's tag as the epoch (the next
+  // call tags with one more) and clears the count for the next call.
+  if (jr == 0 && threadIdx.x == 0) {
+    uint32_t* const done = ka->epoch_done;
+    if (done == nullptr) {
+      ka->phase[r] = phase + 1u == 0u ? 1u : phase + 1u;
+    } else if (__hip_atomic_fetch_add(done, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+               (uint32_t)ka->n_stripes - 1u) {
+      __hip_atomic_store(done, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(ka->phase, phase, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
 }
 
 using spdp::fail;
@@ -967,10 +995,19 @@ int early_first(int batch, int64_t workgroups) {
   return workgroups <= kEarlyFirstMaxWorkgroups ? 1 : 0;
 }
 
-// Validates one product of a call and fills its kernel arguments (sizing
-// the handle's workspace for the batch if needed).
+// A split-K workspace that is not the handle's own: the library's static
+// one (partials and the device-wide epoch with its stripe count).
+struct SharedWorkspace {
+  unsigned long long* partials;
+  size_t capacity;  // pairs
+  uint32_t* epoch;
+  uint32_t* epoch_done;
+};
+
+// Validates one product of a call and fills its kernel arguments: with the
+// handle's workspace (sized for the batch if needed), or with `shared`.
 int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, int32_t mask, uint16_t* Y, int dev,
-            hipStream_t stream, MatArgs* out, int64_t* n_wg) {
+            hipStream_t stream, const SharedWorkspace* shared, MatArgs* out, int64_t* n_wg) {
   if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
   if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
   if (!X || !Y) return fail(SPDP_ERR_INVALID_ARG, "X or Y is NULL");
@@ -990,8 +1027,16 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
 
   int segments = 1, wave_cols = 16;
   choose_split(h, &segments, &wave_cols);
-  st = ensure_workspace(h, batch, segments, true, stream);
-  if (st != SPDP_OK) return st;
+  if (shared) {
+    const size_t need = (size_t)segments * batch * h->n_stripes * h->tile_m;
+    if (need > shared->capacity)
+      return fail(SPDP_ERR_UNSUPPORTED, "the product needs " + std::to_string(need * 8) +
+                                            " bytes of split-K partials; the static workspace holds " +
+                                            std::to_string(shared->capacity * 8));
+  } else {
+    st = ensure_workspace(h, batch, segments, true, stream);
+    if (st != SPDP_OK) return st;
+  }
 
   MatArgs& a = *out;
   a.tile_offset = static_cast<const uint32_t*>(h->d_tile_offset);
@@ -1001,8 +1046,10 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   a.scales = static_cast<const float*>(h->d_scales);
   a.x = X;
   a.y = Y;
-  a.partials = h->d_partials;
-  a.phase = h->d_phase;
+  a.partials = shared ? shared->partials : h->d_partials;
+  a.phase = shared ? shared->epoch : h->d_phase;
+  a.epoch_done = shared ? shared->epoch_done : nullptr;
+  a.phase_step = shared ? 0 : 1;
   a.rows = (int)h->rows;
   a.cols = (int)h->cols;
   a.tile_m = h->tile_m;
@@ -1079,6 +1126,112 @@ int finish_device(spdp_matrix* m, spdp_handle_t* out) {
   return SPDP_OK;
 }
 
+// The launch behind every spMspV entry point: validates all products, then
+// enqueues one kernel; `shared` selects the static workspace (one product).
+int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X, int32_t batch,
+                    const float* thresholds, int32_t mask, uint16_t* const* Y, void* stream,
+                    const SharedWorkspace* shared) {
+  if (!handles || !X || !Y || !thresholds) return fail(SPDP_ERR_INVALID_ARG, "an argument array is NULL");
+  if (mask != SPDP_MASK_TOKEN && mask != SPDP_MASK_BATCH)
+    return fail(SPDP_ERR_INVALID_ARG, "mask must be SPDP_MASK_TOKEN or SPDP_MASK_BATCH");
+  if (count < 1 || count > kMaxGroup) return fail(SPDP_ERR_INVALID_ARG, "count must lie in [1, 8]");
+  if (batch < 1 || batch > kMaxBatch) return fail(SPDP_ERR_INVALID_ARG, "batch must lie in [1, 32]");
+  for (int i = 0; i < count; ++i) {
+    if (!handles[i]) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
+    if (handles[i]->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
+  }
+  for (int i = 0; i < count; ++i) {
+    for (int j = 0; j < i; ++j) {
+      if (handles[i] == handles[j])
+        return fail(SPDP_ERR_INVALID_ARG, "a handle appears twice in one call (its workspace is shared)");
+      {
+        const size_t xi = (size_t)batch * handles[i]->cols * 2, yi = (size_t)batch * handles[i]->rows * 2;
+        const size_t xj = (size_t)batch * handles[j]->cols * 2, yj = (size_t)batch * handles[j]->rows * 2;
+        if (overlap(Y[i], yi, Y[j], yj) || overlap(Y[i], yi, X[j], xj) || overlap(Y[j], yj, X[i], xi))
+          return fail(SPDP_ERR_INVALID_ARG, "an output overlaps another product's input or output");
+      }
+    }
+  }
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  LaunchArgs la;
+  std::memset(&la, 0, sizeof(la));
+  la.batch = batch;
+  int64_t widest = 0;
+  bool early = false;
+  const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
+  for (int i = 0; i < count; ++i) {
+    int64_t n_wg = 0;
+    const int st = prepare(handles[i], X[i], batch, thresholds[i], mask, Y[i], dev, static_cast<hipStream_t>(stream),
+                           shared, &la.m[i], &n_wg);
+    if (st != SPDP_OK) return st;
+    if (handles[i]->tile_m != handles[0]->tile_m)
+      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
+    if ((handles[i]->value_bits < 16) != (handles[0]->value_bits < 16))
+      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must all hold fp16 values or all codes");
+    if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
+    widest = std::max(widest, n_wg);
+    early = early || la.m[i].early_first;
+  }
+
+  const int wpc = handles[0]->tile_m / 64;
+  const dim3 grid((unsigned)widest, (unsigned)count);
+  const bool q = handles[0]->value_bits < 16;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (batch <= 1)
+    e = launch<1>(la, wpc, early, bmask, q, grid, s);
+  else if (batch <= 2)
+    e = launch<2>(la, wpc, early, bmask, q, grid, s);
+  else if (batch <= 4)
+    e = launch<4>(la, wpc, early, bmask, q, grid, s);
+  else if (batch <= 8)
+    e = launch<8>(la, wpc, early, bmask, q, grid, s);
+  else if (batch <= 16)
+    e = launch<16>(la, wpc, early, bmask, q, grid, s);
+  else
+    e = launch<32>(la, wpc, early, bmask, q, grid, s);
+  if (e != hipSuccess) return hip_fail(e, "kernel launch");
+  return SPDP_OK;
+}
+
+// The static split-K workspace of spdp_spmspv_noalloc, for callers that
+// cannot allocate device memory. Bytes [0, 256) hold the device-wide epoch
+// (byte 0) and the count of stripes done with it (byte 128); the partials
+// follow. Static storage starts zeroed, so no partial carries a live tag
+// before a call writes it. Host code never uses the name `scratch` as an
+// address (on the host it stands for the symbol): the device address comes
+// from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchHeaderBytes = 256;
+constexpr size_t kScratchPartialBytes = SPDP_NOALLOC_PARTIAL_BYTES;
+static __device__ __align__(256) unsigned long long scratch[(kScratchHeaderBytes + kScratchPartialBytes) / 8];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch` (dev is current).
+int scratch_on(int dev, SharedWorkspace* ws) {
+  if (dev < 0 || dev >= kMaxDevices) return fail(SPDP_ERR_UNSUPPORTED, "device ordinal beyond 63");
+  void* p = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+      hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+      if (!p) return fail(SPDP_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+      g_scratch_ptr[dev] = p;
+    }
+    p = g_scratch_ptr[dev];
+  }
+  char* base = static_cast<char*>(p);
+  ws->epoch = reinterpret_cast<uint32_t*>(base);
+  ws->epoch_done = reinterpret_cast<uint32_t*>(base + 128);
+  ws->partials = reinterpret_cast<unsigned long long*>(base + kScratchHeaderBytes);
+  ws->capacity = kScratchPartialBytes / sizeof(unsigned long long);
+  return SPDP_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1128,68 +1281,7 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uin
                           int32_t batch, const float* thresholds, int32_t mask, uint16_t* const* Y,
                           void* stream) {
   spdp::clear_error();
-  if (!handles || !X || !Y || !thresholds) return fail(SPDP_ERR_INVALID_ARG, "an argument array is NULL");
-  if (mask != SPDP_MASK_TOKEN && mask != SPDP_MASK_BATCH)
-    return fail(SPDP_ERR_INVALID_ARG, "mask must be SPDP_MASK_TOKEN or SPDP_MASK_BATCH");
-  if (count < 1 || count > kMaxGroup) return fail(SPDP_ERR_INVALID_ARG, "count must lie in [1, 8]");
-  if (batch < 1 || batch > kMaxBatch) return fail(SPDP_ERR_INVALID_ARG, "batch must lie in [1, 32]");
-  for (int i = 0; i < count; ++i) {
-    if (!handles[i]) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
-    if (handles[i]->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
-  }
-  for (int i = 0; i < count; ++i) {
-    for (int j = 0; j < i; ++j) {
-      if (handles[i] == handles[j])
-        return fail(SPDP_ERR_INVALID_ARG, "a handle appears twice in one call (its workspace is shared)");
-      {
-        const size_t xi = (size_t)batch * handles[i]->cols * 2, yi = (size_t)batch * handles[i]->rows * 2;
-        const size_t xj = (size_t)batch * handles[j]->cols * 2, yj = (size_t)batch * handles[j]->rows * 2;
-        if (overlap(Y[i], yi, Y[j], yj) || overlap(Y[i], yi, X[j], xj) || overlap(Y[j], yj, X[i], xi))
-          return fail(SPDP_ERR_INVALID_ARG, "an output overlaps another product's input or output");
-      }
-    }
-  }
-  int dev = -1;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-  LaunchArgs la;
-  std::memset(&la, 0, sizeof(la));
-  la.batch = batch;
-  int64_t widest = 0;
-  bool early = false;
-  const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
-  for (int i = 0; i < count; ++i) {
-    int64_t n_wg = 0;
-    const int st = prepare(handles[i], X[i], batch, thresholds[i], mask, Y[i], dev, static_cast<hipStream_t>(stream),
-                           &la.m[i], &n_wg);
-    if (st != SPDP_OK) return st;
-    if (handles[i]->tile_m != handles[0]->tile_m)
-      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must share tile_m");
-    if ((handles[i]->value_bits < 16) != (handles[0]->value_bits < 16))
-      return fail(SPDP_ERR_INVALID_ARG, "the matrices of one call must all hold fp16 values or all codes");
-    if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
-    widest = std::max(widest, n_wg);
-    early = early || la.m[i].early_first;
-  }
-
-  const int wpc = handles[0]->tile_m / 64;
-  const dim3 grid((unsigned)widest, (unsigned)count);
-  const bool q = handles[0]->value_bits < 16;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (batch <= 1)
-    e = launch<1>(la, wpc, early, bmask, q, grid, s);
-  else if (batch <= 2)
-    e = launch<2>(la, wpc, early, bmask, q, grid, s);
-  else if (batch <= 4)
-    e = launch<4>(la, wpc, early, bmask, q, grid, s);
-  else if (batch <= 8)
-    e = launch<8>(la, wpc, early, bmask, q, grid, s);
-  else if (batch <= 16)
-    e = launch<16>(la, wpc, early, bmask, q, grid, s);
-  else
-    e = launch<32>(la, wpc, early, bmask, q, grid, s);
-  if (e != hipSuccess) return hip_fail(e, "kernel launch");
-  return SPDP_OK;
+  return launch_products(handles, count, X, batch, thresholds, mask, Y, stream, nullptr);
 }
 
 int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
@@ -1199,7 +1291,23 @@ int spdp_spmspv_many(const spdp_handle_t* handles, int32_t count, const uint16_t
 
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold,
                 uint16_t* Y, void* stream) {
-  return spdp_spmspv_many_mask(&h, 1, &X, batch, &threshold, SPDP_MASK_TOKEN, &Y, stream);
+  spdp::clear_error();
+  return launch_products(&h, 1, &X, batch, &threshold, SPDP_MASK_TOKEN, &Y, stream, nullptr);
+}
+
+int spdp_spmspv_noalloc(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold,
+                        uint16_t* Y, void* stream) {
+  spdp::clear_error();
+  if (!h) return fail(SPDP_ERR_INVALID_ARG, "handle is NULL");
+  if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev != h->device) return fail(SPDP_ERR_INVALID_ARG, "current device differs from the handle's");
+  SharedWorkspace ws;
+  const int st = scratch_on(dev, &ws);
+  if (st != SPDP_OK) return st;
+  return launch_products(&h, 1, &X, batch, &threshold, SPDP_MASK_TOKEN, &Y, stream, &ws);
 }
 
 void spdp_free(spdp_handle_t h) {
