@@ -1,6 +1,6 @@
 """Benchmark of the decode-time Tiled-CBC spMspV on one MI355X.
 
-Default workload: the four Llama-7B attention projections (q, k, v, o; each
+Headline workload: the four Llama-7B attention projections (q, k, v, o; each
 4096 x 4096 fp16) swept over weight sparsity {50, 60, 70}% and activation
 sparsity {0, 25, 50}% at batch 1. One "step" is the whole sweep: 36 spMspV
 calls (3 x 3 points x 4 projections), each on its own encoded copy; copies
@@ -21,14 +21,23 @@ Prints one JSON line. ``value`` is the whole step's algorithmic bytes over its
 time (GB/s). Algorithmic bytes per call = for every row stripe and every
 column active for some token: ColInfo (4 B) + bitmap (tile_m/8 B) + padded
 values (2 B x pad8(nnz)); + 4 B per touched GTile (TileOffset); + x and y.
+``secondary`` carries the other workloads, each timed the same way: the
+1024 x 1024 single layer; the Llama-7B MLP at batch 1/2/4/8; the Llama-13B
+decoder layer (seven calls chained) at batch 1/4/16; and a slice of the
+Llama-70B layer sweep.
+
+``--summarize-profiles DIR`` turns rocprofv3 outputs written under DIR by the
+commands it prints into the summaries under profiles/ (no GPU needed).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                       [--launch graph|stream]
+                       [--launch graph|stream] [--no-secondary]
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
+import ctypes
 import hashlib
 import json
 import os
@@ -47,9 +56,10 @@ HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
 # per cycle (a two-wide fp32 FMA, or v_dot2_f32_f16's two fp16 products added
 # into fp32) x 2.4 GHz
 VEC_PEAK_TFLOPS = 157.3
+LINE = 128  # bytes per L2 cache line (the granularity the traffic model uses)
 
 
-def parse():
+def parse(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
@@ -62,11 +72,14 @@ def parse():
                     help="minimum distinct encoded bytes between two uses of one copy")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the other workloads (single layer, 7B MLP, 13B layer, 70B slice)")
+    ap.add_argument("--secondary-steps", type=int, default=12)
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed steps only (for rocprofv3 runs)")
-    ap.add_argument("--calib-copy-mib", type=int, default=0,
-                    help="after the timed steps, run one device-to-device copy of this many MiB "
-                         "(a known-size reference for hardware byte counters)")
+    ap.add_argument("--calib-read-mib", type=int, default=0,
+                    help="after the timed steps, read this many MiB once with the streaming-read "
+                         "kernel (a known-size reference for the hardware byte counters)")
     ap.add_argument("--group", choices=("decoder", "none"), default="decoder",
                     help="decoder: products that read one input are one grouped launch; none: one launch each")
     ap.add_argument("--calibration", type=int, default=0, metavar="TOKENS",
@@ -83,7 +96,9 @@ def parse():
     ap.add_argument("--launch", choices=("graph", "stream"), default="graph",
                     help="graph: each step is one captured HIP graph of its calls (how a decode "
                          "loop runs them); stream: one host launch per call")
-    return ap.parse_args()
+    ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
+                    help="write profiles/*.txt from the rocprofv3 outputs under DIR and exit")
+    return ap.parse_args(argv)
 
 
 # ---------------------------------------------------------------------------
@@ -152,6 +167,51 @@ def call_flops(fmt: dict, act: np.ndarray) -> int:
     K = fmt["cols"]
     nnz_col = (fmt["col_info"].reshape(R, C * tk) & 0xFFFF).astype(np.int64).sum(axis=0)[:K]
     return int(2 * (act * nnz_col[None, :]).sum())
+
+
+def line_model(fmt: dict, act: np.ndarray) -> dict:
+    """Bytes per source of one call: the algorithmic bytes (what the method
+    must move) and the whole 128-byte lines that hold them (what an L2 fetch
+    of exactly those bytes brings). The kernel reads ColInfo and TileOffset
+    of every column (speculatively, with the activations), the bitmaps and
+    padded values of the active (stripe, column) pairs, x once and writes y;
+    split-K partials are measured, not modelled."""
+    R, C, tk, tm = fmt["n_stripes"], fmt["n_colblocks"], fmt["tile_k"], fmt["tile_m"]
+    K, M = fmt["cols"], fmt["rows"]
+    codes = fmt.get("value_bits", 16) < 16
+    vb, pad = (1, 16) if codes else (2, 8)
+    union = act.any(axis=0)
+    actp = np.zeros(C * tk, dtype=bool)
+    actp[:K] = union
+    ci = fmt["col_info"].reshape(R, C * tk).astype(np.int64)
+    nnz, off = ci & 0xFFFF, ci >> 16
+    to = fmt["tile_offset"][:-1].astype(np.int64).reshape(R, C)
+    start = (to[:, np.arange(C * tk) // tk] + off) * vb          # [R, C*tk] byte offsets
+    length = (nnz + pad - 1) // pad * pad * vb
+    sel = actp[None, :] & (length > 0)
+    s, e = start[sel], start[sel] + length[sel]                  # in layout order
+    first, last = s // LINE, (e - 1) // LINE
+    val_lines = int((last - first + 1).sum() - (first[1:] == last[:-1]).sum()) if s.size else 0
+    bm_bytes = tm // 8
+    pairs = np.broadcast_to(actp[None, :], (R, C * tk))            # (stripe, column) pairs read
+    n_pairs = int(pairs.sum())
+    g_col = (np.arange(R)[:, None] * (C * tk) + np.arange(C * tk)[None, :])[pairs]
+    bm_lines = int(np.unique(g_col * bm_bytes // LINE).size) if g_col.size else 0
+    touched = int(actp.reshape(C, tk).any(axis=1).sum()) * R
+    b = act.shape[0]
+
+    def lines(n):
+        return -(-n // LINE) * LINE
+
+    return {
+        "values": (int(length[sel].sum()), val_lines * LINE),
+        "bitmap": (n_pairs * bm_bytes, bm_lines * LINE),
+        "colinfo": (4 * n_pairs, lines(4 * R * C * tk)),
+        "tileoffset": (4 * touched, lines(4 * R * C)),
+        "x": (2 * b * K, lines(2 * b * K)),
+        "y": (2 * b * M, lines(2 * b * M)),
+        "scales": ((4 * M, lines(4 * M)) if codes else (0, 0)),
+    }
 
 
 def dropped_fraction(act: np.ndarray) -> float:
@@ -253,54 +313,89 @@ def cpu_baseline(points, mask="token", budget_s=20.0, rtn_bits=0):
     }
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(json.dumps({"error": "the benchmark runs on one GPU only; --gpus must be 1"}))
-        sys.exit(2)
-    import torch
+# ---------------------------------------------------------------------------
+# measurement engine
 
-    import paper_2607_21985_amd as spdp
-    import synth
+class Bench:
+    """Device, stream, timing and graph capture shared by every measurement."""
 
-    if not torch.cuda.is_available():
-        print(json.dumps({"error": "no ROCm GPU visible"}))
-        sys.exit(2)
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    wl = synth.workload(args.workload)
-    tile = wl["tile"]
-    batch = args.batch if args.batch is not None else wl["batch"][0]
-    if args.sw:
-        wl = dict(wl, weight_sparsity=[float(v) for v in args.sw.split(",")])
-    if args.p:
-        wl = dict(wl, act_sparsity=[float(v) for v in args.p.split(",")])
+    def __init__(self, launch: str):
+        import torch
 
-    # ---- inputs: prune (library host C++), calibrate, encode rotated copies
-    t_prep = time.perf_counter()
-    pruned = {}
-    for sw in wl["weight_sparsity"]:
-        for proj in wl["projections"]:
-            pruned[(sw, proj.name)] = spdp.prune_magnitude(proj.weight(), sw)
-    xs = {proj.name: proj.activations(batch) for proj in wl["projections"]}
-    # offline calibration sets: one per layer input (projections that read
-    # one input share it), drawn apart from the inputs (draw 1)
+        import paper_2607_21985_amd as spdp
+        import synth
+        self.torch, self.spdp, self.synth = torch, spdp, synth
+        self.dev = torch.device("cuda:0")
+        torch.cuda.set_device(self.dev)
+        self.stream = torch.cuda.current_stream(self.dev)
+        self.launch = launch
+        self._dense_w = {}
+
+    def sync(self):
+        self.torch.cuda.synchronize(self.dev)
+
+    def timed(self, fn, n):
+        """ms of n calls of fn(i), HIP events on the launch stream."""
+        torch = self.torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        for i in range(n):
+            fn(i)
+        e1.record(self.stream)
+        self.sync()
+        return e0.elapsed_time(e1)
+
+    def capture(self, fn):
+        """fn() captured into a graph on a side stream (replays go to the
+        current stream)."""
+        torch = self.torch
+        s = torch.cuda.Stream(device=self.dev)
+        s.wait_stream(torch.cuda.current_stream(self.dev))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=s):
+            fn()
+        torch.cuda.current_stream(self.dev).wait_stream(s)
+        return g
+
+    def to_dev(self, a16):
+        return self.torch.from_numpy(np.ascontiguousarray(a16).view(np.int16)).view(self.torch.float16).to(self.dev)
+
+    def dense_weight(self, proj):
+        key = (proj.rows, proj.cols, proj.w_seed)
+        if key not in self._dense_w:
+            self._dense_w[key] = proj.weight()
+        return self._dense_w[key]
+
+
+def input_key(pt):
+    return (pt["sw"], pt["p"], pt["proj"].x_seed, pt["proj"].x_kind, pt["proj"].cols)
+
+
+def make_points(B, wl, sw_list, p_list, batch, mask, calibration, pruned):
+    """The calls of one step: every (sw, p) point x every projection, each
+    with its input and threshold (the input's own p-quantile, or offline
+    calibration)."""
+    spdp = B.spdp
+    xs = {}
+    for proj in wl["projections"]:
+        key = (proj.x_seed, proj.x_kind, proj.cols)
+        if key not in xs:
+            xs[key] = proj.activations(batch)
     cal = {}
-    if args.calibration > 0:
+    if calibration > 0:
         for proj in wl["projections"]:
             key = (proj.x_seed, proj.x_kind, proj.cols)
             if key not in cal:
-                cal[key] = proj.activations(args.calibration, draw=1)
+                cal[key] = proj.activations(calibration, draw=1)
     points = []
-    for sw in wl["weight_sparsity"]:
-        for p in wl["act_sparsity"]:
+    for sw in sw_list:
+        for p in p_list:
             for proj in wl["projections"]:
-                x = xs[proj.name]
-                if args.mask == "batch":
+                key = (proj.x_seed, proj.x_kind, proj.cols)
+                x = xs[key]
+                if mask == "batch":
                     if cal:
-                        # the calibration tokens in batches of this size,
-                        # their column scores pooled
-                        cs = cal[(proj.x_seed, proj.x_kind, proj.cols)]
+                        cs = cal[key]
                         n = cs.shape[0] // batch * batch
                         groups = cs[:n].reshape(-1, batch, cs.shape[1])
                         sc = np.sort(np.concatenate([batch_scores(g) for g in groups]))
@@ -308,280 +403,412 @@ def main():
                     else:
                         t = batch_threshold_for(x, p)
                 elif cal:
-                    t = spdp.calibrate_threshold(cal[(proj.x_seed, proj.x_kind, proj.cols)], p)
+                    t = spdp.calibrate_threshold(cal[key], p)
                 else:
                     t = spdp.calibrate_threshold(x, p)
-                points.append({"sw": sw, "p": p, "proj": proj, "x": x, "t": t,
-                               "w": pruned[(sw, proj.name)],
+                points.append({"sw": sw, "p": p, "proj": proj, "x": x, "t": t, "w": pruned[(sw, proj.name)],
                                "label": f"{proj.name}@sw{sw:g}/p{p:g}"})
-    t_enc = time.perf_counter()
-    if args.rtn_bits:
-        enc = lambda w: spdp.encode_rtn(w, tile, args.rtn_bits)  # noqa: E731
-    else:
-        enc = lambda w: spdp.encode(w, tile)  # noqa: E731
+    return points
+
+
+def make_units(points, idx, grouped):
+    """Launch units: the products of one sweep point that read one input
+    form a group (at most 8); every other product is a unit of its own."""
+    units, open_ = [], {}
+    for j in idx:
+        key = input_key(points[j])
+        if grouped and key in open_ and len(units[open_[key]]) < 8:
+            units[open_[key]].append(j)
+        else:
+            open_[key] = len(units)
+            units.append([j])
+    return units
+
+
+def encode_copies(B, points, tile, rtn_bits, rotation_mb):
+    """Encoded copies of every call's matrix, enough of them that at least
+    rotation_mb of distinct weights lie between two uses of one copy."""
+    spdp = B.spdp
+    enc = (lambda w: spdp.encode_rtn(w, tile, rtn_bits)) if rtn_bits else (lambda w: spdp.encode(w, tile))
+    t0 = time.perf_counter()
     copy0 = [enc(pt["w"]) for pt in points]
-    enc_s = (time.perf_counter() - t_enc) / len(points)
-    dev_bytes = sum(len(m.format()["values"]) * (1 if args.rtn_bits else 2) for m in copy0)
-    n_copies = max(2, int(np.ceil(args.rotation_mb * 1e6 / max(dev_bytes, 1))) + 1)
+    enc_s = (time.perf_counter() - t0) / len(points)
+    fmts = [m.format() for m in copy0]
+    dev_bytes = sum(len(f["values"]) * (1 if rtn_bits else 2) for f in fmts)
+    n_copies = max(2, int(np.ceil(rotation_mb * 1e6 / max(dev_bytes, 1))) + 1)
     copies = [copy0] + [[enc(pt["w"]) for pt in points] for _ in range(n_copies - 1)]
-    for pt, m in zip(points, copy0):
-        f = m.format()
-        act = (batch_activity(pt["x"], pt["t"]) if args.mask == "batch"
+    return copies, fmts, enc_s
+
+
+def annotate(points, fmts, mask, spdp):
+    for pt, f in zip(points, fmts):
+        act = (batch_activity(pt["x"], pt["t"]) if mask == "batch"
                else token_activity(pt["x"], spdp.threshold_code(pt["t"])))
         pt["bytes"], pt["active_frac"] = call_bytes(f, act)
         pt["dropped"] = dropped_fraction(act)
         pt["flops"] = call_flops(f, act)
+        pt["lines"] = line_model(f, act)
         pt["rows"], pt["cols"] = f["rows"], f["cols"]
-        del f
-    # one device copy of each distinct input per rotation copy (grouped
-    # products share it, as a decoder's q, k and v share the layer input)
+
+
+def measure(B, points, copies, batch, mask, grouped, steps, warmup, *, floor=False, single=False,
+            per_point=False, stream_rate=False, profile_only=False, n_proj=None, calib_read_mib=0):
+    """Time steps of `points` (one call each, decoder grouping) over the
+    rotation copies: whole rotation cycles replayed as one graph (or host
+    launches). Returns the step time and what was asked for."""
+    torch, spdp = B.torch, B.spdp
+    n_copies = len(copies)
     X = []
     for _ in range(n_copies):
-        by_input = {}
-        row = []
+        by_input, row = {}, []
         for pt in points:
-            key = (pt["sw"], pt["p"], pt["proj"].x_seed, pt["proj"].x_kind, pt["proj"].cols)
+            key = input_key(pt)
             if key not in by_input:
-                by_input[key] = torch.from_numpy(pt["x"].view(np.int16)).view(torch.float16).to(dev)
+                by_input[key] = B.to_dev(pt["x"])
             row.append(by_input[key])
         X.append(row)
-
-    # launch units: the products of one sweep point that read one input form a
-    # group (at most 8), every other product is a unit of its own
-    def make_units(idx, grouped):
-        units, open_ = [], {}
-        for j in idx:
-            pt = points[j]
-            key = (pt["sw"], pt["p"], pt["proj"].x_seed, pt["proj"].x_kind, pt["proj"].cols)
-            if grouped and key in open_ and len(units[open_[key]]) < 8:
-                units[open_[key]].append(j)
-            else:
-                open_[key] = len(units)
-                units.append([j])
-        return units
-    Y = [[torch.empty((batch, pt["rows"]), dtype=torch.float16, device=dev) for pt in points]
+    Y = [[torch.empty((batch, pt["rows"]), dtype=torch.float16, device=B.dev) for pt in points]
          for _ in range(n_copies)]
     for cp in copies:
         for m in cp:
             m.reserve(batch)
-    prep_s = time.perf_counter() - t_prep
-    stream = torch.cuda.current_stream(dev)
+    all_idx = list(range(len(points)))
+    step_units = make_units(points, all_idx, grouped)
+    single_units = make_units(points, all_idx, False)
 
     def launch_calls(c, units, t_all=None):
-        # t_all: one threshold for every call instead of the points' own
         th = (lambda j: points[j]["t"]) if t_all is None else (lambda j: t_all)
         for u in units:
             if len(u) == 1:
-                copies[c][u[0]].spmspv_into(X[c][u[0]], th(u[0]), Y[c][u[0]], mask=args.mask)
+                copies[c][u[0]].spmspv_into(X[c][u[0]], th(u[0]), Y[c][u[0]], mask=mask)
             else:
                 spdp.spmspv_many([copies[c][j] for j in u], [X[c][j] for j in u],
-                                 [th(j) for j in u], [Y[c][j] for j in u], mask=args.mask)
+                                 [th(j) for j in u], [Y[c][j] for j in u], mask=mask)
 
-    all_idx = list(range(len(points)))
-    grouped = args.group == "decoder"
-    step_units = make_units(all_idx, grouped)
-    single_units = make_units(all_idx, False)
     graphs = {}
 
-    def capture(key, c, idx):
-        # capture on a side stream; replays go to the current stream
-        s = torch.cuda.Stream(device=dev)
-        s.wait_stream(torch.cuda.current_stream(dev))
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s):
-            launch_calls(c, idx)
-        torch.cuda.current_stream(dev).wait_stream(s)
-        graphs[key] = g
+    def cycle_graph(key, units, t_all=None):
+        graphs[key] = B.capture(lambda: [launch_calls(c, units, t_all) for c in range(n_copies)])
 
-    def step(i, mode, key="step", units=None):
-        c = i % n_copies
-        if mode == "graph":
-            graphs[(key, c)].replay()
-        else:
-            launch_calls(c, units if units is not None else step_units)
-
-    def capture_cycle(key, units, t_all=None):
-        # one rotation cycle (the steps of copies 0 .. n_copies-1, in order)
-        # as one graph: a decoder replays a whole token's pass over all its
-        # layers as one graph, so the graph's own start-up is paid once per
-        # many launches, not once per layer
-        s = torch.cuda.Stream(device=dev)
-        s.wait_stream(torch.cuda.current_stream(dev))
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=s):
-            for c in range(n_copies):
-                launch_calls(c, units, t_all)
-        torch.cuda.current_stream(dev).wait_stream(s)
-        graphs[(key, "cycle")] = g
-
-    def run_steps(first, n, mode, key="step", units=None):
-        # steps first .. first+n-1; in graph mode whole rotation cycles are
-        # one replay, the steps outside a whole cycle one replay each
+    def run_steps(first, n, key, units):
+        # whole rotation cycles as one graph replay; steps outside a whole
+        # cycle as host launches
         i, end = first, first + n
         while i < end:
-            if mode == "graph" and i % n_copies == 0 and i + n_copies <= end:
-                graphs[(key, "cycle")].replay()
+            if B.launch == "graph" and i % n_copies == 0 and i + n_copies <= end:
+                graphs[key].replay()
                 i += n_copies
             else:
-                step(i, mode, key, units)
+                launch_calls(i % n_copies, units)
                 i += 1
 
-    def timed(fn, n):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for i in range(n):
-            fn(i)
-        e1.record(stream)
-        torch.cuda.synchronize(dev)
-        return e0.elapsed_time(e1)
+    for i in range(max(1, warmup)):
+        launch_calls(i % n_copies, step_units)
+    B.sync()
+    if B.launch == "graph":
+        cycle_graph("step", step_units)
+        B.sync()
+    # whole cycles only, so that graph mode times graph replays alone
+    steps = max(n_copies, steps // n_copies * n_copies) if B.launch == "graph" else steps
+    run_steps(0, max(warmup // n_copies, 1) * n_copies, "step", step_units)
+    B.sync()
+    total_ms = B.timed(lambda _: run_steps(0, steps, "step", step_units), 1)
+    res = {"ms_per_step": total_ms / steps, "steps": steps, "n_launch": len(step_units),
+           "n_calls": len(points), "n_copies": n_copies,
+           "step_bytes": sum(pt["bytes"] for pt in points), "step_flops": sum(pt["flops"] for pt in points)}
+    if calib_read_mib:
+        peak_read_once(B, calib_read_mib)
+    if profile_only:
+        res["launches_in_run"] = (max(1, warmup) + max(warmup // n_copies, 1) * n_copies + steps) * len(step_units)
+        return res, step_units
+    if stream_rate:
+        res["stream_ms_per_step"] = B.timed(lambda i: launch_calls(i % n_copies, step_units), steps) / steps
+    if floor and B.launch == "graph":
+        # the same launches with threshold +inf: no column is active, every
+        # step but the value stream runs
+        cycle_graph("floor", step_units, float("inf"))
+        run_steps(0, n_copies, "floor", step_units)
+        B.sync()
+        res["floor_ms_per_step"] = B.timed(lambda _: run_steps(0, steps, "floor", step_units), 1) / steps
+    if single:
+        if B.launch == "graph":
+            cycle_graph("single", single_units)
+        run_steps(0, n_copies, "single", single_units)
+        B.sync()
+        res["single_ms_per_step"] = B.timed(lambda _: run_steps(0, steps, "single", single_units), 1) / steps
+    if per_point and n_proj:
+        # each sweep point's calls back to back (a graph per copy)
+        reps = max(2, min(10, steps))
+        per_call = np.zeros(len(points))
+        for k in range(0, len(points), n_proj):
+            units = make_units(points, list(range(k, k + n_proj)), grouped)
+            if B.launch == "graph":
+                gs = [B.capture(lambda c=c: launch_calls(c, units)) for c in range(n_copies)]
+                ms = B.timed(lambda r: gs[r % n_copies].replay(), reps)
+                del gs
+            else:
+                ms = B.timed(lambda r: launch_calls(r % n_copies, units), reps)
+            per_call[k:k + n_proj] = ms / (reps * n_proj)
+        res["per_call_ms"] = per_call
+    graphs.clear()
+    return res, step_units
 
-    # warm up eagerly (first calls load code, size workspaces), then capture
-    for i in range(max(1, args.warmup)):
-        step(i, "stream")
-    torch.cuda.synchronize(dev)
-    if args.launch == "graph":
-        for c in range(n_copies):
-            capture(("step", c), c, step_units)
-            capture(("single", c), c, single_units)
-        capture_cycle("step", step_units)
-        capture_cycle("single", single_units)
-        torch.cuda.synchronize(dev)
-    run_steps(0, args.warmup, args.launch)
-    torch.cuda.synchronize(dev)
-    total_ms = timed(lambda _: run_steps(args.warmup, args.steps, args.launch), 1)
-    if args.calib_copy_mib:
-        n = args.calib_copy_mib * (1 << 20)
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty(n, dtype=torch.uint8, device=dev)
-        torch.cuda.synchronize(dev)
-        dst.copy_(src)
-        torch.cuda.synchronize(dev)
-        del src, dst
-    if args.profile_only:
-        print(json.dumps({"profile_only": True, "launch": args.launch, "group": args.group,
-                          "ms_per_step": total_ms / args.steps,
-                          "launches": (2 * args.warmup + args.steps) * len(step_units),
-                          "algorithmic_bytes_per_launch": sum(pt["bytes"] for pt in points) / len(step_units)}),
-              flush=True)
+
+def dense_step_ms(B, projections, batch, steps, warmup, rotation_mb):
+    """One fp16 torch F.linear per projection (the dense GEMV/GEMM on the
+    same GPU), rotated over copies like the sparse calls."""
+    import torch.nn.functional as F
+    torch = B.torch
+    w_bytes = sum(proj.rows * proj.cols * 2 for proj in projections)
+    n_dc = max(2, int(np.ceil(rotation_mb * 1e6 / w_bytes)) + 1)
+    dW = {}
+    for proj in projections:
+        w16 = B.dense_weight(proj)
+        for c in range(n_dc):
+            dW[(c, proj.name)] = B.to_dev(w16)
+    dX = {proj.name: B.to_dev(proj.activations(batch)) for proj in projections}
+
+    def dcalls(c):
+        for proj in projections:
+            F.linear(dX[proj.name], dW[(c, proj.name)])
+
+    for c in range(n_dc):
+        dcalls(c)
+    B.sync()
+    g = B.capture(lambda: [dcalls(c) for c in range(n_dc)]) if B.launch == "graph" else None
+    steps = max(n_dc, steps // n_dc * n_dc)
+
+    def run(n):
+        for i in range(0, n, n_dc):
+            if g is not None:
+                g.replay()
+            else:
+                for c in range(n_dc):
+                    dcalls(c)
+
+    run(max(warmup // n_dc, 1) * n_dc)
+    B.sync()
+    ms = B.timed(lambda _: run(steps), 1) / steps
+    del g, dW, dX
+    torch.cuda.empty_cache()
+    return ms
+
+
+_PEAK = None
+
+
+def peak_lib():
+    global _PEAK
+    if _PEAK is None:
+        path = os.path.join(ROOT, "paper_2607_21985_amd", "libspdp_peak.so")
+        if not os.path.exists(path):
+            raise ImportError(f"{path} is not built; run `python -m paper_2607_21985_amd.build`")
+        L = ctypes.CDLL(path)
+        L.spdp_peak_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                     ctypes.c_void_p]
+        L.spdp_peak_read.restype = ctypes.c_int
+        _PEAK = L
+    return _PEAK
+
+
+def _peak_read(B, buf, off, nbytes, sink, blocks):
+    # the current stream: the capture stream while a graph is being captured
+    s = B.torch.cuda.current_stream(B.dev)
+    st = peak_lib().spdp_peak_read(ctypes.c_void_p(buf.data_ptr() + off), nbytes, ctypes.c_void_p(sink.data_ptr()),
+                                   blocks, ctypes.c_void_p(s.cuda_stream))
+    if st != 0:
+        raise RuntimeError(f"spdp_peak_read failed ({st})")
+
+
+def peak_read_once(B, mib):
+    """One streaming read of `mib` MiB (a known-size reference for counters)."""
+    torch = B.torch
+    n = mib << 20
+    buf = torch.ones(n // 2, dtype=torch.float16, device=B.dev)
+    sink = torch.empty(8192, dtype=torch.int32, device=B.dev)
+    B.sync()
+    _peak_read(B, buf, 0, n, sink, 4096)
+    B.sync()
+    del buf, sink
+
+
+def measured_peaks(B, launch_bytes):
+    """Streaming-read roof of this GPU (the library's read kernel, best grid,
+    1 GiB) and what the same kernel reaches on reads of one launch's
+    algorithmic size (consecutive chunks of 1 GiB so that each comes from
+    HBM, replayed as one graph like the spMspV launches); plus a 1 GiB torch
+    device copy (read + write bytes)."""
+    torch = B.torch
+    n = 1 << 30
+    buf = torch.ones(n // 2, dtype=torch.float16, device=B.dev)
+    sink = torch.empty(16384, dtype=torch.int32, device=B.dev)
+    best = (0.0, 0)
+    for blocks in (1024, 2048, 4096, 8192, 16384):
+        _peak_read(B, buf, 0, n, sink, blocks)
+        B.sync()
+        ms = B.timed(lambda i: _peak_read(B, buf, 0, n, sink, blocks), 5) / 5
+        best = max(best, (n / (ms * 1e-3) / 1e9, blocks))
+    chunk = max(16, int(launch_bytes) // 16 * 16)
+    n_chunks = max(2, n // chunk)
+    best_c = (0.0, 0)
+    for blocks in (512, 1024, 2048, 4096):
+        g = B.capture(lambda: [_peak_read(B, buf, i * chunk, chunk, sink, blocks) for i in range(n_chunks)])
+        g.replay()
+        B.sync()
+        ms = B.timed(lambda i: g.replay(), 3) / (3 * n_chunks)
+        best_c = max(best_c, (chunk / (ms * 1e-3) / 1e9, blocks))
+        del g
+    b_pk = torch.empty_like(buf)
+    for _ in range(2):
+        b_pk.copy_(buf)
+    B.sync()
+    copy_ms = B.timed(lambda i: b_pk.copy_(buf), 5) / 5
+    del buf, b_pk, sink
+    torch.cuda.empty_cache()
+    return {"read_gbs": round(best[0], 1), "read_blocks": best[1],
+            "read_gbs_at_launch_bytes": round(best_c[0], 1), "launch_bytes": chunk, "launch_blocks": best_c[1],
+            "copy_gbs": round(2 * n / (copy_ms * 1e-3) / 1e9, 1),
+            "how": "libspdp_peak streaming read (16-byte loads, 4 in flight per lane, best of 1024-16384 "
+                   "workgroups) of 1 GiB, mean of 5; the same kernel on consecutive chunks of one launch's "
+                   "algorithmic bytes, replayed as one graph; torch copy_ of 1 GiB (read + write bytes)"}
+
+
+# ---------------------------------------------------------------------------
+# one workload, end to end
+
+def prune_all(B, wl, sw_list):
+    return {(sw, proj.name): B.spdp.prune_magnitude(B.dense_weight(proj), sw)
+            for sw in sw_list for proj in wl["projections"]}
+
+
+def roof(step_bytes, step_flops, ms):
+    t_hbm = step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3
+    t_alu = step_flops / (VEC_PEAK_TFLOPS * 1e12) * 1e3
+    return {"frac": round(max(t_hbm, t_alu) / ms, 4), "binding": "alu" if t_alu > t_hbm else "hbm"}
+
+
+# the other workloads, each a (name, sw, p, batches) slice measured like the
+# headline: decoder grouping, graph replays of rotation cycles, dense fp16
+# baseline on the same batches
+SECONDARY = [
+    ("single-1024", 0.5, 0.5, [1]),
+    ("llama7b-mlp", 0.6, 0.5, [1, 2, 4, 8]),
+    ("llama13b-layer", 0.7, 0.5, [1, 4, 16]),
+    ("llama70b-layer", 0.7, 0.5, [1, 8, 32]),
+    ("llama70b-layer", 0.5, 0.0, [1, 8, 32]),
+    ("llama70b-layer", 0.8, 0.7, [1]),
+]
+
+
+def secondary(B, args):
+    out = []
+    dense_cache = {}
+    for name, sw, p, batches in SECONDARY:
+        wl = B.synth.workload(name)
+        pruned = prune_all(B, wl, [sw])
+        pts0 = make_points(B, wl, [sw], [p], batches[0], "token", 0, pruned)
+        copies, fmts, _ = encode_copies(B, pts0, wl["tile"], 0, args.rotation_mb)
+        for b in batches:
+            pts = make_points(B, wl, [sw], [p], b, "token", 0, pruned)
+            annotate(pts, fmts, "token", B.spdp)
+            r, _ = measure(B, pts, copies, b, "token", True, args.secondary_steps, 3)
+            ms = r["ms_per_step"]
+            if (name, b) not in dense_cache and not args.no_dense:
+                dense_cache[(name, b)] = dense_step_ms(B, wl["projections"], b, args.secondary_steps, 3,
+                                                       args.rotation_mb)
+            d = dense_cache.get((name, b))
+            e = {"workload": name, "sw": sw, "p": p, "batch": b,
+                 "calls": r["n_calls"], "launches": r["n_launch"],
+                 "us_per_product": round(ms * 1e3 / r["n_calls"], 3),
+                 "gbs": round(r["step_bytes"] / (ms * 1e-3) / 1e9, 1),
+                 "pct_of_hbm_peak": round(100 * r["step_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
+                 "roofline": roof(r["step_bytes"], r["step_flops"], ms),
+                 "active_frac": round(float(np.mean([pt["active_frac"] for pt in pts])), 4),
+                 "speedup_vs_dense": round(d / ms, 3) if d else None,
+                 "dense_us_per_product": round(d * 1e3 / r["n_calls"], 3) if d else None}
+            print(f"[bench] secondary {json.dumps(e)}", file=sys.stderr, flush=True)
+            out.append(e)
+        for cp in copies:
+            for m in cp:
+                m.close()
+        del copies
+        B.torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles)
         return
-    ms_per_step = total_ms / args.steps
-    step_bytes = sum(pt["bytes"] for pt in points)
-    value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    # the same steps with one host launch per call, and with every product
-    # as its own launch, for comparison
-    stream_ms = timed(lambda i: step(args.warmup + i, "stream"), args.steps) / args.steps
-    # the latency floor: the same launches with a threshold of +inf, so that
-    # no column is active and every step but the value stream runs (launch,
-    # set-up loads, activity test, list, split-K exchange, output)
-    floor_ms = None
-    if args.launch == "graph":
-        capture_cycle("floor", step_units, float("inf"))
-        run_steps(0, n_copies, "graph", "floor")
-        torch.cuda.synchronize(dev)
-        floor_ms = timed(lambda _: run_steps(0, args.steps // n_copies * n_copies or n_copies, "graph", "floor"),
-                         1) / (args.steps // n_copies * n_copies or n_copies)
-    single_ms = timed(lambda _: run_steps(args.warmup, args.steps, args.launch, "single", single_units),
-                      1) / args.steps
+    if args.gpus != 1:
+        print(json.dumps({"error": "this benchmark runs on one GPU: --gpus above 1 is not supported"}))
+        sys.exit(2)
+    import torch
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no ROCm GPU visible"}))
+        sys.exit(2)
+    B = Bench(args.launch)
+    spdp, synth = B.spdp, B.synth
+    wl = synth.workload(args.workload)
+    tile = wl["tile"]
+    batch = args.batch if args.batch is not None else wl["batch"][0]
+    sw_list = [float(v) for v in args.sw.split(",")] if args.sw else wl["weight_sparsity"]
+    p_list = [float(v) for v in args.p.split(",")] if args.p else wl["act_sparsity"]
 
-    # ---- duration per sweep point: the point's calls run back to back (as a
-    # captured graph in graph mode), so HIP events around a run of them
-    # divided by their number give the kernels' average duration; an event
-    # pair around every single launch would add its own overhead.
+    t_prep = time.perf_counter()
+    pruned = prune_all(B, wl, sw_list)
+    points = make_points(B, wl, sw_list, p_list, batch, args.mask, args.calibration, pruned)
+    copies, fmts, enc_s = encode_copies(B, points, tile, args.rtn_bits, args.rotation_mb)
+    annotate(points, fmts, args.mask, spdp)
+    prep_s = time.perf_counter() - t_prep
+    grouped = args.group == "decoder"
     n_proj = len(wl["projections"])
-    reps = max(2, min(10, args.steps))
-    per_call = np.zeros(len(points))
-    for k in range(0, len(points), n_proj):
-        idx = make_units(list(range(k, k + n_proj)), grouped)
-        if args.launch == "graph":
-            for c in range(n_copies):
-                capture(("pt", k, c), c, idx)
-            ms = timed(lambda r: graphs[("pt", k, r % n_copies)].replay(), reps)
-        else:
-            ms = timed(lambda r: launch_calls(r % n_copies, idx), reps)
-        per_call[k:k + n_proj] = ms / (reps * n_proj)
-    kern_ms = ms_per_step
-    achieved = step_bytes / (kern_ms * 1e-3) / 1e9
-    # the two roofs: T_roof = max(bytes / HBM peak, useful flops / vector peak)
-    step_flops = sum(pt["flops"] for pt in points)
+
+    if args.profile_only:
+        r, units = measure(B, points, copies, batch, args.mask, grouped, args.steps, args.warmup,
+                           profile_only=True, calib_read_mib=args.calib_read_mib)
+        lines = {k: [0, 0] for k in points[0]["lines"]}
+        for pt in points:
+            for k, (a, l) in pt["lines"].items():
+                lines[k][0] += a
+                lines[k][1] += l
+        n = len(units)
+        print(json.dumps({"profile_only": True, "argv": sys.argv[1:], "launch": args.launch, "group": args.group,
+                          "ms_per_step": r["ms_per_step"], "launches": r["launches_in_run"],
+                          "launches_per_step": n,
+                          "algorithmic_bytes_per_launch": r["step_bytes"] / n,
+                          "y_bytes_per_launch": lines["y"][0] / n,
+                          "line_model_per_launch": {k: [a / n, l / n] for k, (a, l) in lines.items()},
+                          "calib_read_bytes": args.calib_read_mib << 20}), flush=True)
+        return
+
+    r, step_units = measure(B, points, copies, batch, args.mask, grouped, args.steps, args.warmup,
+                            floor=True, single=True, per_point=True, stream_rate=True, n_proj=n_proj)
+    for cp in copies:
+        for m in cp:
+            m.close()
+    del copies
+    torch.cuda.empty_cache()
+    ms_per_step = r["ms_per_step"]
+    step_bytes, step_flops = r["step_bytes"], r["step_flops"]
+    n_launch = r["n_launch"]
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
     t_hbm_us = step_bytes / (HBM_PEAK_GBS * 1e9) * 1e6
     t_alu_us = step_flops / (VEC_PEAK_TFLOPS * 1e12) * 1e6
     alu_bound = t_alu_us > t_hbm_us
-    graphs.clear()
 
-    # ---- measured streaming peaks on this GPU: a 1 GiB device copy (read +
-    # write bytes) and a 1 GiB read-only reduction
-    n_pk = 1 << 30
-    a_pk = torch.empty(n_pk // 2, dtype=torch.float16, device=dev).fill_(1.0)
-    b_pk = torch.empty_like(a_pk)
-    for _ in range(2):
-        b_pk.copy_(a_pk)
-        a_pk.sum(dtype=torch.float32)
-    torch.cuda.synchronize(dev)
-    copy_ms = timed(lambda i: b_pk.copy_(a_pk), 5) / 5
-    read_ms = timed(lambda i: a_pk.sum(dtype=torch.float32), 5) / 5
-    peaks = {"copy_gbs": round(2 * n_pk / (copy_ms * 1e-3) / 1e9, 1),
-             "read_gbs": round(n_pk / (read_ms * 1e-3) / 1e9, 1),
-             "how": "torch copy_ of 1 GiB fp16 (read + write bytes) and torch sum of 1 GiB fp16 (read bytes), "
-                    "mean of 5 after 2 warm-ups"}
-    del a_pk, b_pk
-
-    # ---- dense fp16 GEMV baseline (torch F.linear), rotated the same way
+    peaks = measured_peaks(B, step_bytes / n_launch)
+    dense_ms = None if args.no_dense else dense_step_ms(B, wl["projections"], batch, args.steps, args.warmup,
+                                                        args.rotation_mb)
     dense = None
-    if not args.no_dense:
-        import torch.nn.functional as F
-        dW = {}
-        names = [proj.name for proj in wl["projections"]]
-        w_bytes = sum(proj.rows * proj.cols * 2 for proj in wl["projections"])
-        n_dc = max(2, int(np.ceil(args.rotation_mb * 1e6 / w_bytes)) + 1)
-        for proj in wl["projections"]:
-            w16 = proj.weight()
-            for c in range(n_dc):
-                dW[(c, proj.name)] = torch.from_numpy(w16.view(np.int16)).view(torch.float16).to(dev)
-        dX = {n: torch.from_numpy(xs[n].view(np.int16)).view(torch.float16).to(dev) for n in names}
+    if dense_ms is not None:
+        dense = {"us_per_call": dense_ms * 1e3 / n_proj,
+                 "gbs": sum(proj.rows * proj.cols * 2 + 2 * batch * (proj.rows + proj.cols)
+                            for proj in wl["projections"]) / (dense_ms * 1e-3) / 1e9}
 
-        def dcalls(c):
-            for n in names:
-                F.linear(dX[n], dW[(c, n)])
-
-        for c in range(n_dc):
-            dcalls(c)
-        torch.cuda.synchronize(dev)
-        dgraphs = []
-        if args.launch == "graph":
-            # per copy, and one rotation cycle as one graph, as for spMspV
-            for cs in [[c] for c in range(n_dc)] + [list(range(n_dc))]:
-                s_cap = torch.cuda.Stream(device=dev)
-                s_cap.wait_stream(torch.cuda.current_stream(dev))
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=s_cap):
-                    for c in cs:
-                        dcalls(c)
-                torch.cuda.current_stream(dev).wait_stream(s_cap)
-                dgraphs.append(g)
-
-        def drun(first, n):
-            i, end = first, first + n
-            while i < end:
-                if dgraphs and i % n_dc == 0 and i + n_dc <= end:
-                    dgraphs[n_dc].replay()
-                    i += n_dc
-                else:
-                    if dgraphs:
-                        dgraphs[i % n_dc].replay()
-                    else:
-                        dcalls(i % n_dc)
-                    i += 1
-
-        drun(0, args.warmup)
-        torch.cuda.synchronize(dev)
-        d_us = timed(lambda _: drun(args.warmup, args.steps), 1) * 1e3 / (args.steps * len(names))
-        del dgraphs
-        dense = {"us_per_call": d_us,
-                 "gbs": (w_bytes / len(names) + 2 * batch * (wl["projections"][0].rows + wl["projections"][0].cols)) / (d_us * 1e-6) / 1e9}
-        del dW
-
-    # ---- per-point summary
     pts_out = []
+    per_call = r["per_call_ms"]
     for k in range(0, len(points), n_proj):
         grp = points[k:k + n_proj]
         us = float(per_call[k:k + n_proj].sum() * 1e3 / n_proj)
@@ -595,21 +822,17 @@ def main():
             d["speedup_vs_dense"] = round(dense["us_per_call"] / us, 3)
         pts_out.append(d)
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(points, args.mask, rtn_bits=args.rtn_bits)
-
-    # the committed counter summaries are of fp16 Values
+    sec = None if args.no_secondary else secondary(B, args)
+    cpu = None if args.no_cpu_baseline else cpu_baseline(points, args.mask, rtn_bits=args.rtn_bits)
     traffic = None if args.rtn_bits else read_traffic(args.workload, args.group)
-    n_launch = len(step_units)
     us_per_call = ms_per_step * 1e3 / len(points)
-    kernel_us = kern_ms * 1e3 / n_launch
+    kernel_us = ms_per_step * 1e3 / n_launch
     out = {
-        "metric": "spMspV \u00b5s/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
+        "metric": "spMspV µs/call + achieved HBM GB/s (% of peak), Llama-7B shapes, batch 1",
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": r["steps"],
         "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True,
@@ -621,10 +844,10 @@ def main():
             "workload": args.workload,
             "shapes": sorted({f"{pt['rows']}x{pt['cols']}" for pt in points}),
             "projections": [proj.name for proj in wl["projections"]],
-            "weight_sparsity": wl["weight_sparsity"], "act_sparsity": wl["act_sparsity"],
+            "weight_sparsity": sw_list, "act_sparsity": p_list,
             "batch": batch, "tile": list(tile), "calls_per_step": len(points),
             "launches_per_step": n_launch, "grouping": args.group,
-            "rotation_copies": n_copies, "accumulate": "f32",
+            "rotation_copies": r["n_copies"], "accumulate": "f32",
             "values": (f"rtn{args.rtn_bits}: {args.rtn_bits}-bit round-to-nearest codes, one byte each, one "
                        "fp32 scale per row" if args.rtn_bits else "fp16"),
             "mask": args.mask,
@@ -634,19 +857,21 @@ def main():
                           {"rule": "own percentile", "how": "p-quantile of |x| over the input itself"}),
         },
         "us_per_call": round(us_per_call, 3),
-        "us_per_call_ungrouped": round(single_ms * 1e3 / len(points), 3),
-        "gbs_ungrouped": round(step_bytes / (single_ms * 1e-3) / 1e9, 2),
-        "us_per_call_stream_launch": round(stream_ms * 1e3 / len(points), 3),
+        "us_per_call_ungrouped": round(r["single_ms_per_step"] * 1e3 / len(points), 3),
+        "gbs_ungrouped": round(step_bytes / (r["single_ms_per_step"] * 1e-3) / 1e9, 2),
+        "us_per_call_stream_launch": round(r["stream_ms_per_step"] * 1e3 / len(points), 3),
         "launch": args.launch,
         "pct_of_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "measured_peaks": peaks,
         "pct_of_measured_read_peak": round(100 * value / peaks["read_gbs"], 2),
+        "pct_of_read_at_launch_bytes": round(100 * value / peaks["read_gbs_at_launch_bytes"], 2),
         "roofline": {
-            **({"bound": "alu", "achieved": round(step_flops / (kern_ms * 1e-3) / 1e12, 3),
+            **({"bound": "alu", "achieved": round(step_flops / (ms_per_step * 1e-3) / 1e12, 3),
                 "peak": VEC_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(t_alu_us / (kern_ms * 1e3), 4)} if alu_bound else
-               {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4)}),
+                "frac": round(t_alu_us / (ms_per_step * 1e3), 4)} if alu_bound else
+               {"bound": "hbm", "achieved": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 2),
+                "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}),
             "traffic": traffic,
             "t_roof_us_per_step": {"hbm": round(t_hbm_us, 3), "alu": round(t_alu_us, 3),
                                    "binding": "alu" if alu_bound else "hbm"},
@@ -657,19 +882,159 @@ def main():
                                f"({'one captured graph per rotation cycle of steps' if args.launch == 'graph' else 'back-to-back launches'})",
             "algorithmic_bytes_per_launch": int(step_bytes / n_launch),
         },
-        "latency_floor": ({"us_per_launch": round(floor_ms * 1e3 / n_launch, 3),
-                           "frac_of_launch": round(floor_ms / kern_ms, 4),
+        "latency_floor": ({"us_per_launch": round(r["floor_ms_per_step"] * 1e3 / n_launch, 3),
+                           "frac_of_launch": round(r["floor_ms_per_step"] / ms_per_step, 4),
                            "how": "the same launches with threshold +inf: no column active, every step "
-                                  "but the value stream runs"} if floor_ms is not None else None),
+                                  "but the value stream runs"} if "floor_ms_per_step" in r else None),
         "cpu_baseline": cpu,
         "dense_gemv": dense,
         "speedup_vs_dense": round(dense["us_per_call"] / us_per_call, 3) if dense else None,
         "points": pts_out,
+        "secondary": sec,
         "prep_s": round(prep_s, 2),
         "encode_s_per_matrix": round(enc_s, 4),
         "host": platform.node(),
     }
     print(json.dumps(out), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# rocprofv3 summaries (profiles/*.txt) from the raw outputs of the commands
+# below, written under DIR on the GPU machine:
+#   rocprofv3 --kernel-trace --stats --output-format csv -d DIR/trace_TAG -o run -- \
+#       python3 bench.py --profile-only ARGS > DIR/trace_TAG.log
+#   rocprofv3 --pmc PASS_R --output-format csv -d DIR/pmcR_TAG -o run -- \
+#       python3 bench.py --profile-only --calib-read-mib 256 ARGS > DIR/pmcR_TAG.log
+#   rocprofv3 --pmc PASS_W ... -d DIR/pmcW_TAG ... > DIR/pmcW_TAG.log
+# Read bytes are counted by request size (32, 64 and 128-byte requests from
+# the L2 to memory), write bytes by the 32/64-byte write requests; the
+# streaming-read kernel of known size checks those formulas.
+
+PASS_R = ["TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum", "TCC_EA0_RDREQ_sum"]
+PASS_W = ["TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum", "TCC_BUBBLE_sum", "TCC_EA0_RDREQ_DRAM_sum"]
+
+
+def _profile_line(path):
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("{") and "profile_only" in line:
+                return json.loads(line)
+    raise ValueError(f"{path}: no --profile-only line")
+
+
+def _counters(path):
+    """{counter: ([per spmspv dispatch], [per read-kernel dispatch])}."""
+    out = {}
+    with open(path) as fh:
+        for row in csv.DictReader(fh):
+            name = row["Counter_Name"]
+            k = row["Kernel_Name"]
+            v = float(row["Counter_Value"])
+            sp, rd = out.setdefault(name, ([], []))
+            if "spmspv_kernel" in k:
+                sp.append(v)
+            elif "read_kernel" in k:
+                rd.append(v)
+    return out
+
+
+def _cmd(kind, d, tag, pj, extra=""):
+    prof = {"trace": "--kernel-trace --stats", "pmcR": "--pmc " + " ".join(PASS_R),
+            "pmcW": "--pmc " + " ".join(PASS_W)}[kind]
+    return (f"rocprofv3 {prof} --output-format csv -d {d}/{kind}_{tag} -o run -- python3 bench.py "
+            + " ".join(pj["argv"]) + f" > {d}/{kind}_{tag}.log")
+
+
+def summarize_profiles(d, prof_dir=None):
+    sha = kernel_source_sha()
+    prof_dir = prof_dir or os.path.join(ROOT, "profiles")
+    tags = sorted(n[len("trace_"):] for n in os.listdir(d)
+                  if n.startswith("trace_") and os.path.isdir(os.path.join(d, n)))
+    for tag in tags:
+        pj = _profile_line(os.path.join(d, f"trace_{tag}.log"))
+        rows = list(csv.DictReader(open(os.path.join(d, f"trace_{tag}", "run_kernel_stats.csv"))))
+        out = [f"# spmspv_kernel: {tag}", "", "command (GPU box, repository root, TMPDIR=/tmp):",
+               "  " + _cmd("trace", d, tag, pj), "",
+               "kernel_stats (durations in ns):", "Name | Calls | AverageNs | MinNs | MaxNs"]
+        for r in rows:
+            out.append(f"{r['Name'].replace('(anonymous namespace)::', '')[:70]} | {r['Calls']} | "
+                       f"{float(r['AverageNs']):.1f} | {r['MinNs']} | {r['MaxNs']}")
+        kr = [r for r in rows if "spmspv_kernel" in r["Name"]]
+        calls = sum(int(r["Calls"]) for r in kr)
+        avg = sum(int(r["Calls"]) * float(r["AverageNs"]) for r in kr) / max(calls, 1)
+        alg = pj["algorithmic_bytes_per_launch"]
+        out += ["", f"all spmspv_kernel variants: {calls} launches, launch-weighted average {avg:.1f} ns",
+                f"  -> {alg / avg:.1f} GB/s algorithmic ({100 * alg / avg / HBM_PEAK_GBS:.2f} % of "
+                f"{HBM_PEAK_GBS:.0f} GB/s)",
+                "", "bench.py --profile-only (same command) reported:",
+                f"  ms_per_step = {pj['ms_per_step']:.5f} ({pj['launches_per_step']} launches per step: "
+                f"{pj['ms_per_step'] * 1e6 / pj['launches_per_step']:.1f} ns per launch)",
+                f"  launches = {pj['launches']}", f"  algorithmic_bytes_per_launch = {alg:.0f}",
+                f"kernel_us_per_launch: {avg / 1e3:.4f}", f"kernel_sha: {sha}", ""]
+        with open(os.path.join(prof_dir, f"spmspv_{tag}_kernel_trace.txt"), "w") as fh:
+            fh.write("\n".join(out))
+        print("\n".join(out))
+
+        pr, pw = os.path.join(d, f"pmcR_{tag}"), os.path.join(d, f"pmcW_{tag}")
+        if not (os.path.isdir(pr) and os.path.isdir(pw)):
+            continue
+        cr = _counters(os.path.join(pr, "run_counter_collection.csv"))
+        cw = _counters(os.path.join(pw, "run_counter_collection.csv"))
+        pjr = _profile_line(os.path.join(d, f"pmcR_{tag}.log"))
+
+        def mean(c, name, which=0):
+            v = c[name][which]
+            return sum(v) / len(v) if v else float("nan")
+
+        n32, n64, n128, nall = (mean(cr, c) for c in PASS_R)
+        nw, nw64, nbub, ndram = (mean(cw, c) for c in PASS_W)
+        rd = 32 * n32 + 64 * n64 + 128 * n128
+        wr = 64 * nw64 + 32 * (nw - nw64)
+        fetch_formula = (nbub * 128 + (nall - nbub - n32) * 64 + n32 * 32)
+        # the streaming read of known size
+        c32, c64, c128, call_ = (mean(cr, c, 1) for c in PASS_R)
+        crd = 32 * c32 + 64 * c64 + 128 * c128
+        cbub = mean(cw, "TCC_BUBBLE_sum", 1)
+        cfetch = (cbub * 128 + (call_ - cbub - c32) * 64 + c32 * 32)
+        ref = pjr["calib_read_bytes"]
+        y = pj["y_bytes_per_launch"]
+        lm = pj["line_model_per_launch"]
+        line_rd = sum(l for k, (a, l) in lm.items() if k != "y")
+        alg_rd = sum(a for k, (a, l) in lm.items() if k != "y")
+        partial_w = max(wr - y, 0.0)
+        out = [f"# HBM traffic of spmspv_kernel: {tag}", "",
+               "commands (GPU box, repository root, TMPDIR=/tmp), one counter pass per run:",
+               "  " + _cmd("pmcR", d, tag, pjr), "  " + _cmd("pmcW", d, tag, _profile_line(os.path.join(d, f"pmcW_{tag}.log"))),
+               "",
+               f"reference: the streaming-read kernel over {ref} bytes (16-byte loads):",
+               f"  read requests 32/64/128 B = {c32:.0f} / {c64:.0f} / {c128:.0f} (all sizes: {call_:.0f})",
+               f"  bytes by request size = {crd:.0f} = {crd / ref:.4f} x the bytes read",
+               f"  FETCH_SIZE's formula (TCC_BUBBLE as the 128-byte count) = {cfetch:.0f} = {cfetch / ref:.4f} x",
+               "",
+               f"spmspv_kernel, mean per dispatch ({len(cr[PASS_R[0]][0])} dispatches per pass):",
+               f"  read requests 32/64/128 B = {n32:.0f} / {n64:.0f} / {n128:.0f} (all sizes: {nall:.0f}; "
+               f"to DRAM: {ndram:.0f}; TCC_BUBBLE {nbub:.0f})",
+               f"  read bytes by request size = {rd:.0f}",
+               f"  write requests = {nw:.0f} ({nw64:.0f} of 64 B) -> write bytes = {wr:.0f}",
+               f"  FETCH_SIZE's formula = {fetch_formula:.0f} B, WRITE_SIZE = {wr:.0f} B (raw derived counters)",
+               "",
+               "per source, bytes per launch: algorithmic | whole 128-byte lines holding them",
+               ]
+        for k, (a, l) in lm.items():
+            out.append(f"  {k:11s} {a:14.0f} | {l:14.0f}")
+        out += [f"  {'reads':11s} {alg_rd:14.0f} | {line_rd:14.0f}   (measured read bytes {rd:.0f}: "
+                f"{rd / line_rd:.3f} x the lines, {rd / alg_rd:.3f} x the algorithmic reads)",
+                f"  split-K partials written (measured writes - y) = {partial_w:.0f}; read back at least as many",
+                f"  reads beyond the lines = {rd - line_rd:.0f} "
+                f"({(rd - line_rd) / max(partial_w, 1):.2f} x the partial bytes written)",
+                "",
+                f"algorithmic bytes per launch = {pj['algorithmic_bytes_per_launch']:.0f}",
+                f"measured traffic per launch (reads + writes) = {rd + wr:.0f} = "
+                f"{(rd + wr) / pj['algorithmic_bytes_per_launch']:.3f} x algorithmic",
+                f"hbm_bytes_per_launch: {rd + wr:.0f}", f"kernel_sha: {sha}", ""]
+        with open(os.path.join(prof_dir, f"traffic_spmspv_{tag}.txt"), "w") as fh:
+            fh.write("\n".join(out))
+        print("\n".join(out))
 
 
 if __name__ == "__main__":

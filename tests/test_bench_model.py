@@ -1,5 +1,7 @@
 """bench.py's byte model agrees with the oracle's (CPU only)."""
 
+import json
+
 import numpy as np
 import pytest
 
@@ -84,3 +86,86 @@ def test_batch_mask_models_match_oracle(rows, cols, tile, sw, p, batch):
     got, frac = bench.call_bytes(f, act)
     assert got == oracle.algorithmic_bytes(oracle.encode(w, *tile), x, t, "batch")
     assert bench.call_flops(f, act) == oracle.useful_flops(w, x, t, "batch")
+
+
+@pytest.mark.parametrize("rows,cols,tile,sw,p,batch,bits", [
+    (700, 900, (256, 16), 0.6, 0.25, 1, 16), (300, 1000, (128, 8), 0.5, 0.5, 3, 16),
+    (333, 517, (192, 4), 0.7, 0.5, 8, 16), (520, 700, (256, 16), 0.5, 0.4, 2, 4),
+])
+def test_line_model_against_brute_force(rows, cols, tile, sw, p, batch, bits):
+    """Per-source bytes: the algorithmic parts add up to call_bytes, and the
+    128-byte lines are those a scalar walk over every active (stripe,
+    column) range touches."""
+    w = oracle.magnitude_prune(synth.weights(rows, cols, rows + 3 * cols), sw)
+    x = synth.laplace_activations(batch, cols, 17)
+    t = float(oracle.threshold_for(x, p))
+    f = (spdp.encode_rtn_host(w, tile, bits) if bits < 16 else spdp.encode_host(w, tile)).format()
+    act = bench.token_activity(x, spdp.threshold_code(t))
+    lm = bench.line_model(f, act)
+    total, _ = bench.call_bytes(f, act)
+    assert sum(a for a, _ in lm.values()) == total
+    assert all(l >= a for a, l in lm.values())
+    tm, tk = tile
+    R, C = f["n_stripes"], f["n_colblocks"]
+    vb, pad = (1, 16) if bits < 16 else (2, 8)
+    union = act.any(axis=0)
+    vlines, blines = set(), set()
+    for r in range(R):
+        for k in range(cols):
+            if not union[k]:
+                continue
+            g = r * C + k // tk
+            ci = int(f["col_info"][g * tk + k % tk])
+            nnz = ci & 0xFFFF
+            start = (int(f["tile_offset"][g]) + (ci >> 16)) * vb
+            n = -(-nnz // pad) * pad * vb
+            vlines.update(range(start // 128, (start + n - 1) // 128 + 1) if n else [])
+            boff = (g * tk + k % tk) * (tm // 8)
+            blines.add(boff // 128)
+    assert lm["values"][1] == 128 * len(vlines)
+    assert lm["bitmap"][1] == 128 * len(blines)
+
+
+def test_profile_summaries_from_raw_counters(tmp_path):
+    """--summarize-profiles: kernel time from the trace pass, read bytes by
+    request size and write bytes from the two counter passes, checked on a
+    made-up raw output directory."""
+    d = tmp_path / "raw"
+    out = tmp_path / "profiles"
+    out.mkdir()
+    tag = "wl_decoder"
+    pj = {"profile_only": True, "argv": ["--profile-only", "--workload", "wl"], "ms_per_step": 0.02,
+          "launches": 4, "launches_per_step": 2, "algorithmic_bytes_per_launch": 10000.0,
+          "y_bytes_per_launch": 100.0, "calib_read_bytes": 4096,
+          "line_model_per_launch": {"values": [8000, 8192], "bitmap": [1000, 1280], "colinfo": [500, 512],
+                                    "tileoffset": [100, 128], "x": [300, 384], "y": [100, 128],
+                                    "scales": [0, 0]}}
+    for kind in ("trace", "pmcR", "pmcW"):
+        (d / f"{kind}_{tag}").mkdir(parents=True)
+        (d / f"{kind}_{tag}.log").write_text("noise\n" + json.dumps(dict(pj, argv=pj["argv"] + [kind])) + "\n")
+    (d / f"trace_{tag}" / "run_kernel_stats.csv").write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+        '"void spmspv_kernel<1, 4, true, false, false>(LaunchArgs)",4,40000,10000.0,90,9000,11000,1\n')
+    hdr = '"Kernel_Name","Counter_Name","Counter_Value"\n'
+    rows_r = [("spmspv_kernel<1>", "TCC_EA0_RDREQ_32B_sum", 10), ("spmspv_kernel<1>", "TCC_EA0_RDREQ_64B_sum", 20),
+              ("spmspv_kernel<1>", "TCC_EA0_RDREQ_128B_sum", 80), ("spmspv_kernel<1>", "TCC_EA0_RDREQ_sum", 110),
+              ("read_kernel", "TCC_EA0_RDREQ_32B_sum", 0), ("read_kernel", "TCC_EA0_RDREQ_64B_sum", 0),
+              ("read_kernel", "TCC_EA0_RDREQ_128B_sum", 32), ("read_kernel", "TCC_EA0_RDREQ_sum", 32)]
+    rows_w = [("spmspv_kernel<1>", "TCC_EA0_WRREQ_sum", 30), ("spmspv_kernel<1>", "TCC_EA0_WRREQ_64B_sum", 10),
+              ("spmspv_kernel<1>", "TCC_BUBBLE_sum", 80), ("spmspv_kernel<1>", "TCC_EA0_RDREQ_DRAM_sum", 100),
+              ("read_kernel", "TCC_BUBBLE_sum", 32), ("read_kernel", "TCC_EA0_WRREQ_sum", 1),
+              ("read_kernel", "TCC_EA0_WRREQ_64B_sum", 0), ("read_kernel", "TCC_EA0_RDREQ_DRAM_sum", 32)]
+    for kind, rows in (("pmcR", rows_r), ("pmcW", rows_w)):
+        (d / f"{kind}_{tag}" / "run_counter_collection.csv").write_text(
+            hdr + "".join(f'"{k}","{c}",{v}\n' for k, c, v in rows))
+    bench.summarize_profiles(str(d), str(out))
+    trace = (out / f"spmspv_{tag}_kernel_trace.txt").read_text()
+    assert "kernel_us_per_launch: 10.0000" in trace and "1.0 GB/s algorithmic" in trace
+    traffic = (out / f"traffic_spmspv_{tag}.txt").read_text()
+    rd = 32 * 10 + 64 * 20 + 128 * 80
+    wr = 64 * 10 + 32 * 20
+    assert f"read bytes by request size = {rd}" in traffic
+    assert f"write bytes = {wr}" in traffic
+    assert f"hbm_bytes_per_launch: {rd + wr}" in traffic
+    assert "= 4096 = 1.0000 x the bytes read" in traffic
+    assert f"kernel_sha: {bench.kernel_source_sha()}" in traffic
