@@ -28,6 +28,9 @@ Functions and the passages of the paper they follow:
 * ``spmspv`` / ``spmspv_rows`` -- the masked product
   ``y = W_sp . mask(x)`` (Sec. 2.2 SP and DP definitions combined; Sec. 4.2
   says inactive columns contribute nothing).
+* ``spmm`` / ``spmm_flops`` -- the prefill product ``Y = X W_sp^T`` for N
+  tokens (Sec. 4.3: prefill keeps static pruning and drops dynamic pruning)
+  and its useful and dense flop counts.
 * ``storage_bytes`` -- the Tiled-CBC storage formula (Sec. 4.1).
 * ``compression_ratio``, ``compute_intensity``, ``compute_intensity_spdp``,
   ``attainable``, ``combined_sparsity`` -- Eq. 1, Eq. 2, the roofline, Eq. 3
@@ -75,6 +78,8 @@ __all__ = [
     "decode",
     "spmspv",
     "spmspv_rows",
+    "spmm",
+    "spmm_flops",
     "storage_bytes",
     "unpadded_bytes",
     "compression_ratio",
@@ -473,6 +478,34 @@ def spmspv_rows(w_sp: np.ndarray, x: np.ndarray, t: float, rows, mask: str = "to
     w64 = np.asarray(w_sp, dtype=np.float16)[rows].astype(np.float64)
     xm = masked_activations(np.atleast_2d(x), t, mask).astype(np.float64)
     return xm @ w64.T, np.abs(xm) @ np.abs(w64).T
+
+
+# --------------------------------------------------------------------------
+# The prefill product (Sec. 4.3: prefill applies static pruning only, a
+# sparse matrix times many tokens)
+# --------------------------------------------------------------------------
+
+def spmm(w_sp: np.ndarray, x: np.ndarray):
+    """``Y[n, m] = sum_k W_sp[m, k] * X[n, k]`` for N tokens, in float64.
+
+    No dynamic pruning: every column takes part (the prefill path drops the
+    DP stage). Returns ``(y64, s64, y16)`` like ``spmspv``: the float64
+    result, ``S[n, m] = sum_k |W_sp[m, k]| |X[n, k]|`` for the error bound,
+    and ``y64`` rounded once to fp16.
+    """
+    w64 = np.asarray(w_sp, dtype=np.float16).astype(np.float64)
+    x64 = np.atleast_2d(np.asarray(x, dtype=np.float16)).astype(np.float64)
+    y64 = x64 @ w64.T
+    s64 = np.abs(x64) @ np.abs(w64).T
+    return y64, s64, y64.astype(np.float16)
+
+
+def spmm_flops(w_sp: np.ndarray, n_tokens: int):
+    """(useful, dense) flops of a prefill product: 2 x nonzeros x tokens,
+    and 2 M K N for the dense matrix of the same shape."""
+    nnz = int(((_bits(np.asarray(w_sp, dtype=np.float16)) & 0x7FFF) != 0).sum())
+    m, k = np.asarray(w_sp).shape
+    return 2 * nnz * int(n_tokens), 2 * m * k * int(n_tokens)
 
 
 # --------------------------------------------------------------------------

@@ -706,3 +706,56 @@ def test_algorithmic_bytes_codes_brute():
         total += 4 * len({k // 8 for k in range(40) if act[k]})
     total += 2 * 40 + 2 * 130 + 4 * 130
     assert oracle.algorithmic_bytes_codes(f, x, t) == total
+
+
+# ---------------------------------------------------------------------------
+# The prefill product (Sec. 4.3: static pruning only, N tokens)
+
+def test_spmm_exact_rational_brute_force():
+    from fractions import Fraction
+    rng = np.random.default_rng(123)
+    for rows, cols, n in [(3, 5, 2), (7, 4, 5), (1, 9, 3), (6, 6, 1)]:
+        w = oracle.magnitude_prune(rng.normal(0, 1, (rows, cols)).astype(np.float16), 0.4)
+        x = (rng.normal(0, 2, (n, cols))).astype(np.float16)
+        y64, s64, y16 = oracle.spmm(w, x)
+        for t in range(n):
+            for m in range(rows):
+                exact = sum(Fraction(float(w[m, k])) * Fraction(float(x[t, k])) for k in range(cols))
+                mag = sum(abs(Fraction(float(w[m, k])) * Fraction(float(x[t, k]))) for k in range(cols))
+                assert abs(Fraction(y64[t, m]) - exact) <= Fraction(cols, 2 ** 52) * mag
+                assert Fraction(s64[t, m]) == mag or abs(Fraction(s64[t, m]) - mag) <= Fraction(cols, 2 ** 52) * mag
+    # small integers: every sum is exact, so the float64 result is the integer
+    w = rng.integers(-5, 6, (9, 13)).astype(np.float16)
+    x = rng.integers(-5, 6, (4, 13)).astype(np.float16)
+    y64, _, _ = oracle.spmm(w, x)
+    ref = [[sum(int(w[m, k]) * int(x[t, k]) for k in range(13)) for m in range(9)] for t in range(4)]
+    assert np.array_equal(y64, np.array(ref, dtype=np.float64))
+
+
+def test_spmm_special_cases():
+    rng = np.random.default_rng(5)
+    x = rng.normal(0, 1, (6, 40)).astype(np.float16)
+    # identity weights give the tokens back, bit for bit
+    y64, _, y16 = oracle.spmm(np.eye(40, dtype=np.float16), x)
+    assert np.array_equal(y16.view(np.uint16), x.view(np.uint16))
+    # unit tokens pick columns of W
+    w = oracle.magnitude_prune(rng.normal(0, 1, (30, 40)).astype(np.float16), 0.5)
+    e = np.zeros((3, 40), dtype=np.float16)
+    e[0, 7] = e[1, 0] = e[2, 39] = 1.0
+    y64, _, _ = oracle.spmm(w, e)
+    assert np.array_equal(y64[0], w[:, 7].astype(np.float64))
+    assert np.array_equal(y64[1], w[:, 0].astype(np.float64))
+    assert np.array_equal(y64[2], w[:, 39].astype(np.float64))
+    # all-zero weights: exact zeros; and no threshold drops anything, so it
+    # is the decode product with a negative threshold
+    assert not oracle.spmm(np.zeros((5, 40), np.float16), x)[0].any()
+    assert np.array_equal(oracle.spmm(w, x)[0], oracle.spmspv(w, x, -1.0)[0])
+
+
+def test_spmm_flops_hand_count():
+    w = np.zeros((4, 6), dtype=np.float16)
+    w[0, 1] = 1.0
+    w[2, 3] = -2.0
+    w[3, 5] = np.float16(-0.0)  # -0 is not a nonzero
+    w[1, 0] = 3.0
+    assert oracle.spmm_flops(w, 10) == (2 * 3 * 10, 2 * 4 * 6 * 10)
