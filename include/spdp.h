@@ -198,6 +198,30 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count,
                           const float* thresholds, int32_t mask,
                           uint16_t* const* Y, void* stream);
 
+/*
+ * spdp_spmm -- the prefill product on the same encoded matrix (Sec. 4.3):
+ * Y = X W_sp^T for n_tokens tokens, static pruning only (no activation
+ * test: every column takes part), on the matrix cores: each 256 x 16 GTile
+ * is expanded into a dense tile in LDS and multiplied with fp16 MFMA
+ * instructions, fp32 accumulation, one rounding to fp16 (nearest even).
+ *
+ *   h          handle from spdp_encode with tile_m = 256 and tile_k >= 16
+ *              (a power of two); fp16 Values. Other handles:
+ *              SPDP_ERR_UNSUPPORTED.
+ *   X          device, n_tokens x cols fp16, row-major, 16-byte aligned.
+ *   n_tokens   1 <= n_tokens <= 65535 * 128.
+ *   Y          device, n_tokens x rows fp16, row-major, 16-byte aligned,
+ *              fully overwritten; must not overlap X.
+ *   stream     hipStream_t to enqueue on.
+ *
+ * Asynchronous, one kernel launch, no allocation and no workspace (no
+ * split-K: each output element is summed by one wave), so it may be
+ * captured into a HIP graph. The fp32 summation order is fixed by the
+ * matrix, so equal inputs give equal bits.
+ */
+int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens,
+              uint16_t* Y, void* stream);
+
 /* spdp_reserve -- size the handle's workspace for batches up to max_batch. */
 int spdp_reserve(spdp_handle_t h, int32_t max_batch);
 

@@ -47,7 +47,7 @@ EXPORTED_SYMBOLS = (
     "spdp_reserve", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
-    "spdp_encode_rtn", "spdp_encode_rtn_host", "spdp_spmspv_noalloc",
+    "spdp_encode_rtn", "spdp_encode_rtn_host", "spdp_spmspv_noalloc", "spdp_spmm",
 )
 
 SPDP_OK = 0
@@ -107,6 +107,7 @@ def lib() -> ctypes.CDLL:
     L.spdp_encode_rtn_host.argtypes = [u16p, i64, i64, i32, i32, i32, ctypes.POINTER(H)]
     L.spdp_spmspv.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
     L.spdp_spmspv_noalloc.argtypes = [H, ctypes.c_void_p, i32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p]
+    L.spdp_spmm.argtypes = [H, ctypes.c_void_p, i64, ctypes.c_void_p, ctypes.c_void_p]
     L.spdp_spmspv_many.argtypes = [ctypes.POINTER(H), i32, ctypes.POINTER(ctypes.c_void_p), i32,
                                    ctypes.POINTER(ctypes.c_float), ctypes.POINTER(ctypes.c_void_p),
                                    ctypes.c_void_p]
@@ -124,7 +125,8 @@ def lib() -> ctypes.CDLL:
     L.spdp_strerror.restype = ctypes.c_char_p
     L.spdp_last_error.argtypes = []
     L.spdp_last_error.restype = ctypes.c_char_p
-    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_noalloc", "spdp_spmspv_many",
+    for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_noalloc", "spdp_spmm",
+                 "spdp_spmspv_many",
                  "spdp_spmspv_many_mask",
                  "spdp_reserve",
                  "spdp_format",
@@ -250,6 +252,30 @@ class Matrix:
         _check(lib().spdp_spmspv_noalloc(self._h, ctypes.c_void_p(x.data_ptr()), int(b),
                                          ctypes.c_float(threshold), ctypes.c_void_p(y.data_ptr()),
                                          ctypes.c_void_p(s.cuda_stream)))
+
+    def spmm_into(self, x, y, stream=None) -> None:
+        """Enqueue the prefill product ``y = x W_sp^T`` (every column, no
+        threshold) for ``x`` [tokens, cols] into ``y`` [tokens, rows]."""
+        import torch
+        if x.dtype != torch.float16 or y.dtype != torch.float16:
+            raise TypeError("x and y must be torch.float16")
+        if x.dim() != 2 or x.shape[1] != self.cols or not x.is_contiguous():
+            raise ValueError(f"x must be a contiguous [tokens, {self.cols}] tensor")
+        n = x.shape[0]
+        if tuple(y.shape) != (n, self.rows) or not y.is_contiguous():
+            raise ValueError(f"y must be a contiguous [{n}, {self.rows}] tensor")
+        if not (x.is_cuda and y.is_cuda):
+            raise ValueError("x and y must be device tensors")
+        s = stream if stream is not None else torch.cuda.current_stream(x.device)
+        _check(lib().spdp_spmm(self._h, ctypes.c_void_p(x.data_ptr()), int(n), ctypes.c_void_p(y.data_ptr()),
+                               ctypes.c_void_p(s.cuda_stream)))
+
+    def spmm(self, x, stream=None):
+        """The prefill product ``x W_sp^T`` as a new fp16 tensor."""
+        import torch
+        y = torch.empty((x.shape[0], self.rows), dtype=torch.float16, device=x.device)
+        self.spmm_into(x, y, stream)
+        return y
 
     def __call__(self, x, threshold: float, stream=None, mask: str = "token"):
         import torch

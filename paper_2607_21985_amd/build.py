@@ -43,6 +43,8 @@ def build(verbose: bool = False) -> str:
                                        "-o", os.path.join(objdir, "host.o")]),
         ([cc] + common + device + ["-c", os.path.join(CSRC, "spdp.hip"),
                                    "-o", os.path.join(objdir, "spdp.o")]),
+        ([cc] + common + device + ["-c", os.path.join(CSRC, "spmm.hip"),
+                                   "-o", os.path.join(objdir, "spmm.o")]),
     ]
     for cmd in jobs:
         if verbose:
@@ -56,7 +58,8 @@ def build(verbose: bool = False) -> str:
             print(out, flush=True)
     tmp = LIB + ".tmp"
     link = [cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp,
-            os.path.join(objdir, "host.o"), os.path.join(objdir, "spdp.o"), "-lpthread"]
+            os.path.join(objdir, "host.o"), os.path.join(objdir, "spdp.o"), os.path.join(objdir, "spmm.o"),
+            "-lpthread"]
     res = subprocess.run(link, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(link)}\n{res.stdout}{res.stderr}")

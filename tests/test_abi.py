@@ -68,6 +68,7 @@ def test_null_and_size_errors():
     assert L.spdp_reserve(None, 1) == ERR_INVALID
     assert L.spdp_spmspv(None, None, 1, ctypes.c_float(0.0), None, None) == ERR_INVALID
     assert L.spdp_spmspv_noalloc(None, None, 1, ctypes.c_float(0.0), None, None) == ERR_INVALID
+    assert L.spdp_spmm(None, None, 1, None, None) == ERR_INVALID
     L.spdp_free(None)  # no-op
     out = np.empty(16, dtype=np.uint16)
     assert L.spdp_prune_magnitude(None, 16, ctypes.c_double(0.5), ctypes.c_void_p(out.ctypes.data)) == ERR_INVALID
@@ -86,6 +87,8 @@ def test_spmspv_on_host_only_handle_is_rejected():
     assert b"device" in L.spdp_last_error()
     st = L.spdp_spmspv_noalloc(m._h, ctypes.c_void_p(x.ctypes.data), 1, ctypes.c_float(0.0),
                                ctypes.c_void_p(x.ctypes.data + 64), None)
+    assert st == ERR_INVALID
+    st = L.spdp_spmm(m._h, ctypes.c_void_p(x.ctypes.data), 1, ctypes.c_void_p(x.ctypes.data + 64), None)
     assert st == ERR_INVALID
     assert b"device" in L.spdp_last_error()
     assert L.spdp_reserve(m._h, 4) == ERR_INVALID
