@@ -26,6 +26,9 @@ values (2 B x pad8(nnz)); + 4 B per touched GTile (TileOffset); + x and y.
 decoder layer (seven calls chained) at batch 1/4/16; and a slice of the
 Llama-70B layer sweep.
 
+``prefill`` times the prefill product (spdp_spmm, Sec. 4.3) on Llama shapes
+at prompt lengths against the dense fp16 matrix peak and F.linear.
+
 ``--summarize-profiles DIR`` turns rocprofv3 outputs written under DIR by the
 commands it prints into the summaries under profiles/ (no GPU needed).
 
@@ -75,6 +78,7 @@ def parse(argv=None):
     ap.add_argument("--no-secondary", action="store_true",
                     help="skip the other workloads (single layer, 7B MLP, 13B layer, 70B slice)")
     ap.add_argument("--secondary-steps", type=int, default=12)
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefill products (spdp_spmm)")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed steps only (for rocprofv3 runs)")
     ap.add_argument("--calib-read-mib", type=int, default=0,
@@ -736,6 +740,73 @@ def secondary(B, args):
     return out
 
 
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X published dense fp16 matrix peak
+
+# prefill products (Sec. 4.3): (workload, projection, sw, tokens)
+PREFILL = [
+    ("llama7b-attn", "q", 0.5, 512),
+    ("llama7b-attn", "q", 0.5, 2048),
+    ("llama7b-mlp", "gate", 0.6, 2048),
+    ("llama7b-mlp", "down", 0.6, 2048),
+    ("llama70b-layer", "gate", 0.7, 1024),
+]
+
+
+def prefill(B, args, steps=10):
+    """The prefill product spdp_spmm on Llama shapes at prompt lengths:
+    MFMA work executed (every 256 x 16 tile expanded, the token count
+    rounded up to the 128-token tile) against the dense fp16 matrix peak,
+    useful flops (2 x nonzeros x tokens), and the dense fp16 F.linear on the
+    same shapes. Two encoded copies alternate so that consecutive calls read
+    different weights."""
+    import torch.nn.functional as F
+    torch, spdp, synth = B.torch, B.spdp, B.synth
+    out = []
+    for name, pname, sw, n in PREFILL:
+        proj = next(p for p in synth.workload(name)["projections"] if p.name == pname)
+        w16 = B.dense_weight(proj)
+        w = spdp.prune_magnitude(w16, sw)
+        mats = [spdp.encode(w, (256, 16)) for _ in range(2)]
+        X = B.to_dev(proj.activations(n, draw=2))
+        Ys = [torch.empty((n, proj.rows), dtype=torch.float16, device=B.dev) for _ in range(2)]
+        for i in range(2):
+            mats[i].spmm_into(X, Ys[i])
+        B.sync()
+        g = B.capture(lambda: [mats[i % 2].spmm_into(X, Ys[i % 2]) for i in range(steps)])
+        g.replay()
+        B.sync()
+        ms = B.timed(lambda _: g.replay(), 3) / (3 * steps)
+        del g
+        Wd = [B.to_dev(w16) for _ in range(2)]
+        gd = B.capture(lambda: [F.linear(X, Wd[i % 2]) for i in range(steps)])
+        gd.replay()
+        B.sync()
+        dms = B.timed(lambda _: gd.replay(), 3) / (3 * steps)
+        del gd, Wd
+        f = mats[0].format()
+        nnz = int(((f["col_info"] & 0xFFFF).astype(np.int64)).sum())
+        executed = 2.0 * f["n_stripes"] * 256 * f["n_colblocks"] * 16 * (-(-n // 128) * 128)
+        useful = 2.0 * nnz * n
+        dense_fl = 2.0 * proj.rows * proj.cols * n
+        e = {"workload": name, "projection": f"{pname} {proj.rows}x{proj.cols}", "sw": sw, "tokens": n,
+             "us_per_call": round(ms * 1e3, 3),
+             "mfma_tflops": round(executed / (ms * 1e-3) / 1e12, 1),
+             "useful_tflops": round(useful / (ms * 1e-3) / 1e12, 1),
+             "roofline": {"bound": "mfma", "achieved": round(executed / (ms * 1e-3) / 1e12, 1),
+                          "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                          "frac": round(executed / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)},
+             "dense_us_per_call": round(dms * 1e3, 3),
+             "dense_tflops": round(dense_fl / (dms * 1e-3) / 1e12, 1),
+             "speedup_vs_dense": round(dms / ms, 3)}
+        print(f"[bench] prefill {json.dumps(e)}", file=sys.stderr, flush=True)
+        out.append(e)
+        for m in mats:
+            m.close()
+        del X, Ys
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.summarize_profiles:
@@ -823,6 +894,7 @@ def main():
         pts_out.append(d)
 
     sec = None if args.no_secondary else secondary(B, args)
+    pre = None if args.no_prefill else prefill(B, args)
     cpu = None if args.no_cpu_baseline else cpu_baseline(points, args.mask, rtn_bits=args.rtn_bits)
     traffic = None if args.rtn_bits else read_traffic(args.workload, args.group)
     us_per_call = ms_per_step * 1e3 / len(points)
@@ -891,6 +963,7 @@ def main():
         "speedup_vs_dense": round(dense["us_per_call"] / us_per_call, 3) if dense else None,
         "points": pts_out,
         "secondary": sec,
+        "prefill": pre,
         "prep_s": round(prep_s, 2),
         "encode_s_per_matrix": round(enc_s, 4),
         "host": platform.node(),

@@ -179,6 +179,226 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// The pipelined form for 256 x 16 GTiles and a width that is a multiple of
+// 8 (every Llama shape): each k-step is one GTile, and everything a step
+// reads from memory -- the GTile's padded values (one contiguous run), its
+// 16 columns' bitmap words and ColInfo, and the 128 x 16 block of X -- is
+// copied into a ring of kRing LDS slots by global->LDS DMA, kRing steps
+// ahead, so that no wave waits on memory for the decode. Per wave and step:
+// two 16-byte DMA loads of values (the GTile's values in 16-byte chunks over
+// 4 waves x 2 loads x 64 lanes; lanes past the end re-read the last chunk),
+// one 4-byte DMA load of bitmap words or ColInfo, one 16-byte DMA load of
+// its own 32 tokens of X: four loads, so "step s has landed" is "at most
+// 4 x (later steps requested) loads outstanding". Step s: the MFMAs of step
+// s (dense tile s & 1, B operand from the wave's own X rows of slot s), then
+// the DMA of step s + kRing into slot s (its values, bitmaps and ColInfo
+// were decoded in step s - 1, its X rows were just read), then the decode of
+// step s + 1 into dense tile (s + 1) & 1 while the MFMAs run, then one
+// barrier.
+
+constexpr int kRing = 4;
+constexpr int kMetaBytes = 1024;               // bitmaps (512 B), ColInfo (64 B), DMA spill
+constexpr int kValBytes = kTM * kKStep * 2;    // a dense GTile's worth of values
+constexpr int kXBytes = kBN * kKStep * 2;      // 128 tokens x 16 columns
+constexpr int kSlotBytes = kMetaBytes + kValBytes + kXBytes;
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// Global -> LDS DMA (lane l's bytes land at lds + 16 l, or + 4 l). Issued as
+// assembly so that the compiler does not order LDS reads of other ring
+// slots behind every outstanding load; the waits are explicit. The compiler
+// does not look inside assembly for hazards: a vector memory instruction
+// needs 5 wait states after a VALU write of an SGPR it reads, hence s_nop 4.
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+__device__ __forceinline__ void dma4(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_nop 4\n\tglobal_load_lds_dword %0, %1" ::"v"(off), "s"(base), "{m0}"(lds) : "memory");
+}
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+constexpr int kDmaPerStep = 4;
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void spmm_ring_kernel(SpmmArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRing][kSlotBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char tile[2][kTileBytes];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = blockIdx.x;
+  const long long nb0 = (long long)blockIdx.y * kBN;
+  const int khalf = (lane >> 5) * 8;
+  const int steps = a.steps;
+  const const_ptr<uint32_t> to_s = (const_ptr<uint32_t>)a.tile_offset;
+  const uint32_t g0 = (uint32_t)r * (uint32_t)a.n_colblocks;
+  // this workgroup's 128 tokens of X (tokens past the end re-read the last)
+  const uint16_t* const xblk = a.x + nb0 * (long long)a.cols;
+  const long long left = a.n_tokens - nb0;
+  // X DMA: lane l of wave w brings token 32w + l / 2, columns 8 (l & 1) ..
+  // + 8 of the step, to byte 1024 w + 16 l of the slot's X block
+  const int xt = 32 * wave + (lane >> 1);
+  const uint32_t x_row = (uint32_t)((xt < left ? xt : left - 1) * (long long)a.cols * 2);
+
+  auto issue = [&](int s) __attribute__((always_inline)) {
+    unsigned char* slot = ring[s % kRing];
+    const uint32_t g = g0 + (uint32_t)s;
+    const uint32_t t0 = to_s[g], t1 = to_s[g + 1];
+    const uint32_t last = t1 > t0 ? (t1 - t0) / 8u - 1u : 0u;  // last 16-byte chunk of the values
+    const uint32_t vbase = lds_addr(slot + kMetaBytes);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t q = (uint32_t)((i * kWaves + wave) * 64 + lane);
+      dma16(a.values, 2u * t0 + 16u * (q < last ? q : last),
+            (uint32_t)__builtin_amdgcn_readfirstlane((int)(vbase + (uint32_t)(i * kWaves + wave) * 1024u)));
+    }
+    // waves 0, 1: the 16 columns' bitmap words (512 bytes); wave 2 the
+    // ColInfo (64 bytes; its other lanes re-read it); wave 3 re-reads it too
+    const uint32_t mbase = lds_addr(slot) + 256u * (uint32_t)wave;
+    if (wave < 2)
+      dma4(a.bitmap, g * 512u + 256u * (uint32_t)wave + 4u * (uint32_t)lane,
+           (uint32_t)__builtin_amdgcn_readfirstlane((int)mbase));
+    else
+      dma4(a.col_info, g * 64u + 4u * (uint32_t)(lane & 15), (uint32_t)__builtin_amdgcn_readfirstlane((int)mbase));
+    const uint32_t xk = (uint32_t)(s * kKStep + 8 * (lane & 1));
+    // columns past the width: any valid 16 bytes (the weights there are 0;
+    // the B operand is cleared after the read)
+    const uint32_t xoff = x_row + 2u * (xk < (uint32_t)a.cols ? xk : 0u);
+    dma16(xblk, xoff, (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_addr(slot + kMetaBytes + kValBytes + 1024 * wave)));
+  };
+  // "step s landed": at most kDmaPerStep x (steps requested after s) loads
+  // in flight, the count being min(kRing - 1, steps - 1 - s) in the steady state
+  auto wait_landed = [&](int later) __attribute__((always_inline)) {
+    if (later >= 3)
+      wait_vmcnt<3 * kDmaPerStep>();
+    else if (later == 2)
+      wait_vmcnt<2 * kDmaPerStep>();
+    else if (later == 1)
+      wait_vmcnt<kDmaPerStep>();
+    else
+      wait_vmcnt<0>();
+  };
+  static_assert(kRing == 4, "wait_landed counts up to three later steps");
+  // decode of step s (slot s % kRing) into dense tile `t`: wave w expands
+  // columns 4w .. 4w + 3, lane i of word v giving row 64 v + i. ColInfo and
+  // the bitmap words come from scalar loads (the step's DMA has brought
+  // their lines into L2) straight into scalar registers, where they serve as
+  // mbcnt masks and as the select mask of the lanes' values; the values come
+  // from the slot.
+  const const_ptr<uint32_t> ci_s = (const_ptr<uint32_t>)a.col_info;
+  const const_ptr<uint64_t> bm_s = (const_ptr<uint64_t>)a.bitmap;
+  struct Meta {
+    uint32_t ci[4];
+    uint64_t words[4][4];
+  };
+  // requested one step ahead of its decode, so that the scalar loads' round
+  // trip overlaps the previous step's work
+  auto meta_of = [&](int s, Meta& m) __attribute__((always_inline)) {
+    const uint32_t col0 = (g0 + (uint32_t)s) * (uint32_t)kKStep + 4u * (uint32_t)wave;
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      m.ci[jj] = ci_s[col0 + jj];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) m.words[jj][v] = bm_s[(size_t)(col0 + jj) * 4 + v];
+    }
+  };
+  auto decode = [&](int s, const Meta& m, unsigned char* t) __attribute__((always_inline)) {
+    const unsigned char* slot = ring[s % kRing];
+    const uint32_t (&ci)[4] = m.ci;
+    const uint64_t (&words)[4][4] = m.words;
+    const uint32_t vb = lds_addr(slot + kMetaBytes);
+    uint32_t h[4][4];
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      uint32_t base = vb + 2u * (ci[jj] >> 16);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint64_t word = words[jj][v];
+        const uint32_t hv =
+            *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(base + 2u * mbcnt64(word));
+        // the lane's value where its bit is set, else 0 (the word as the select mask)
+        uint32_t sel;
+        asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(sel) : "v"(hv), "s"(word));
+        h[v][jj] = sel;
+        base += 2u * (uint32_t)__builtin_popcountll(word);
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      *reinterpret_cast<uint2*>(t + (64 * v + lane) * kRowBytes + 8 * wave) =
+          make_uint2(h[v][0] | (h[v][1] << 16), h[v][2] | (h[v][3] << 16));
+  };
+
+  float16v acc[kBlocks];
+#pragma unroll
+  for (int i = 0; i < kBlocks; ++i) acc[i] = float16v{};
+
+  // prologue: the first kRing steps requested, step 0 decoded, step 1 landed
+  for (int s = 0; s < kRing && s < steps; ++s) issue(s);
+  Meta meta;
+  meta_of(0, meta);
+  wait_landed(min(kRing - 1, steps - 1));
+  __syncthreads();
+  decode(0, meta, tile[0]);
+  if (steps > 1) meta_of(1, meta);
+  wait_landed(min(kRing - 2, steps - 2));
+  __syncthreads();
+
+  for (int s = 0; s < steps; ++s) {
+    unsigned char* slot = ring[s % kRing];
+    const unsigned char* t = tile[s & 1];
+    // B operand: this wave's 32 tokens, 8 columns, from its own X rows
+    half8 b = *reinterpret_cast<const half8*>(slot + kMetaBytes + kValBytes +
+                                              (32 * wave + (lane & 31)) * 32 + 2 * khalf);
+    if (s * kKStep + khalf >= a.cols) b = half8{0, 0, 0, 0, 0, 0, 0, 0};
+    half8 av[kBlocks];
+#pragma unroll
+    for (int i = 0; i < kBlocks; ++i) {
+      const unsigned char* p = t + (32 * i + (lane & 31)) * kRowBytes + 2 * khalf;
+      const uint2 lo = *reinterpret_cast<const uint2*>(p);
+      const uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
+      av[i] = __builtin_bit_cast(half8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+    }
+#pragma unroll
+    for (int i = 0; i < kBlocks; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], b, acc[i], 0, 0, 0);
+    // the slot's X rows have been read (the operands are in registers); its
+    // values and metadata were decoded before the last barrier
+    if (s + kRing < steps) issue(s + kRing);
+    if (s + 1 < steps) decode(s + 1, meta, tile[(s + 1) & 1]);
+    // step s + 2 (decoded in the next iteration) has landed: the steps
+    // requested after it are s + 3 .. min(s + kRing, steps - 1)
+    if (s + 2 < steps) {
+      wait_landed(min(kRing - 2, steps - 1 - (s + 2)));
+      meta_of(s + 2, meta);
+    }
+    __syncthreads();
+  }
+
+  const long long n = nb0 + 32 * wave + (lane & 31);
+  if (n >= a.n_tokens) return;
+  uint16_t* const yrow = a.y + n * (long long)a.rows;
+#pragma unroll
+  for (int i = 0; i < kBlocks; ++i) {
+#pragma unroll
+    for (int grp = 0; grp < 4; ++grp) {
+      const int m = r * kTM + 32 * i + 8 * grp + 4 * (lane >> 5);
+      uint16_t hh[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hh[e] = __half_as_ushort(__float2half_rn(acc[i][4 * grp + e]));
+      if (a.y_vec && m + 3 < a.rows) {
+        *reinterpret_cast<uint2*>(yrow + m) =
+            make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (m + e < a.rows) yrow[m + e] = hh[e];
+      }
+    }
+  }
+}
+
 int hip_fail(hipError_t e, const char* what) {
   return spdp::fail(SPDP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
 }
@@ -225,7 +445,11 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
   a.x_vec = h->cols % 8 == 0;
   a.y_vec = h->rows % 4 == 0;
   const dim3 grid((unsigned)h->n_stripes, (unsigned)((n_tokens + kBN - 1) / kBN));
-  hipLaunchKernelGGL(spmm_kernel, grid, dim3(kWaves * 64), 0, static_cast<hipStream_t>(stream), a);
+  // the pipelined form for 256 x 16 GTiles and 16-byte X rows; the plain one otherwise
+  if (h->tile_k == kKStep && a.x_vec)
+    hipLaunchKernelGGL(spmm_ring_kernel, grid, dim3(kWaves * 64), 0, static_cast<hipStream_t>(stream), a);
+  else
+    hipLaunchKernelGGL(spmm_kernel, grid, dim3(kWaves * 64), 0, static_cast<hipStream_t>(stream), a);
   e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
