@@ -299,14 +299,24 @@ __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
+typedef float float16_t __attribute__((ext_vector_type(16)));
+// MFMA form: a wave's dense tile of decoded weights, one row per matrix row
+// of the stripe, 8 columns (two batches) per row, padded to 24 bytes
+constexpr int kMRowBytes = 24;
+
 // NB: tokens per call rounded up to a power of two; WPC: bitmap words per
 // column (tile_m / 64); Q: Values are one-byte round-to-nearest codes with a
-// scale per row (else fp16).
-template <int NB, int WPC, bool EARLY, bool BMASK, bool Q>
-__global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
+// scale per row (else fp16); MM: accumulate on the matrix cores (8 or more
+// tokens: the product of a batch of 8 active columns with up to 32 tokens
+// is a small dense contraction; see step 4).
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MM>
+__device__ __forceinline__ void spmspv_body() {
+  static_assert(!MM || (NB >= 8 && !Q && !EARLY), "the MFMA form serves 8 or more tokens of fp16 values");
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[S::kRingBytes];
+  __shared__ __attribute__((aligned(16))) unsigned char mt_s[MM ? kWaves * 64 * WPC * kMRowBytes : 16];
   // the workgroup's active columns in activity order: {byte offset of the
   // column's values, the column's bitmap offset and the index of its
   // last 16-byte chunk}; padded to a whole batch with entries that load
@@ -355,6 +365,12 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   for (int w = 0; w < WPC; ++w)
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
+  // MFMA form: the stripe's 32-row blocks x 32 tokens (tokens past the
+  // batch stay 0), in the 32x32 accumulator layout
+  constexpr int kMBlocks = 2 * WPC;
+  float16_t macc[MM ? kMBlocks : 1];
+#pragma unroll
+  for (int i = 0; i < (MM ? kMBlocks : 1); ++i) macc[i] = float16_t{};
 
   const int k_begin = (seg * kWaves + wave) * wave_cols;
   const int range = max(0, min(wave_cols, cols - k_begin));
@@ -556,7 +572,7 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
       for (int w = 0; w < WPC; ++w) m[c][w] = bp[w];
     }
   };
-  auto decode_quad = [&](const unsigned char* slot, int e0, int u0, const uint64_t (&m)[kQuad][WPC])
+  auto decode_quad = [&](const unsigned char* slot, int e0, int u0, const uint64_t (&m)[kQuad][WPC], int half)
       __attribute__((always_inline)) {
     // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
     // below the lane plus the popcounts of the column's earlier words (every
@@ -596,7 +612,19 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     // per column word) and one dot product per token (v_dot2_f32_f16 against
     // the pair's two activations) adds both columns: 1 + NB/2 instructions
     // per word instead of NB, fewer from four tokens on.
-    if constexpr (NB == 2) {
+    if constexpr (MM) {
+      // 4 (MFMA form). The batch's four columns, zero where the bit is
+      // clear, into the wave's dense tile: row 64 w + lane, columns 4 h ..
+      // 4 h + 3 for batch parity h (one 8-byte store per word); the
+      // multiply runs once per two batches (below).
+      unsigned char* mt = mt_s + wave * (64 * WPC * kMRowBytes);
+#pragma unroll
+      for (int w = 0; w < WPC; ++w) {
+        const uint32_t p01 = pair_under_words(vb[0][w], vb[1][w], m[0][w], m[1][w]);
+        const uint32_t p23 = pair_under_words(vb[2][w], vb[3][w], m[2][w], m[3][w]);
+        *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8 * half) = make_uint2(p01, p23);
+      }
+    } else if constexpr (NB == 2) {
 #pragma unroll
       for (int pr = 0; pr < 2; ++pr) {
         // the pair's dwords of tokens 0 and 1 (low half column 2pr)
@@ -665,7 +693,37 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
     else
       wait_vmcnt<0>();
     if (!kAhead) masks_of(i);
-    decode_quad(my_ring + (i % kSlots) * kBatchBytes, entry0(i), 0, m);
+    decode_quad(my_ring + (i % kSlots) * kBatchBytes, entry0(i), 0, m, i & 1);
+    if constexpr (MM) {
+      // every second batch (and the last): the step's 8 columns (entries
+      // e .. e + 7) times the 32 tokens: per 32-row block one
+      // v_mfma_f32_32x32x8_f16, A = the tile's rows (lane l: row l mod 32,
+      // columns 4 (l / 32) .. + 4), B = the columns' masked activations
+      // (lane l: token l mod 32, the same 4 columns; 0 for tokens past NB)
+      if ((i & 1) || i + 1 == n_mine) {
+        unsigned char* mt = mt_s + wave * (64 * WPC * kMRowBytes);
+        const int hl = lane >> 5;
+        if (!(i & 1)) {
+          // a single batch: the tile's second half is cleared (its columns
+          // are the next wave's, and stale weights must not meet 0)
+#pragma unroll
+          for (int w = 0; w < WPC; ++w) *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8) = make_uint2(0u, 0u);
+        }
+        const int e = entry0(i - (i & 1));
+        const int t = lane & 31;
+        uint2 bx = make_uint2(0u, 0u);
+        if (t < NB && (hl == 0 || (i & 1))) {
+          const uint32_t* xp = reinterpret_cast<const uint32_t*>(xs_s);
+          bx = make_uint2(xp[(e / 2 + 2 * hl) * NB + t], xp[(e / 2 + 2 * hl + 1) * NB + t]);
+        }
+        const half4_t bop = __builtin_bit_cast(half4_t, bx);
+#pragma unroll
+        for (int blk = 0; blk < kMBlocks; ++blk) {
+          const uint2 av = *reinterpret_cast<const uint2*>(mt + (32 * blk + t) * kMRowBytes + 8 * hl);
+          macc[blk] = __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(half4_t, av), bop, macc[blk], 0, 0, 0);
+        }
+      }
+    }
     if (i + kSlots < n_mine) {
       // the slot's LDS reads have completed (their results were consumed)
       issue(i + kSlots);
@@ -682,11 +740,38 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   const int nb = batch;
   const int row = threadIdx.x;
   float* red = reinterpret_cast<float*>(ring);
+  static_assert(!MM || kWaves * 32 * 32 * 4 <= S::kRingBytes, "the MFMA form's reduction reuses the ring");
   constexpr int kSlice = Smem<NB>::kSlice;
   unsigned long long* dst = ka->partials + (size_t)seg * nb * mpad + (size_t)r * ka->tile_m + row;
   const unsigned long long tag = (unsigned long long)phase << 32;
+  if constexpr (MM) {
+    // per 32-row block: each wave's 32 x 32 accumulators to LDS as
+    // [wave][token][row], then thread (row, 4 tokens) adds the waves in
+    // order 0..3 and publishes (consecutive threads, consecutive rows)
+    const int prow = threadIdx.x & 31;
+    const int ptg = threadIdx.x >> 5;
 #pragma unroll
-  for (int b0 = 0; b0 < NB; b0 += kSlice) {
+    for (int blk = 0; blk < kMBlocks; ++blk) {
+      __syncthreads();
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        red[(wave * 32 + (lane & 31)) * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)] = macc[blk][e];
+      __syncthreads();
+#pragma unroll
+      for (int bb = 0; bb < 4; ++bb) {
+        const int b = 4 * ptg + bb;
+        if (b < nb) {
+          float sum = 0.0f;
+#pragma unroll
+          for (int wv = 0; wv < kWaves; ++wv) sum += red[(wv * 32 + b) * 32 + prow];
+          __hip_atomic_store(dst - row + 32 * blk + prow + (size_t)b * mpad, tag | __float_as_uint(sum),
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int b0 = 0; b0 < (MM ? 0 : NB); b0 += kSlice) {
     __syncthreads();
 #pragma unroll
     for (int w = 0; w < WPC; ++w)
@@ -820,6 +905,17 @@ __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
   }
 }
 
+// The kernels: the vector-ALU forms, and the matrix-core form, whose 32 x 32
+// accumulator blocks live in AGPRs; two waves per SIMD are asked of it.
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q>
+__global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
+  spmspv_body<NB, WPC, EARLY, BMASK, Q, false>();
+}
+template <int NB, int WPC, bool BMASK>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void spmspv_mm_kernel(LaunchArgs) {
+  spmspv_body<NB, WPC, false, BMASK, false, true>();
+}
+
 using spdp::fail;
 
 int hip_fail(hipError_t e, const char* what) {
@@ -944,17 +1040,27 @@ int upload(const std::vector<T>& v, void** dst) {
 }
 
 template <int NB, int WPC, bool Q>
-hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, dim3 grid, hipStream_t stream) {
+hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, dim3 grid, hipStream_t stream) {
   // the one-token kernel has the early-first-batch form (no product with
   // more tokens asks for it); the kernels for more tokens have the shared
   // batch mask form (at one token the two masks are the same rule, and the
-  // host sends such calls to the per-token kernel)
+  // host sends such calls to the per-token kernel); from 8 tokens on, fp16
+  // values accumulate on the matrix cores unless mm is false
   if constexpr (NB == 1) {
     if (early) {
       hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   } else {
+    if constexpr (NB >= 8 && !Q) {
+      if (mm) {
+        if (bmask)
+          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, true>), grid, dim3(kThreads), 0, stream, args);
+        else
+          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, false>), grid, dim3(kThreads), 0, stream, args);
+        return hipGetLastError();
+      }
+    }
     if (bmask) {
       hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
@@ -965,19 +1071,32 @@ hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, dim3 grid
 }
 
 template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool q, dim3 grid, hipStream_t stream) {
-  return q ? launch_form<NB, WPC, true>(args, early, bmask, grid, stream)
-           : launch_form<NB, WPC, false>(args, early, bmask, grid, stream);
+hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool mm, bool q, dim3 grid, hipStream_t stream) {
+  return q ? launch_form<NB, WPC, true>(args, early, bmask, mm, grid, stream)
+           : launch_form<NB, WPC, false>(args, early, bmask, mm, grid, stream);
 }
 
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool q, dim3 grid, hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool mm, bool q, dim3 grid,
+                  hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, early, bmask, q, grid, stream);
-    case 2: return launch_one<NB, 2>(args, early, bmask, q, grid, stream);
-    case 3: return launch_one<NB, 3>(args, early, bmask, q, grid, stream);
-    default: return launch_one<NB, 4>(args, early, bmask, q, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, bmask, mm, q, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, bmask, mm, q, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, bmask, mm, q, grid, stream);
+    default: return launch_one<NB, 4>(args, early, bmask, mm, q, grid, stream);
   }
+}
+
+// The matrix-core accumulate pays above 16 tokens: measured on the Llama-70B
+// layer at 32 tokens 115 against 142 us per product (70/50 and 50/0), while
+// at 8 and 16 tokens the vector-ALU form (NB / 2 dot products per 64-row
+// word) is faster (56 against 90 us at 8 tokens, 39 against 53 at 16).
+// SPDP_MFMA=0 or 1 overrides from 5 tokens on (for tuning). A property of
+// the batch only, so a product gives the same bits alone and grouped.
+bool use_mfma(int batch) {
+  if (batch < 5) return false;
+  if (const char* env = std::getenv("SPDP_MFMA")) return std::atoi(env) != 0;
+  return batch > 16;
 }
 
 // Early first batches (each wave requests its own first four active columns
@@ -1179,18 +1298,19 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
   const dim3 grid((unsigned)widest, (unsigned)count);
   const bool q = handles[0]->value_bits < 16;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const bool mm = use_mfma(batch);
   if (batch <= 1)
-    e = launch<1>(la, wpc, early, bmask, q, grid, s);
+    e = launch<1>(la, wpc, early, bmask, mm, q, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, early, bmask, q, grid, s);
+    e = launch<2>(la, wpc, early, bmask, mm, q, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, early, bmask, q, grid, s);
+    e = launch<4>(la, wpc, early, bmask, mm, q, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, early, bmask, q, grid, s);
+    e = launch<8>(la, wpc, early, bmask, mm, q, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, early, bmask, q, grid, s);
+    e = launch<16>(la, wpc, early, bmask, mm, q, grid, s);
   else
-    e = launch<32>(la, wpc, early, bmask, q, grid, s);
+    e = launch<32>(la, wpc, early, bmask, mm, q, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }
