@@ -116,6 +116,8 @@ struct MatArgs {
   // is active iff the fp32 running sum of |x[b, k]| over the tokens exceeds
   // batch_thr = fp32(batch * t), every token's activation kept there
   float batch_thr;
+  // consecutive K ranges (of kWaves x wave_cols columns) per workgroup
+  int passes;
 };
 
 // A launch runs up to kMaxGroup independent products (same tile height and
@@ -372,363 +374,377 @@ __device__ __forceinline__ void spmspv_body() {
 #pragma unroll
   for (int i = 0; i < (MM ? kMBlocks : 1); ++i) macc[i] = float16_t{};
 
-  const int k_begin = (seg * kWaves + wave) * wave_cols;
-  const int range = max(0, min(wave_cols, cols - k_begin));
+  // The workgroup walks `passes` consecutive K ranges (one unless the batch
+  // is large: fewer segments then mean fewer split-K partials, whose bytes
+  // grow with the batch), accumulating into the same registers; each pass
+  // tests its range, builds its list and streams it. The stripe's phase is
+  // read in the first pass.
+  const int passes = MM ? A->passes : 1;  // the vector-ALU forms walk one range
+  uint32_t phase = 0;
+  for (int pass = 0; pass < passes; ++pass) {
+    if (pass > 0) __syncthreads();  // the last pass's list, activations and ring are free
+    const int k_begin = ((seg * passes + pass) * kWaves + wave) * wave_cols;
+    const int range = max(0, min(wave_cols, cols - k_begin));
 
-  // ---- 1. each wave's K range: activations and column metadata in one round
-  // trip (ColInfo/TileOffset are fetched for every column of the range, which
-  // removes a dependent memory round trip; their cache lines are shared by
-  // neighbouring columns, so little extra traffic results).
-  // All loads are unconditional so that they leave back to back and are
-  // waited for once: lanes past the range (and waves past the last column)
-  // read column k_begin's or column 0's entries, tokens past the batch read
-  // the last token; none of those is used below.
-  constexpr int kChunks = kMaxWaveCols / 64;
-  uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
-  const int k_safe = k_begin < cols ? k_begin : 0;
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const int off = 64 * c + lane;
-    const int k = off < range ? k_begin + off : k_safe;
-    const int g = g_row + (k >> tk_log2);
-    colx[c] = ((uint32_t)g << tk_log2) + (uint32_t)(k & tk_mask);
-    ci[c] = col_info_p[colx[c]];
-    to[c] = tile_offset_p[g];
-#pragma unroll
-    for (int b = 0; b < NB; ++b) xb[c][b] = x_p[(size_t)min(b, batch - 1) * cols + k];
-  }
-  // the stripe's phase: written by the previous call's last segment, read
-  // by every workgroup of the stripe before any of them publishes (the
-  // kernel boundary makes the write visible, so an ordinary cached load
-  // serves). A vector load issued after the loads above, so that waiting for
-  // them does not wait for it (loads return in order), waited for after the
-  // list is built; a scalar load would share the LDS wait counter, and the
-  // compiler would wait for it at the first LDS barrier.
-  const uint32_t phase_lane =
-      __hip_atomic_load(phase_p + r * A->phase_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-  // activity: the union of the tokens' sets, or the batch's shared set
-  uint64_t actm[kChunks];
-  int n_w = 0;
-#pragma unroll
-  for (int c = 0; c < kChunks; ++c) {
-    const bool in = 64 * c + lane < range;
-    uint64_t act = 0;
-    if constexpr (BMASK) {
-      // fp32 running sum of |x| over the tokens in ascending order (NaN
-      // makes it NaN, never active)
-      float score = 0.0f;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-        if (b < batch) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
-      act = __builtin_amdgcn_ballot_w64(in && score > batch_thr);
-    } else {
-#pragma unroll
+    // ---- 1. each wave's K range: activations and column metadata in one round
+    // trip (ColInfo/TileOffset are fetched for every column of the range, which
+    // removes a dependent memory round trip; their cache lines are shared by
+    // neighbouring columns, so little extra traffic results).
+    // All loads are unconditional so that they leave back to back and are
+    // waited for once: lanes past the range (and waves past the last column)
+    // read column k_begin's or column 0's entries, tokens past the batch read
+    // the last token; none of those is used below.
+    constexpr int kChunks = kMaxWaveCols / 64;
+    uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
+    const int k_safe = k_begin < cols ? k_begin : 0;
+  #pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const int off = 64 * c + lane;
+      const int k = off < range ? k_begin + off : k_safe;
+      const int g = g_row + (k >> tk_log2);
+      colx[c] = ((uint32_t)g << tk_log2) + (uint32_t)(k & tk_mask);
+      ci[c] = col_info_p[colx[c]];
+      to[c] = tile_offset_p[g];
+  #pragma unroll
+      for (int b = 0; b < NB; ++b) xb[c][b] = x_p[(size_t)min(b, batch - 1) * cols + k];
+    }
+    // the stripe's phase: written by the previous call's last segment, read
+    // by every workgroup of the stripe before any of them publishes (the
+    // kernel boundary makes the write visible, so an ordinary cached load
+    // serves). A vector load issued after the loads above, so that waiting for
+    // them does not wait for it (loads return in order), waited for after the
+    // list is built; a scalar load would share the LDS wait counter, and the
+    // compiler would wait for it at the first LDS barrier.
+    uint32_t phase_lane = 0;
+    if (pass == 0)
+      phase_lane = __hip_atomic_load(phase_p + r * A->phase_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    // activity: the union of the tokens' sets, or the batch's shared set
+    uint64_t actm[kChunks];
+    int n_w = 0;
+  #pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      const bool in = 64 * c + lane < range;
+      uint64_t act = 0;
+      if constexpr (BMASK) {
+        // fp32 running sum of |x| over the tokens in ascending order (NaN
+        // makes it NaN, never active)
+        float score = 0.0f;
+  #pragma unroll
+        for (int b = 0; b < NB; ++b)
+          if (b < batch) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
+        act = __builtin_amdgcn_ballot_w64(in && score > batch_thr);
+      } else {
+  #pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          const int mag = (int)(xb[c][b] & 0x7FFFu);
+          act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
+        }
+      }
+      actm[c] = act;
+      n_w += __builtin_popcountll(act);
+    }
+    // list entry p of this lane's column of chunk c, with its masked
+    // activations (every token's under the batch's shared set; pair-
+    // interleaved: entries 2j and 2j+1 share a dword per token); entries of
+    // the all-zero column pad a batch: they read the
+    // bitmap array's zeroed tail and the first 16 bytes of the values, and
+    // decode to nothing
+    // An entry's second word: with tile_m a power of two (WPC 1, 2 or 4) the
+    // byte offset of the column's bitmap words, a multiple of WPC x 8, with
+    // the index of the column's last 16-byte chunk (< WPC x 8) in its low
+    // bits, so that both come out with one AND each; with 192-row tiles the
+    // column index << 6 and the chunk index.
+    constexpr bool kPow2 = (WPC & (WPC - 1)) == 0;
+    constexpr uint32_t kLow = kPow2 ? WPC * 8u - 1u : 63u;
+    auto ent_col = [&](uint32_t col, uint32_t chunk) __attribute__((always_inline)) {
+      return kPow2 ? col * (WPC * 8u) + chunk : (col << 6) | chunk;
+    };
+    auto ent_chunk = [&](uint32_t y) __attribute__((always_inline)) { return y & kLow; };
+    auto ent_bitmap = [&](uint32_t y) __attribute__((always_inline)) {
+      return kPow2 ? y & ~kLow : (y >> 6) * (WPC * 8u);
+    };
+    auto put = [&](int c, int p) __attribute__((always_inline)) {
+      // 16-byte chunks of the column's padded values (8 fp16 or 16 codes each)
+      const uint32_t chunks = Q ? ((ci[c] & 0xFFFFu) + 15u) >> 4 : ((ci[c] & 0xFFFFu) + 7u) >> 3;
+      ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), ent_col(colx[c], chunks ? chunks - 1u : 0u));
+  #pragma unroll
       for (int b = 0; b < NB; ++b) {
         const int mag = (int)(xb[c][b] & 0x7FFFu);
-        act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
+        const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
+        xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+      }
+    };
+    auto put_zero = [&](int p) __attribute__((always_inline)) {
+      ent_s[p] = make_uint2(0u, ent_col(zero_col, 0u));
+  #pragma unroll
+      for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = 0;
+    };
+
+    // A batch = kBatch list entries, streamed through the wave's ring of kSlots
+    // batch slots in LDS (LDS DMA, no registers held by loads in flight).
+    // Values: lane l of load pr brings 16 bytes of column 2pr + (l >= 32),
+    // chunk l & 31, to that column's 512-byte slot; lanes past a column's end
+    // re-read its last chunk (a line the column loads anyway). Bitmaps: lane l
+    // < 16 WPC brings dword l of the batch's words (column l / (2 WPC)).
+    const int hsel = lane >> 5;
+    const int q = lane & 31;
+    unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
+    auto issue_at = [&](int e0, int si) __attribute__((always_inline)) {
+      const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(
+          (int)lds_addr(my_ring + si * kBatchBytes));
+  #pragma unroll
+      for (int pr = 0; pr < kBatch / 2; ++pr) {
+        const uint2 e = ent_s[e0 + 2 * pr + hsel];
+        dma16(values, e.x + (min((uint32_t)q, ent_chunk(e.y)) << 4), slot + pr * 2 * kSlotBytes);
+      }
+      if (lane < 2 * WPC * kBatch) {
+        const uint2 e = ent_s[e0 + lane / (2 * WPC)];
+        dma4(bitmap, ent_bitmap(e.y) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
+      }
+    };
+
+    // ---- 2a. (when the launch asks for it) the wave's first batch: its own
+    // first kBatch active columns, listed at the tail of the list arrays and
+    // requested at once, so that their loads are in flight while the
+    // workgroup builds its list (two barriers) from the remaining columns. The phase load has landed with
+    // the loads above (loads return in order); it is read here because it is
+    // the only vector load the compiler tracks and must be complete before the
+    // first DMA: the compiler does not see those loads, so a wait it placed
+    // for a load of its own among them would count them and drain the ring.
+    // the static workspace's epoch starts at 0 (static storage), the value
+    // its zeroed partials carry: a call's tag is the stored epoch plus one
+    // (0 skipped), and the call stores its tag back when it is done
+    if (pass == 0) {
+      phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
+      if (A->phase_step == 0) phase = phase + 1u == 0u ? 1u : phase + 1u;
+    }
+    asm volatile("" ::"s"(phase));
+    const bool has_first = EARLY && early_first && n_w > 0;
+    const int e_first = kFirstList + kBatch * wave;
+    if (has_first) {
+      int rank0 = 0;
+  #pragma unroll
+      for (int c = 0; c < kChunks; ++c) {
+        if ((actm[c] >> lane) & 1) {
+          const int rk = rank0 + (int)mbcnt64(actm[c]);
+          if (rk < kBatch) put(c, e_first + rk);
+        }
+        rank0 += __builtin_popcountll(actm[c]);
+      }
+      if (lane >= n_w && lane < kBatch) put_zero(e_first + lane);
+      issue_at(e_first, 0);
+    }
+
+    // ---- 2b. the workgroup-wide list of the remaining active columns: each
+    // wave's follow those of the lower waves
+    const int n_skip = EARLY && has_first ? kBatch : 0;  // ranks already in the first batch
+    if (lane == 0) cnt_s[wave] = max(n_w - n_skip, 0);
+    __syncthreads();
+    int total = 0, pos = 0;
+  #pragma unroll
+    for (int v = 0; v < kWaves; ++v) {
+      const int cv = cnt_s[v];
+      pos += v < wave ? cv : 0;
+      total += cv;
+    }
+    {
+      int rank0 = 0;
+  #pragma unroll
+      for (int c = 0; c < kChunks; ++c) {
+        if ((actm[c] >> lane) & 1) {
+          const int rk = rank0 + (int)mbcnt64(actm[c]);
+          if (rk >= n_skip) put(c, pos + rk - n_skip);
+        }
+        rank0 += __builtin_popcountll(actm[c]);
       }
     }
-    actm[c] = act;
-    n_w += __builtin_popcountll(act);
-  }
-  // list entry p of this lane's column of chunk c, with its masked
-  // activations (every token's under the batch's shared set; pair-
-  // interleaved: entries 2j and 2j+1 share a dword per token); entries of
-  // the all-zero column pad a batch: they read the
-  // bitmap array's zeroed tail and the first 16 bytes of the values, and
-  // decode to nothing
-  // An entry's second word: with tile_m a power of two (WPC 1, 2 or 4) the
-  // byte offset of the column's bitmap words, a multiple of WPC x 8, with
-  // the index of the column's last 16-byte chunk (< WPC x 8) in its low
-  // bits, so that both come out with one AND each; with 192-row tiles the
-  // column index << 6 and the chunk index.
-  constexpr bool kPow2 = (WPC & (WPC - 1)) == 0;
-  constexpr uint32_t kLow = kPow2 ? WPC * 8u - 1u : 63u;
-  auto ent_col = [&](uint32_t col, uint32_t chunk) __attribute__((always_inline)) {
-    return kPow2 ? col * (WPC * 8u) + chunk : (col << 6) | chunk;
-  };
-  auto ent_chunk = [&](uint32_t y) __attribute__((always_inline)) { return y & kLow; };
-  auto ent_bitmap = [&](uint32_t y) __attribute__((always_inline)) {
-    return kPow2 ? y & ~kLow : (y >> 6) * (WPC * 8u);
-  };
-  auto put = [&](int c, int p) __attribute__((always_inline)) {
-    // 16-byte chunks of the column's padded values (8 fp16 or 16 codes each)
-    const uint32_t chunks = Q ? ((ci[c] & 0xFFFFu) + 15u) >> 4 : ((ci[c] & 0xFFFFu) + 7u) >> 3;
-    ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), ent_col(colx[c], chunks ? chunks - 1u : 0u));
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int mag = (int)(xb[c][b] & 0x7FFFu);
-      const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
-      xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
-    }
-  };
-  auto put_zero = [&](int p) __attribute__((always_inline)) {
-    ent_s[p] = make_uint2(0u, ent_col(zero_col, 0u));
-#pragma unroll
-    for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = 0;
-  };
+    // pad the list's last batch
+    if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) put_zero(total + lane);
+    __syncthreads();
 
-  // A batch = kBatch list entries, streamed through the wave's ring of kSlots
-  // batch slots in LDS (LDS DMA, no registers held by loads in flight).
-  // Values: lane l of load pr brings 16 bytes of column 2pr + (l >= 32),
-  // chunk l & 31, to that column's 512-byte slot; lanes past a column's end
-  // re-read its last chunk (a line the column loads anyway). Bitmaps: lane l
-  // < 16 WPC brings dword l of the batch's words (column l / (2 WPC)).
-  const int hsel = lane >> 5;
-  const int q = lane & 31;
-  unsigned char* my_ring = ring + wave * (kSlots * kBatchBytes);
-  auto issue_at = [&](int e0, int si) __attribute__((always_inline)) {
-    const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(
-        (int)lds_addr(my_ring + si * kBatchBytes));
-#pragma unroll
-    for (int pr = 0; pr < kBatch / 2; ++pr) {
-      const uint2 e = ent_s[e0 + 2 * pr + hsel];
-      dma16(values, e.x + (min((uint32_t)q, ent_chunk(e.y)) << 4), slot + pr * 2 * kSlotBytes);
-    }
-    if (lane < 2 * WPC * kBatch) {
-      const uint2 e = ent_s[e0 + lane / (2 * WPC)];
-      dma4(bitmap, ent_bitmap(e.y) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
-    }
-  };
+    // ---- 2c. the list's batches are split evenly over the waves; each wave
+    // streams its first batch, then its share, and decodes a batch as soon as
+    // its loads have landed.
+    const int n_bt = (total + kBatch - 1) / kBatch;
+    const int bb0 = n_bt * wave / kWaves;
+    const int n_first = EARLY && has_first ? 1 : 0;
+    const int n_mine = n_bt * (wave + 1) / kWaves - bb0 + n_first;
+    auto entry0 = [&](int i) { return n_first && i == 0 ? e_first : (bb0 + i - n_first) * kBatch; };
+    auto issue = [&](int i) __attribute__((always_inline)) { issue_at(entry0(i), i % kSlots); };
 
-  // ---- 2a. (when the launch asks for it) the wave's first batch: its own
-  // first kBatch active columns, listed at the tail of the list arrays and
-  // requested at once, so that their loads are in flight while the
-  // workgroup builds its list (two barriers) from the remaining columns. The phase load has landed with
-  // the loads above (loads return in order); it is read here because it is
-  // the only vector load the compiler tracks and must be complete before the
-  // first DMA: the compiler does not see those loads, so a wait it placed
-  // for a load of its own among them would count them and drain the ring.
-  // the static workspace's epoch starts at 0 (static storage), the value
-  // its zeroed partials carry: a call's tag is the stored epoch plus one
-  // (0 skipped), and the call stores its tag back when it is done
-  uint32_t phase = (uint32_t)__builtin_amdgcn_readfirstlane((int)phase_lane);
-  if (A->phase_step == 0) phase = phase + 1u == 0u ? 1u : phase + 1u;
-  asm volatile("" ::"s"(phase));
-  const bool has_first = EARLY && early_first && n_w > 0;
-  const int e_first = kFirstList + kBatch * wave;
-  if (has_first) {
-    int rank0 = 0;
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      if ((actm[c] >> lane) & 1) {
-        const int rk = rank0 + (int)mbcnt64(actm[c]);
-        if (rk < kBatch) put(c, e_first + rk);
+    // Decode of four columns of a landed batch. The bitmap words come from
+    // scalar loads of the bitmap array (the batch's DMA has just brought their
+    // lines into L2) straight into scalar registers, where they serve as
+    // MaskedPopcount masks and as EXEC masks of the value reads.
+    const const_ptr<unsigned char> bitmap_s = (const_ptr<unsigned char>)bitmap;
+    auto load_masks = [&](uint64_t (&m)[kQuad][WPC], uint32_t bo_v, int u0) __attribute__((always_inline)) {
+  #pragma unroll
+      for (int c = 0; c < kQuad; ++c) {
+        const uint32_t bo = (uint32_t)__builtin_amdgcn_readlane((int)bo_v, u0 + c);
+        const const_ptr<uint64_t> bp = (const_ptr<uint64_t>)(bitmap_s + bo);
+  #pragma unroll
+        for (int w = 0; w < WPC; ++w) m[c][w] = bp[w];
       }
-      rank0 += __builtin_popcountll(actm[c]);
-    }
-    if (lane >= n_w && lane < kBatch) put_zero(e_first + lane);
-    issue_at(e_first, 0);
-  }
-
-  // ---- 2b. the workgroup-wide list of the remaining active columns: each
-  // wave's follow those of the lower waves
-  const int n_skip = EARLY && has_first ? kBatch : 0;  // ranks already in the first batch
-  if (lane == 0) cnt_s[wave] = max(n_w - n_skip, 0);
-  __syncthreads();
-  int total = 0, pos = 0;
-#pragma unroll
-  for (int v = 0; v < kWaves; ++v) {
-    const int cv = cnt_s[v];
-    pos += v < wave ? cv : 0;
-    total += cv;
-  }
-  {
-    int rank0 = 0;
-#pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-      if ((actm[c] >> lane) & 1) {
-        const int rk = rank0 + (int)mbcnt64(actm[c]);
-        if (rk >= n_skip) put(c, pos + rk - n_skip);
-      }
-      rank0 += __builtin_popcountll(actm[c]);
-    }
-  }
-  // pad the list's last batch
-  if (wave == 0 && lane < ((kBatch - (total & (kBatch - 1))) & (kBatch - 1))) put_zero(total + lane);
-  __syncthreads();
-
-  // ---- 2c. the list's batches are split evenly over the waves; each wave
-  // streams its first batch, then its share, and decodes a batch as soon as
-  // its loads have landed.
-  const int n_bt = (total + kBatch - 1) / kBatch;
-  const int bb0 = n_bt * wave / kWaves;
-  const int n_first = EARLY && has_first ? 1 : 0;
-  const int n_mine = n_bt * (wave + 1) / kWaves - bb0 + n_first;
-  auto entry0 = [&](int i) { return n_first && i == 0 ? e_first : (bb0 + i - n_first) * kBatch; };
-  auto issue = [&](int i) __attribute__((always_inline)) { issue_at(entry0(i), i % kSlots); };
-
-  // Decode of four columns of a landed batch. The bitmap words come from
-  // scalar loads of the bitmap array (the batch's DMA has just brought their
-  // lines into L2) straight into scalar registers, where they serve as
-  // MaskedPopcount masks and as EXEC masks of the value reads.
-  const const_ptr<unsigned char> bitmap_s = (const_ptr<unsigned char>)bitmap;
-  auto load_masks = [&](uint64_t (&m)[kQuad][WPC], uint32_t bo_v, int u0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int c = 0; c < kQuad; ++c) {
-      const uint32_t bo = (uint32_t)__builtin_amdgcn_readlane((int)bo_v, u0 + c);
-      const const_ptr<uint64_t> bp = (const_ptr<uint64_t>)(bitmap_s + bo);
-#pragma unroll
-      for (int w = 0; w < WPC; ++w) m[c][w] = bp[w];
-    }
-  };
-  auto decode_quad = [&](const unsigned char* slot, int e0, int u0, const uint64_t (&m)[kQuad][WPC], int half)
-      __attribute__((always_inline)) {
-    // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
-    // below the lane plus the popcounts of the column's earlier words (every
-    // lane reads; lanes whose bit is clear read a neighbour inside the slot
-    // and are masked off below)
-    uint32_t vb[kQuad][WPC];
-#pragma unroll
-    for (int c = 0; c < kQuad; ++c) {
-      // running LDS byte address of the word's first value (scalar): one
-      // popcount and one shift-add per word
-      uint32_t sb = lds_addr(slot + (u0 + c) * kSlotBytes);
-#pragma unroll
-      for (int w = 0; w < WPC; ++w) {
-        if constexpr (Q) {
-          // a code is one byte: no shift in the address (an add instead:
-          // the mbcnt cannot take both the mask and the base from scalar
-          // registers); the signed code becomes an fp16 integer (exact for
-          // |q| <= 127), and the rest of the decode is that of fp16 values
-          const uint32_t a = sb + mbcnt64(m[c][w]);
-          const int q = *(const __attribute__((address_space(3))) int8_t*)(uintptr_t)a;
-          vb[c][w] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)(int16_t)q);
-          if (w + 1 < WPC) sb += (uint32_t)__builtin_popcountll(m[c][w]);
-        } else {
-          const uint32_t a = sb + 2u * mbcnt64(m[c][w]);
-          vb[c][w] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)a;
-          if (w + 1 < WPC) {
-            const uint32_t pop = (uint32_t)__builtin_popcountll(m[c][w]);
-            asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+    };
+    auto decode_quad = [&](const unsigned char* slot, int e0, int u0, const uint64_t (&m)[kQuad][WPC], int half)
+        __attribute__((always_inline)) {
+      // 3. bitmap decode: a row's value sits at the MaskedPopcount of its word
+      // below the lane plus the popcounts of the column's earlier words (every
+      // lane reads; lanes whose bit is clear read a neighbour inside the slot
+      // and are masked off below)
+      uint32_t vb[kQuad][WPC];
+  #pragma unroll
+      for (int c = 0; c < kQuad; ++c) {
+        // running LDS byte address of the word's first value (scalar): one
+        // popcount and one shift-add per word
+        uint32_t sb = lds_addr(slot + (u0 + c) * kSlotBytes);
+  #pragma unroll
+        for (int w = 0; w < WPC; ++w) {
+          if constexpr (Q) {
+            // a code is one byte: no shift in the address (an add instead:
+            // the mbcnt cannot take both the mask and the base from scalar
+            // registers); the signed code becomes an fp16 integer (exact for
+            // |q| <= 127), and the rest of the decode is that of fp16 values
+            const uint32_t a = sb + mbcnt64(m[c][w]);
+            const int q = *(const __attribute__((address_space(3))) int8_t*)(uintptr_t)a;
+            vb[c][w] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)(int16_t)q);
+            if (w + 1 < WPC) sb += (uint32_t)__builtin_popcountll(m[c][w]);
+          } else {
+            const uint32_t a = sb + 2u * mbcnt64(m[c][w]);
+            vb[c][w] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)a;
+            if (w + 1 < WPC) {
+              const uint32_t pop = (uint32_t)__builtin_popcountll(m[c][w]);
+              asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+            }
           }
         }
       }
-    }
-    // 4. accumulate in fp32. One or two tokens: the words become EXEC around
-    // single FMAs (v_fma_mix, fp16 operands; no branch, no select), NB per
-    // word. More tokens: the two columns of a pair are selected into the
-    // halves of one register (zero where the bit is clear: one SDWA select
-    // per column word) and one dot product per token (v_dot2_f32_f16 against
-    // the pair's two activations) adds both columns: 1 + NB/2 instructions
-    // per word instead of NB, fewer from four tokens on.
-    if constexpr (MM) {
-      // 4 (MFMA form). The batch's four columns, zero where the bit is
-      // clear, into the wave's dense tile: row 64 w + lane, columns 4 h ..
-      // 4 h + 3 for batch parity h (one 8-byte store per word); the
-      // multiply runs once per two batches (below).
-      unsigned char* mt = mt_s + wave * (64 * WPC * kMRowBytes);
-#pragma unroll
-      for (int w = 0; w < WPC; ++w) {
-        const uint32_t p01 = pair_under_words(vb[0][w], vb[1][w], m[0][w], m[1][w]);
-        const uint32_t p23 = pair_under_words(vb[2][w], vb[3][w], m[2][w], m[3][w]);
-        *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8 * half) = make_uint2(p01, p23);
-      }
-    } else if constexpr (NB == 2) {
-#pragma unroll
-      for (int pr = 0; pr < 2; ++pr) {
-        // the pair's dwords of tokens 0 and 1 (low half column 2pr)
-        const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
-        masked_fma_column2<WPC, false>(acc, vb[2 * pr], xq.x, xq.y, m[2 * pr]);
-        masked_fma_column2<WPC, true>(acc, vb[2 * pr + 1], xq.x, xq.y, m[2 * pr + 1]);
-      }
-    } else if constexpr (NB == 1) {
-      const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[e0 + u0]);
-#pragma unroll
-      for (int c = 0; c < kQuad; ++c) {
-        const uint32_t xpair = c < 2 ? xq.x : xq.y;
-        if (c & 1)
-          masked_fma_column<WPC, true>(acc, vb[c], xpair, m[c]);
-        else
-          masked_fma_column<WPC, false>(acc, vb[c], xpair, m[c]);
-      }
-    } else {
-#pragma unroll
-      for (int pr = 0; pr < 2; ++pr) {
-        uint32_t pv[WPC];
-#pragma unroll
-        for (int w = 0; w < WPC; ++w) pv[w] = pair_under_words(vb[2 * pr][w], vb[2 * pr + 1][w], m[2 * pr][w], m[2 * pr + 1][w]);
-        const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
-#pragma unroll
-        for (int b = 0; b < NB; ++b) {
-          const uint32_t x2 = xp[b];
-#pragma unroll
-          for (int w = 0; w < WPC; ++w) acc[w][b] = dot2(pv[w], x2, acc[w][b]);
-        }
-      }
-    }
-  };
-  static_assert(kQuad == 4, "decode works on quads of columns");
-
-  // The ring: batches 0 .. kSlots-1 are requested up front; after batch i is
-  // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
-  // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
-  // requested after i) loads outstanding". In the early-first-batch form
-  // (small products, few waves per CU to hide latency with) and with more
-  // than one token (measured: 0-2.5 % faster at 2-8 tokens, -2 to +1 % at
-  // 16 and 32) the bitmap words
-  // of batch i + 1 are requested as soon as batch i no longer needs their
-  // registers, so that their round trip overlaps the wait for batch i + 1's
-  // values; with many waves per CU, requesting them after that wait is
-  // faster (measured: -2 to -3 % at 4096x4096 and 11008x4096 one way, +3 to
-  // +6 % at 28672x8192 the other).
-  static_assert(kBatch == kQuad, "a batch is one decode quad");
-  for (int i = n_first; i < min(n_mine, kSlots); ++i) issue(i);
-  uint64_t m[kQuad][WPC];
-  auto masks_of = [&](int i) __attribute__((always_inline)) {
-    // byte offsets of the batch's bitmaps: lane u < kBatch holds column u's
-    const uint32_t bo_v = ent_bitmap(ent_s[entry0(i) + (lane & (kBatch - 1))].y);
-    load_masks(m, bo_v, 0);
-  };
-  constexpr bool kAhead = EARLY || NB > 1;
-  if (kAhead && n_mine > 0) masks_of(0);
-  for (int i = 0; i < n_mine; ++i) {
-    const int later = min(n_mine - 1 - i, kSlots - 1);
-    if (later >= 3)
-      wait_vmcnt<3 * kDmaPerBatch>();
-    else if (later == 2)
-      wait_vmcnt<2 * kDmaPerBatch>();
-    else if (later == 1)
-      wait_vmcnt<kDmaPerBatch>();
-    else
-      wait_vmcnt<0>();
-    if (!kAhead) masks_of(i);
-    decode_quad(my_ring + (i % kSlots) * kBatchBytes, entry0(i), 0, m, i & 1);
-    if constexpr (MM) {
-      // every second batch (and the last): the step's 8 columns (entries
-      // e .. e + 7) times the 32 tokens: per 32-row block one
-      // v_mfma_f32_32x32x8_f16, A = the tile's rows (lane l: row l mod 32,
-      // columns 4 (l / 32) .. + 4), B = the columns' masked activations
-      // (lane l: token l mod 32, the same 4 columns; 0 for tokens past NB)
-      if ((i & 1) || i + 1 == n_mine) {
+      // 4. accumulate in fp32. One or two tokens: the words become EXEC around
+      // single FMAs (v_fma_mix, fp16 operands; no branch, no select), NB per
+      // word. More tokens: the two columns of a pair are selected into the
+      // halves of one register (zero where the bit is clear: one SDWA select
+      // per column word) and one dot product per token (v_dot2_f32_f16 against
+      // the pair's two activations) adds both columns: 1 + NB/2 instructions
+      // per word instead of NB, fewer from four tokens on.
+      if constexpr (MM) {
+        // 4 (MFMA form). The batch's four columns, zero where the bit is
+        // clear, into the wave's dense tile: row 64 w + lane, columns 4 h ..
+        // 4 h + 3 for batch parity h (one 8-byte store per word); the
+        // multiply runs once per two batches (below).
         unsigned char* mt = mt_s + wave * (64 * WPC * kMRowBytes);
-        const int hl = lane >> 5;
-        if (!(i & 1)) {
-          // a single batch: the tile's second half is cleared (its columns
-          // are the next wave's, and stale weights must not meet 0)
-#pragma unroll
-          for (int w = 0; w < WPC; ++w) *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8) = make_uint2(0u, 0u);
+  #pragma unroll
+        for (int w = 0; w < WPC; ++w) {
+          const uint32_t p01 = pair_under_words(vb[0][w], vb[1][w], m[0][w], m[1][w]);
+          const uint32_t p23 = pair_under_words(vb[2][w], vb[3][w], m[2][w], m[3][w]);
+          *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8 * half) = make_uint2(p01, p23);
         }
-        const int e = entry0(i - (i & 1));
-        const int t = lane & 31;
-        uint2 bx = make_uint2(0u, 0u);
-        if (t < NB && (hl == 0 || (i & 1))) {
-          const uint32_t* xp = reinterpret_cast<const uint32_t*>(xs_s);
-          bx = make_uint2(xp[(e / 2 + 2 * hl) * NB + t], xp[(e / 2 + 2 * hl + 1) * NB + t]);
+      } else if constexpr (NB == 2) {
+  #pragma unroll
+        for (int pr = 0; pr < 2; ++pr) {
+          // the pair's dwords of tokens 0 and 1 (low half column 2pr)
+          const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
+          masked_fma_column2<WPC, false>(acc, vb[2 * pr], xq.x, xq.y, m[2 * pr]);
+          masked_fma_column2<WPC, true>(acc, vb[2 * pr + 1], xq.x, xq.y, m[2 * pr + 1]);
         }
-        const half4_t bop = __builtin_bit_cast(half4_t, bx);
-#pragma unroll
-        for (int blk = 0; blk < kMBlocks; ++blk) {
-          const uint2 av = *reinterpret_cast<const uint2*>(mt + (32 * blk + t) * kMRowBytes + 8 * hl);
-          macc[blk] = __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(half4_t, av), bop, macc[blk], 0, 0, 0);
+      } else if constexpr (NB == 1) {
+        const uint2 xq = *reinterpret_cast<const uint2*>(&xs_s[e0 + u0]);
+  #pragma unroll
+        for (int c = 0; c < kQuad; ++c) {
+          const uint32_t xpair = c < 2 ? xq.x : xq.y;
+          if (c & 1)
+            masked_fma_column<WPC, true>(acc, vb[c], xpair, m[c]);
+          else
+            masked_fma_column<WPC, false>(acc, vb[c], xpair, m[c]);
+        }
+      } else {
+  #pragma unroll
+        for (int pr = 0; pr < 2; ++pr) {
+          uint32_t pv[WPC];
+  #pragma unroll
+          for (int w = 0; w < WPC; ++w) pv[w] = pair_under_words(vb[2 * pr][w], vb[2 * pr + 1][w], m[2 * pr][w], m[2 * pr + 1][w]);
+          const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
+  #pragma unroll
+          for (int b = 0; b < NB; ++b) {
+            const uint32_t x2 = xp[b];
+  #pragma unroll
+            for (int w = 0; w < WPC; ++w) acc[w][b] = dot2(pv[w], x2, acc[w][b]);
+          }
         }
       }
+    };
+    static_assert(kQuad == 4, "decode works on quads of columns");
+
+    // The ring: batches 0 .. kSlots-1 are requested up front; after batch i is
+    // decoded its slot takes batch i + kSlots. Every batch is kDmaPerBatch
+    // loads, so "batch i has landed" is "at most kDmaPerBatch x (batches
+    // requested after i) loads outstanding". In the early-first-batch form
+    // (small products, few waves per CU to hide latency with) and with more
+    // than one token (measured: 0-2.5 % faster at 2-8 tokens, -2 to +1 % at
+    // 16 and 32) the bitmap words
+    // of batch i + 1 are requested as soon as batch i no longer needs their
+    // registers, so that their round trip overlaps the wait for batch i + 1's
+    // values; with many waves per CU, requesting them after that wait is
+    // faster (measured: -2 to -3 % at 4096x4096 and 11008x4096 one way, +3 to
+    // +6 % at 28672x8192 the other).
+    static_assert(kBatch == kQuad, "a batch is one decode quad");
+    for (int i = n_first; i < min(n_mine, kSlots); ++i) issue(i);
+    uint64_t m[kQuad][WPC];
+    auto masks_of = [&](int i) __attribute__((always_inline)) {
+      // byte offsets of the batch's bitmaps: lane u < kBatch holds column u's
+      const uint32_t bo_v = ent_bitmap(ent_s[entry0(i) + (lane & (kBatch - 1))].y);
+      load_masks(m, bo_v, 0);
+    };
+    constexpr bool kAhead = EARLY || NB > 1;
+    if (kAhead && n_mine > 0) masks_of(0);
+    for (int i = 0; i < n_mine; ++i) {
+      const int later = min(n_mine - 1 - i, kSlots - 1);
+      if (later >= 3)
+        wait_vmcnt<3 * kDmaPerBatch>();
+      else if (later == 2)
+        wait_vmcnt<2 * kDmaPerBatch>();
+      else if (later == 1)
+        wait_vmcnt<kDmaPerBatch>();
+      else
+        wait_vmcnt<0>();
+      if (!kAhead) masks_of(i);
+      decode_quad(my_ring + (i % kSlots) * kBatchBytes, entry0(i), 0, m, i & 1);
+      if constexpr (MM) {
+        // every second batch (and the last): the step's 8 columns (entries
+        // e .. e + 7) times the 32 tokens: per 32-row block one
+        // v_mfma_f32_32x32x8_f16, A = the tile's rows (lane l: row l mod 32,
+        // columns 4 (l / 32) .. + 4), B = the columns' masked activations
+        // (lane l: token l mod 32, the same 4 columns; 0 for tokens past NB)
+        if ((i & 1) || i + 1 == n_mine) {
+          unsigned char* mt = mt_s + wave * (64 * WPC * kMRowBytes);
+          const int hl = lane >> 5;
+          if (!(i & 1)) {
+            // a single batch: the tile's second half is cleared (its columns
+            // are the next wave's, and stale weights must not meet 0)
+  #pragma unroll
+            for (int w = 0; w < WPC; ++w) *reinterpret_cast<uint2*>(mt + (64 * w + lane) * kMRowBytes + 8) = make_uint2(0u, 0u);
+          }
+          const int e = entry0(i - (i & 1));
+          const int t = lane & 31;
+          uint2 bx = make_uint2(0u, 0u);
+          if (t < NB && (hl == 0 || (i & 1))) {
+            const uint32_t* xp = reinterpret_cast<const uint32_t*>(xs_s);
+            bx = make_uint2(xp[(e / 2 + 2 * hl) * NB + t], xp[(e / 2 + 2 * hl + 1) * NB + t]);
+          }
+          const half4_t bop = __builtin_bit_cast(half4_t, bx);
+  #pragma unroll
+          for (int blk = 0; blk < kMBlocks; ++blk) {
+            const uint2 av = *reinterpret_cast<const uint2*>(mt + (32 * blk + t) * kMRowBytes + 8 * hl);
+            macc[blk] = __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(half4_t, av), bop, macc[blk], 0, 0, 0);
+          }
+        }
+      }
+      if (i + kSlots < n_mine) {
+        // the slot's LDS reads have completed (their results were consumed)
+        issue(i + kSlots);
+      }
+      if (kAhead && i + 1 < n_mine) masks_of(i + 1);
     }
-    if (i + kSlots < n_mine) {
-      // the slot's LDS reads have completed (their results were consumed)
-      issue(i + kSlots);
-    }
-    if (kAhead && i + 1 < n_mine) masks_of(i + 1);
+
   }
 
   // ---- 5. reduce the 4 waves in LDS and publish this segment's partial
@@ -938,27 +954,58 @@ int hip_fail(hipError_t e, const char* what) {
 // faster but three of them (q, k, v) in one launch 5 % slower.
 // SPDP_SPLITK overrides the number of segments (for tuning).
 constexpr int kWaveCols = 48;
+// K ranges per workgroup above 16 tokens (the matrix-core form): measured on
+// the Llama-70B layer at 32 tokens, 118 / 109 / 104 us per product with 1 /
+// 2 / 4 (70/50), latency floor 94 / 68 / 54 us per launch
+constexpr int kLargeBatchPasses = 4;
 constexpr int64_t kOneRoundSegments = 48;
 constexpr int64_t kMinWorkgroups = 512;
 constexpr int64_t kMaxWorkgroups = 1792;
-void choose_split(const spdp_matrix* m, int* segments, int* wave_cols) {
+// The matrix-core accumulate pays above 16 tokens: measured on the Llama-70B
+// layer at 32 tokens 115 against 142 us per product (70/50 and 50/0), while
+// at 8 and 16 tokens the vector-ALU form (NB / 2 dot products per 64-row
+// word) is faster (56 against 90 us at 8 tokens, 39 against 53 at 16).
+// SPDP_MFMA=0 or 1 overrides from 5 tokens on (for tuning). A property of
+// the batch only, so a product gives the same bits alone and grouped.
+bool use_mfma(int batch) {
+  if (batch < 5) return false;
+  if (const char* env = std::getenv("SPDP_MFMA")) return std::atoi(env) != 0;
+  return batch > 16;
+}
+
+// Passes per workgroup: one K range each up to 16 tokens; above, several
+// consecutive ranges per workgroup, so that the split-K partials (segments
+// x batch x rows x 8 bytes, written and read back) shrink. SPDP_PASSES
+// overrides (for tuning). A property of the batch, like the split.
+int passes_for(int batch, bool codes) {
+  // only the matrix-core form (fp16 values) walks several ranges
+  if (codes || !use_mfma(batch)) return 1;
+  if (const char* env = std::getenv("SPDP_PASSES")) {
+    const long v = std::strtol(env, nullptr, 10);
+    if (v >= 1 && v <= 64) return (int)v;
+  }
+  return batch > 16 ? kLargeBatchPasses : 1;
+}
+
+void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols, int* passes) {
   const int64_t cols = std::max<int64_t>(1, m->cols);
   const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
   auto segs = [&](int64_t wc) { return (cols + kWaves * wc - 1) / (kWaves * wc); };
   int64_t wc = kWaveCols;
+  *passes = passes_for(batch, m->value_bits < 16);
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1) {
       wc = std::min<int64_t>(kMaxWaveCols, ((cols + v * kWaves - 1) / (v * kWaves) + 15) / 16 * 16);
       *wave_cols = (int)wc;
-      *segments = (int)segs(wc);
+      *segments = (int)((segs(wc) + *passes - 1) / *passes);
       return;
     }
   }
   while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kOneRoundSegments) && wc < kMaxWaveCols) wc += 16;
   while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kOneRoundSegments) wc -= 16;
   *wave_cols = (int)wc;
-  *segments = (int)segs(wc);
+  *segments = (int)((segs(wc) + *passes - 1) / *passes);
 }
 
 // The workspace holds {fp32, phase} pairs for all segments; it starts zeroed
@@ -1087,17 +1134,6 @@ hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool 
   }
 }
 
-// The matrix-core accumulate pays above 16 tokens: measured on the Llama-70B
-// layer at 32 tokens 115 against 142 us per product (70/50 and 50/0), while
-// at 8 and 16 tokens the vector-ALU form (NB / 2 dot products per 64-row
-// word) is faster (56 against 90 us at 8 tokens, 39 against 53 at 16).
-// SPDP_MFMA=0 or 1 overrides from 5 tokens on (for tuning). A property of
-// the batch only, so a product gives the same bits alone and grouped.
-bool use_mfma(int batch) {
-  if (batch < 5) return false;
-  if (const char* env = std::getenv("SPDP_MFMA")) return std::atoi(env) != 0;
-  return batch > 16;
-}
 
 // Early first batches (each wave requests its own first four active columns
 // before the workgroup builds its list) pay where a product is latency-bound:
@@ -1144,8 +1180,8 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   if (st != SPDP_OK) return st;
   if (dev != h->device) return fail(SPDP_ERR_INVALID_ARG, "current device differs from the handle's");
 
-  int segments = 1, wave_cols = 16;
-  choose_split(h, &segments, &wave_cols);
+  int segments = 1, wave_cols = 16, passes = 1;
+  choose_split(h, batch, &segments, &wave_cols, &passes);
   if (shared) {
     const size_t need = (size_t)segments * batch * h->n_stripes * h->tile_m;
     if (need > shared->capacity)
@@ -1179,6 +1215,7 @@ int prepare(spdp_handle_t h, const uint16_t* X, int32_t batch, float threshold, 
   a.code = code;
   a.wave_cols = wave_cols;
   a.segments = segments;
+  a.passes = passes;
   *n_wg = (int64_t)segments * h->n_stripes;
   a.n_wg = (int)*n_wg;
   a.early_first = early_first(batch, *n_wg);
@@ -1232,8 +1269,8 @@ int finish_device(spdp_matrix* m, spdp_handle_t* out) {
     }
   }
   if (st == SPDP_OK) {
-    int segments = 1, wave_cols = 16;
-    choose_split(m, &segments, &wave_cols);
+    int segments = 1, wave_cols = 16, passes = 1;
+    choose_split(m, 1, &segments, &wave_cols, &passes);
     st = ensure_workspace(m, 1, segments, false, nullptr);
   }
   if (st != SPDP_OK) {
@@ -1392,9 +1429,14 @@ int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
   if (h->device < 0) return fail(SPDP_ERR_INVALID_ARG, "handle has no device copy");
   if (max_batch < 1 || max_batch > kMaxBatch)
     return fail(SPDP_ERR_INVALID_ARG, "max_batch must lie in [1, 32]");
-  int segments = 1, wave_cols = 16;
-  choose_split(h, &segments, &wave_cols);
-  return ensure_workspace(h, max_batch, segments, false, nullptr);
+  // every batch up to max_batch: the split (and so the workspace) depends on it
+  int64_t need = 0;  // segments x batch
+  for (int b = 1; b <= max_batch; ++b) {
+    int segments = 1, wave_cols = 16, passes = 1;
+    choose_split(h, b, &segments, &wave_cols, &passes);
+    need = std::max<int64_t>(need, (int64_t)segments * b);
+  }
+  return ensure_workspace(h, (int)need, 1, false, nullptr);
 }
 
 int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,

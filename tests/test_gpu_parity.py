@@ -503,3 +503,22 @@ def test_batch_mask_edge_cases():
     assert not oracle.active_mask(xn, t, "batch")[0, 10]
     _assert_close(y, y64, s64, "batch mask, NaN token")
     m.close()
+
+
+@pytest.mark.parametrize("passes", ["1", "2", "3", "5"])
+@pytest.mark.parametrize("batch", [8, 17, 32])
+def test_forced_passes_and_matrix_core_form(monkeypatch, passes, batch):
+    """Several K ranges per workgroup (the matrix-core form at large
+    batches) and the matrix-core form itself, forced on from 5 tokens: fp16
+    values and one-byte codes (which keep the vector-ALU form and one range)
+    must both match the oracle."""
+    monkeypatch.setenv("SPDP_PASSES", passes)
+    monkeypatch.setenv("SPDP_MFMA", "1")
+    w, x, t = _case(700, 3000, (256, 16), 0.6, 0.4, batch, 123, 456)
+    _check_full(w, x, t, (256, 16), f"passes={passes} B={batch} fp16")
+    codes, scales, _ = oracle.rtn_quantize(w, 4)
+    m = spdp.encode_rtn(w, (256, 16), 4)
+    y = _run_gpu(m, x, t)
+    y64, s64, _ = oracle.spmspv_rtn(codes, scales, x, t)
+    _assert_close(y, y64, s64, f"passes={passes} B={batch} codes")
+    m.close()

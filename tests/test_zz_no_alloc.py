@@ -148,6 +148,7 @@ def test_noalloc_refuses_more_than_its_workspace(monkeypatch):
     m = spdp.encode(w, (256, 16))
     # 128 segments x 32 tokens x 4096 rows x 8 bytes = 128 MiB of partials
     monkeypatch.setenv("SPDP_SPLITK", "1000")
+    monkeypatch.setenv("SPDP_PASSES", "1")
     X = _to_dev(x)
     Y = _nan_y(m, 32)
     assert _abi_noalloc(m, X, t, Y) == ERR_UNSUPPORTED
