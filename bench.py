@@ -1004,7 +1004,7 @@ def _counters(path):
             k = row["Kernel_Name"]
             v = float(row["Counter_Value"])
             sp, rd = out.setdefault(name, ([], []))
-            if "spmspv_kernel" in k:
+            if "spmspv_kernel" in k or "spmspv_mm_kernel" in k:
                 sp.append(v)
             elif "read_kernel" in k:
                 rd.append(v)
@@ -1032,11 +1032,11 @@ def summarize_profiles(d, prof_dir=None):
         for r in rows:
             out.append(f"{r['Name'].replace('(anonymous namespace)::', '')[:70]} | {r['Calls']} | "
                        f"{float(r['AverageNs']):.1f} | {r['MinNs']} | {r['MaxNs']}")
-        kr = [r for r in rows if "spmspv_kernel" in r["Name"]]
+        kr = [r for r in rows if "spmspv_kernel" in r["Name"] or "spmspv_mm_kernel" in r["Name"]]
         calls = sum(int(r["Calls"]) for r in kr)
         avg = sum(int(r["Calls"]) * float(r["AverageNs"]) for r in kr) / max(calls, 1)
         alg = pj["algorithmic_bytes_per_launch"]
-        out += ["", f"all spmspv_kernel variants: {calls} launches, launch-weighted average {avg:.1f} ns",
+        out += ["", f"all spMspV kernel variants: {calls} launches, launch-weighted average {avg:.1f} ns",
                 f"  -> {alg / avg:.1f} GB/s algorithmic ({100 * alg / avg / HBM_PEAK_GBS:.2f} % of "
                 f"{HBM_PEAK_GBS:.0f} GB/s)",
                 "", "bench.py --profile-only (same command) reported:",
