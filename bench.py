@@ -59,6 +59,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X published HBM3E bandwidth
 # per cycle (a two-wide fp32 FMA, or v_dot2_f32_f16's two fp16 products added
 # into fp32) x 2.4 GHz
 VEC_PEAK_TFLOPS = 157.3
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X published dense fp16 matrix peak
 LINE = 128  # bytes per L2 cache line (the granularity the traffic model uses)
 
 
@@ -685,10 +686,17 @@ def prune_all(B, wl, sw_list):
             for sw in sw_list for proj in wl["projections"]}
 
 
-def roof(step_bytes, step_flops, ms):
+# the library accumulates on the matrix cores above this many tokens (and
+# on the vector ALUs up to it): the compute roof follows the form
+MATRIX_CORE_MIN_BATCH = 17
+
+
+def roof(step_bytes, step_flops, ms, batch=1):
     t_hbm = step_bytes / (HBM_PEAK_GBS * 1e9) * 1e3
-    t_alu = step_flops / (VEC_PEAK_TFLOPS * 1e12) * 1e3
-    return {"frac": round(max(t_hbm, t_alu) / ms, 4), "binding": "alu" if t_alu > t_hbm else "hbm"}
+    mfma = batch >= MATRIX_CORE_MIN_BATCH
+    t_alu = step_flops / ((MFMA_F16_PEAK_TFLOPS if mfma else VEC_PEAK_TFLOPS) * 1e12) * 1e3
+    return {"frac": round(max(t_hbm, t_alu) / ms, 4),
+            "binding": ("mfma" if mfma else "alu") if t_alu > t_hbm else "hbm"}
 
 
 # the other workloads, each a (name, sw, p, batches) slice measured like the
@@ -726,7 +734,7 @@ def secondary(B, args):
                  "us_per_product": round(ms * 1e3 / r["n_calls"], 3),
                  "gbs": round(r["step_bytes"] / (ms * 1e-3) / 1e9, 1),
                  "pct_of_hbm_peak": round(100 * r["step_bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 2),
-                 "roofline": roof(r["step_bytes"], r["step_flops"], ms),
+                 "roofline": roof(r["step_bytes"], r["step_flops"], ms, b),
                  "active_frac": round(float(np.mean([pt["active_frac"] for pt in pts])), 4),
                  "speedup_vs_dense": round(d / ms, 3) if d else None,
                  "dense_us_per_product": round(d * 1e3 / r["n_calls"], 3) if d else None}
@@ -739,8 +747,6 @@ def secondary(B, args):
         B.torch.cuda.empty_cache()
     return out
 
-
-MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X published dense fp16 matrix peak
 
 # prefill products (Sec. 4.3): (workload, projection, sw, tokens)
 PREFILL = [
