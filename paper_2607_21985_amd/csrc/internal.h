@@ -37,6 +37,9 @@ struct spdp_matrix {
   unsigned long long* d_partials = nullptr;
   size_t partial_floats = 0;  // capacity in pairs
   uint32_t* d_phase = nullptr;
+  // Split-K partial sums of the prefill product (fp32, grown on demand).
+  void* d_spmm_part = nullptr;
+  size_t spmm_part_bytes = 0;
   // Workspaces replaced by a larger one: a HIP graph captured earlier still
   // names them, so they live until the handle is freed.
   std::vector<void*> retired;

@@ -1051,7 +1051,8 @@ void release_device(spdp_matrix* m) {
   (void)hipGetDevice(&prev);
   (void)hipSetDevice(m->device);
   (void)hipDeviceSynchronize();
-  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_scales, m->d_partials, m->d_phase};
+  void* ptrs[] = {m->d_tile_offset, m->d_col_info, m->d_bitmap, m->d_values, m->d_scales, m->d_partials, m->d_phase,
+                  m->d_spmm_part};
   for (void* p : ptrs)
     if (p) (void)hipFree(p);
   for (void* p : m->retired) (void)hipFree(p);
@@ -1060,6 +1061,8 @@ void release_device(spdp_matrix* m) {
   m->d_partials = nullptr;
   m->d_phase = nullptr;
   m->partial_floats = 0;
+  m->d_spmm_part = nullptr;
+  m->spmm_part_bytes = 0;
   if (prev >= 0) (void)hipSetDevice(prev);
 }
 

@@ -5,28 +5,29 @@
 // (the paper's layout-alignment stage), then multiplied with
 // v_mfma_f32_32x32x16_f16 (fp16 operands, fp32 accumulation).
 //
-// Workgroup (4 waves) = one 256-row stripe x 128 tokens. Per k-step of 16
-// columns (one GTile of a 256 x 16 tiling):
-//   1. decode: wave w expands columns 4w .. 4w+3 of the step, all four
-//      64-row bitmap words each: lane i of word v takes row 64v + i, its
-//      value at the word's masked popcount below bit i plus the popcounts of
-//      the column's earlier words (HAD-SMBD, Sec. 4.2.1), or 0 where the bit
-//      is clear; the four columns of a row go to LDS as one 8-byte store
-//      (row-major dense tile, 16 fp16 per row, rows padded to 40 bytes);
-//   2. multiply: wave w owns tokens 32w .. 32w+31; its B operand (16 k x
-//      32 tokens) is read straight from X (lane l: token l mod 32, eight
-//      consecutive k), and for each of the eight 32-row blocks of the
-//      stripe one MFMA adds A (32 rows x 16 k, two 8-byte LDS reads per
-//      lane) times B into that block's 32 x 32 accumulators.
-// The dense tile is double-buffered, so one barrier per k-step separates a
-// step's LDS writes from the other waves' reads. Every k-step's metadata,
-// values and X block are requested one step ahead, while the current
-// step's MFMAs run.
+// A workgroup owns one 256-row stripe x 128 tokens and walks the stripe in
+// k-steps of 16 columns. Expansion of a k-step: lane i of bitmap word v of
+// a column takes row 64 v + i; its value sits at the word's masked popcount
+// below bit i plus the popcounts of the column's earlier words (HAD-SMBD,
+// Sec. 4.2.1), or is 0 where the bit is clear; the tile is row-major, 16
+// fp16 per row, rows padded to 40 bytes so that the MFMA operand reads of
+// 32 consecutive rows spread over the banks.
+//
+// Two forms:
+//   * spmm_kernel, any tile_k >= 16 and any width: four waves, each expands
+//     four columns and multiplies the stripe's eight 32-row blocks with its
+//     32 tokens; operands fetched one step ahead into registers;
+//   * spmm_ws_kernel, 256 x 16 GTiles and a width that is a multiple of 8:
+//     warp-specialized, DMA ring, split-K over the GTiles when the grid is
+//     small (described at the kernel).
 
 #include <hip/hip_fp16.h>
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 #include "internal.h"
 
@@ -67,8 +68,9 @@ __device__ __forceinline__ uint32_t mbcnt64(uint64_t mask) {
 template <class T>
 using const_ptr = const __attribute__((address_space(4))) T*;
 
-// What one wave fetches for one k-step: its four columns' values (one per
-// lane and bitmap word, 0 where the bit is clear) and its B operand.
+// The plain form. What one wave fetches for one k-step: its four columns'
+// values (one per lane and bitmap word, 0 where the bit is clear) and its B
+// operand.
 struct StepData {
   uint2 v[4];  // [word]: the four columns' fp16 bits, two per dword
   half8 b;
@@ -180,28 +182,10 @@ __global__ __launch_bounds__(256) void spmm_kernel(SpmmArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// The pipelined form for 256 x 16 GTiles and a width that is a multiple of
-// 8 (every Llama shape): each k-step is one GTile, and everything a step
-// reads from memory -- the GTile's padded values (one contiguous run), its
-// 16 columns' bitmap words and ColInfo, and the 128 x 16 block of X -- is
-// copied into a ring of kRing LDS slots by global->LDS DMA, kRing steps
-// ahead, so that no wave waits on memory for the decode. Per wave and step:
-// two 16-byte DMA loads of values (the GTile's values in 16-byte chunks over
-// 4 waves x 2 loads x 64 lanes; lanes past the end re-read the last chunk),
-// one 4-byte DMA load of bitmap words or ColInfo, one 16-byte DMA load of
-// its own 32 tokens of X: four loads, so "step s has landed" is "at most
-// 4 x (later steps requested) loads outstanding". Step s: the MFMAs of step
-// s (dense tile s & 1, B operand from the wave's own X rows of slot s), then
-// the DMA of step s + kRing into slot s (its values, bitmaps and ColInfo
-// were decoded in step s - 1, its X rows were just read), then the decode of
-// step s + 1 into dense tile (s + 1) & 1 while the MFMAs run, then one
-// barrier.
+// Helpers of the pipelined form below.
 
-constexpr int kRing = 4;
-constexpr int kMetaBytes = 1024;               // bitmaps (512 B), ColInfo (64 B), DMA spill
 constexpr int kValBytes = kTM * kKStep * 2;    // a dense GTile's worth of values
 constexpr int kXBytes = kBN * kKStep * 2;      // 128 tokens x 16 columns
-constexpr int kSlotBytes = kMetaBytes + kValBytes + kXBytes;
 
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
@@ -221,186 +205,361 @@ template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
-constexpr int kDmaPerStep = 4;
+// ---------------------------------------------------------------------------
+// Warp-specialized form, for 256 x 16 GTiles and a width that is a
+// multiple of 8 (every Llama shape): each k-step is one GTile, and what a
+// step reads from memory -- the GTile's padded values (one contiguous run)
+// and the 128 x 16 block of X -- is copied into a ring of LDS slots by
+// global->LDS DMA several steps ahead. Sixteen waves: waves 0-7 multiply, waves
+// 8-15 expand. A wave issues in order and waits while the matrix core is
+// busy with its previous MFMA, so a wave that did both would serialize
+// them; with the roles in different waves every SIMD holds two multiplying
+// and two expanding waves, and the expansion of step s + 1 runs while the
+// MFMAs of step s do. One barrier per step (one GTile).
+//   * multiplying wave m: rows 64 (m & 3) .., tokens 64 (m >> 2) .. of the
+//     256 x 128 output tile (four 32 x 32 blocks, A and B each read once);
+//     it also issues the step's DMA: one 16-byte load of values (8 x 64
+//     lanes x 16 bytes cover a dense GTile) and one of X (m < 4: 32 tokens
+//     each) or of bitmap words / ColInfo (m >= 4: these only warm L2 for
+//     the expanding waves' scalar loads and land in a scratch area). The
+//     TileOffsets come from the LDS table: no scalar memory load, so the
+//     LDS waits of these waves never wait for one;
+//   * expanding wave d: columns 2d, 2d + 1 of the GTile (eight bitmap
+//     words, scalar loads two steps ahead, so the loads of step s + 2 are in
+//     flight while step s + 1 is expanded), values from the slot.
+// A slot is refilled in the step after its X rows were read: step s
+// requests step s + kWsRing - 1 into the slot of step s - 1.
+//
+// Split-K (blockIdx.z of k_splits): a workgroup walks GTiles [z sps, (z + 1)
+// sps) of its stripe and, with more than one split, stores its fp32 sums to
+// part[z][token][row]; spmm_reduce_kernel adds the splits in order.
 
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void spmm_ring_kernel(SpmmArgs a) {
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRing][kSlotBytes];
+constexpr int kWsWaves = 16;
+constexpr int kWsRing = 8;
+constexpr int kWsDma = 2;      // loads per step of a multiplying wave
+constexpr int kToCap = 1800;   // TileOffsets of one stripe's split held in LDS
+constexpr int kGBytes = kValBytes + kXBytes;  // one GTile's values and X block in a ring slot
+
+// the lane's value of column a (low half) and of column b (high half) where
+// its bit of the column's word is set, else 0: one select per column (SDWA
+// writes one half and keeps the other)
+__device__ __forceinline__ uint32_t pair_select(uint32_t a, uint32_t b, uint64_t ma, uint64_t mb) {
+  uint32_t p;
+  asm("s_mov_b64 vcc, %[ma]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[a], vcc dst_sel:WORD_0 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0\n\t"
+      "s_mov_b64 vcc, %[mb]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[b], vcc dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0"
+      : [p] "=&v"(p)
+      : [a] "v"(a), [b] "v"(b), [ma] "s"(ma), [mb] "s"(mb)
+      : "vcc");
+  return p;
+}
+
+// wait until at most kWsDma x `later` loads are in flight (later < N + 1)
+template <int N>
+__device__ __forceinline__ void wait_steps(int later) {
+  if constexpr (N > 0) {
+    if (later >= N) {
+      wait_vmcnt<kWsDma * N>();
+      return;
+    }
+    wait_steps<N - 1>(later);
+  } else {
+    wait_vmcnt<0>();
+  }
+}
+
+struct WsArgs {
+  SpmmArgs s;
+  float* part;  // [k_splits][n_tokens][rows] fp32 when k_splits > 1
+  int k_splits;
+  int sps;      // GTiles per split
+};
+
+__global__ __launch_bounds__(kWsWaves * 64) void spmm_ws_kernel(WsArgs wa) {
+  const SpmmArgs& a = wa.s;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kWsRing][kGBytes];
   __shared__ __attribute__((aligned(16))) unsigned char tile[2][kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char warm[1024];
+  __shared__ uint32_t toff[kToCap];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool mma = wave < 8;
+  const int mw = wave & 7;  // index within the role
   const int r = blockIdx.x;
   const long long nb0 = (long long)blockIdx.y * kBN;
   const int khalf = (lane >> 5) * 8;
-  const int steps = a.steps;
-  const const_ptr<uint32_t> to_s = (const_ptr<uint32_t>)a.tile_offset;
+  const int c0 = (int)blockIdx.z * wa.sps;                 // first GTile of this split
+  const int steps = min(wa.sps, a.n_colblocks - c0);       // >= 1 (the host makes every split non-empty)
   const uint32_t g0 = (uint32_t)r * (uint32_t)a.n_colblocks;
-  // this workgroup's 128 tokens of X (tokens past the end re-read the last)
-  const uint16_t* const xblk = a.x + nb0 * (long long)a.cols;
-  const long long left = a.n_tokens - nb0;
-  // X DMA: lane l of wave w brings token 32w + l / 2, columns 8 (l & 1) ..
-  // + 8 of the step, to byte 1024 w + 16 l of the slot's X block
-  const int xt = 32 * wave + (lane >> 1);
-  const uint32_t x_row = (uint32_t)((xt < left ? xt : left - 1) * (long long)a.cols * 2);
+  for (int i = threadIdx.x; i <= steps; i += kWsWaves * 64) toff[i] = a.tile_offset[g0 + (uint32_t)(c0 + i)];
 
+  // multiplying waves: the second DMA of a GTile, as (source, lane offset
+  // at GTile 0, bytes per GTile, LDS offset): X into the slot, or bitmap
+  // words / ColInfo into the warm-up area
+  const bool x_dma = mw < 4;
+  const void* d_src;
+  uint32_t d_off, d_step, d_lds;
+  {
+    const long long left = a.n_tokens - nb0;
+    const int xt = 32 * mw + (lane >> 1);
+    if (x_dma) {
+      d_src = a.x + nb0 * (long long)a.cols;
+      d_off = (uint32_t)((xt < left ? xt : left - 1) * (long long)a.cols * 2) + 16u * (uint32_t)(lane & 1);
+      d_step = 2u * kKStep;
+      d_lds = (uint32_t)(kValBytes + 1024 * mw);
+    } else if (mw < 6) {
+      d_src = a.bitmap;
+      d_off = g0 * 512u + 256u * (uint32_t)(mw - 4) + 4u * (uint32_t)lane;
+      d_step = 512u;
+      d_lds = lds_addr(warm) + 256u * (uint32_t)(mw - 4);
+    } else {
+      d_src = a.col_info;
+      d_off = g0 * 64u + 4u * (uint32_t)(lane & 15);
+      d_step = 64u;
+      d_lds = lds_addr(warm) + 512u + 256u * (uint32_t)(mw - 6);
+    }
+  }
+  const uint32_t q16 = 16u * (uint32_t)(mw * 64 + lane);
+  __syncthreads();
+
+  // requests step s (GTile c0 + s) into its slot
   auto issue = [&](int s) __attribute__((always_inline)) {
-    unsigned char* slot = ring[s % kRing];
-    const uint32_t g = g0 + (uint32_t)s;
-    const uint32_t t0 = to_s[g], t1 = to_s[g + 1];
-    const uint32_t last = t1 > t0 ? (t1 - t0) / 8u - 1u : 0u;  // last 16-byte chunk of the values
-    const uint32_t vbase = lds_addr(slot + kMetaBytes);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const uint32_t q = (uint32_t)((i * kWaves + wave) * 64 + lane);
-      dma16(a.values, 2u * t0 + 16u * (q < last ? q : last),
-            (uint32_t)__builtin_amdgcn_readfirstlane((int)(vbase + (uint32_t)(i * kWaves + wave) * 1024u)));
+    const uint32_t c = (uint32_t)(c0 + s);
+    const uint32_t slot = lds_addr(ring[s & (kWsRing - 1)]);
+    // the GTile's values: lanes past the end re-read its last 16 bytes
+    const uint32_t t0 = toff[s], t1 = toff[s + 1];
+    const int span = 2 * (int)(t1 - t0) - 16;
+    const uint32_t voff = 2u * t0 + min(q16, (uint32_t)max(span, 0));
+    asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(a.values),
+                 "{m0}"((uint32_t)__builtin_amdgcn_readfirstlane((int)(slot + 1024u * (uint32_t)mw)))
+                 : "memory");
+    if (x_dma) {
+      // columns past the width (the last GTile of a width that is not a
+      // multiple of 16): any valid 16 bytes, the B operand is cleared
+      uint32_t off = d_off + c * d_step;
+      if (c * kKStep + 8u * (uint32_t)(lane & 1) >= (uint32_t)a.cols) off = d_off - 16u * (uint32_t)(lane & 1);
+      dma16(d_src, off, (uint32_t)__builtin_amdgcn_readfirstlane((int)(slot + d_lds)));
+    } else {
+      dma4(d_src, d_off + c * d_step, d_lds);
     }
-    // waves 0, 1: the 16 columns' bitmap words (512 bytes); wave 2 the
-    // ColInfo (64 bytes; its other lanes re-read it); wave 3 re-reads it too
-    const uint32_t mbase = lds_addr(slot) + 256u * (uint32_t)wave;
-    if (wave < 2)
-      dma4(a.bitmap, g * 512u + 256u * (uint32_t)wave + 4u * (uint32_t)lane,
-           (uint32_t)__builtin_amdgcn_readfirstlane((int)mbase));
-    else
-      dma4(a.col_info, g * 64u + 4u * (uint32_t)(lane & 15), (uint32_t)__builtin_amdgcn_readfirstlane((int)mbase));
-    const uint32_t xk = (uint32_t)(s * kKStep + 8 * (lane & 1));
-    // columns past the width: any valid 16 bytes (the weights there are 0;
-    // the B operand is cleared after the read)
-    const uint32_t xoff = x_row + 2u * (xk < (uint32_t)a.cols ? xk : 0u);
-    dma16(xblk, xoff, (uint32_t)__builtin_amdgcn_readfirstlane((int)lds_addr(slot + kMetaBytes + kValBytes + 1024 * wave)));
   };
-  // "step s landed": at most kDmaPerStep x (steps requested after s) loads
-  // in flight, the count being min(kRing - 1, steps - 1 - s) in the steady state
-  auto wait_landed = [&](int later) __attribute__((always_inline)) {
-    if (later >= 3)
-      wait_vmcnt<3 * kDmaPerStep>();
-    else if (later == 2)
-      wait_vmcnt<2 * kDmaPerStep>();
-    else if (later == 1)
-      wait_vmcnt<kDmaPerStep>();
-    else
-      wait_vmcnt<0>();
-  };
-  static_assert(kRing == 4, "wait_landed counts up to three later steps");
-  // decode of step s (slot s % kRing) into dense tile `t`: wave w expands
-  // columns 4w .. 4w + 3, lane i of word v giving row 64 v + i. ColInfo and
-  // the bitmap words come from scalar loads (the step's DMA has brought
-  // their lines into L2) straight into scalar registers, where they serve as
-  // mbcnt masks and as the select mask of the lanes' values; the values come
-  // from the slot.
-  const const_ptr<uint32_t> ci_s = (const_ptr<uint32_t>)a.col_info;
-  const const_ptr<uint64_t> bm_s = (const_ptr<uint64_t>)a.bitmap;
+
+  // expanding waves: the two columns' words and ColInfo, by scalar loads
   struct Meta {
-    uint32_t ci[4];
-    uint64_t words[4][4];
+    uint64_t w[8];  // column 2d: words 0-3, column 2d + 1: words 4-7
+    uint32_t ci[2];
   };
-  // requested one step ahead of its decode, so that the scalar loads' round
-  // trip overlaps the previous step's work
-  auto meta_of = [&](int s, Meta& m) __attribute__((always_inline)) {
-    const uint32_t col0 = (g0 + (uint32_t)s) * (uint32_t)kKStep + 4u * (uint32_t)wave;
+  const const_ptr<uint64_t> bm_s = (const_ptr<uint64_t>)a.bitmap;
+  const const_ptr<uint32_t> ci_s = (const_ptr<uint32_t>)a.col_info;
+  auto load_meta = [&](int s, Meta& m) __attribute__((always_inline)) {
+    const uint32_t col0 = (g0 + (uint32_t)(c0 + s)) * (uint32_t)kKStep + 2u * (uint32_t)mw;
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      m.ci[jj] = ci_s[col0 + jj];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) m.words[jj][v] = bm_s[(size_t)(col0 + jj) * 4 + v];
-    }
+    for (int i = 0; i < 8; ++i) m.w[i] = bm_s[(size_t)col0 * 4 + i];
+    m.ci[0] = ci_s[col0];
+    m.ci[1] = ci_s[col0 + 1];
   };
-  auto decode = [&](int s, const Meta& m, unsigned char* t) __attribute__((always_inline)) {
-    const unsigned char* slot = ring[s % kRing];
-    const uint32_t (&ci)[4] = m.ci;
-    const uint64_t (&words)[4][4] = m.words;
-    const uint32_t vb = lds_addr(slot + kMetaBytes);
-    uint32_t h[4][4];
+  // column 2 d + jj, word v -> row 64 v + lane: the value at the word's
+  // masked popcount below the lane plus the column's earlier words' counts
+  auto decode = [&](int s, const Meta& m) __attribute__((always_inline)) {
+    const uint32_t vb = lds_addr(ring[s & (kWsRing - 1)]);
+    unsigned char* t = tile[s & 1];
+    uint32_t hv[2][4];
 #pragma unroll
-    for (int jj = 0; jj < 4; ++jj) {
-      uint32_t base = vb + 2u * (ci[jj] >> 16);
+    for (int jj = 0; jj < 2; ++jj) {
+      uint32_t sb = vb + 2u * (m.ci[jj] >> 16);
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const uint64_t word = words[jj][v];
-        const uint32_t hv =
-            *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(base + 2u * mbcnt64(word));
-        // the lane's value where its bit is set, else 0 (the word as the select mask)
-        uint32_t sel;
-        asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(sel) : "v"(hv), "s"(word));
-        h[v][jj] = sel;
-        base += 2u * (uint32_t)__builtin_popcountll(word);
+        hv[jj][v] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(sb + 2u * mbcnt64(m.w[4 * jj + v]));
+        if (v < 3) {
+          const uint32_t pop = (uint32_t)__builtin_popcountll(m.w[4 * jj + v]);
+          asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+        }
       }
     }
 #pragma unroll
     for (int v = 0; v < 4; ++v)
-      *reinterpret_cast<uint2*>(t + (64 * v + lane) * kRowBytes + 8 * wave) =
-          make_uint2(h[v][0] | (h[v][1] << 16), h[v][2] | (h[v][3] << 16));
+      *reinterpret_cast<uint32_t*>(t + (64 * v + lane) * kRowBytes + 4 * mw) =
+          pair_select(hv[0][v], hv[1][v], m.w[v], m.w[4 + v]);
   };
 
-  float16v acc[kBlocks];
+  const int rq = mw & 3, th = mw >> 2;
+  float16v acc[2][2];
 #pragma unroll
-  for (int i = 0; i < kBlocks; ++i) acc[i] = float16v{};
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = float16v{};
+  const half8 none = half8{0, 0, 0, 0, 0, 0, 0, 0};
 
-  // prologue: the first kRing steps requested, step 0 decoded, step 1 landed
-  for (int s = 0; s < kRing && s < steps; ++s) issue(s);
-  Meta meta;
-  meta_of(0, meta);
-  wait_landed(min(kRing - 1, steps - 1));
-  __syncthreads();
-  decode(0, meta, tile[0]);
-  if (steps > 1) meta_of(1, meta);
-  wait_landed(min(kRing - 2, steps - 2));
-  __syncthreads();
-
-  for (int s = 0; s < steps; ++s) {
-    unsigned char* slot = ring[s % kRing];
-    const unsigned char* t = tile[s & 1];
-    // B operand: this wave's 32 tokens, 8 columns, from its own X rows
-    half8 b = *reinterpret_cast<const half8*>(slot + kMetaBytes + kValBytes +
-                                              (32 * wave + (lane & 31)) * 32 + 2 * khalf);
-    if (s * kKStep + khalf >= a.cols) b = half8{0, 0, 0, 0, 0, 0, 0, 0};
-    half8 av[kBlocks];
+  // one step. Multiplying waves: MFMAs of step s, request of step
+  // s + kWsRing - 1, wait for step s + 2. Expanding waves: scalar loads of
+  // step s + 2 into `next`, expansion of step s + 1 from `cur`. Barrier.
+  // STEADY: every one of these happens, kWsRing - 3 later steps are in
+  // flight, and every column is inside the width.
+  auto step = [&](int s, Meta& cur, Meta& next, auto steady) __attribute__((always_inline)) {
+    constexpr bool kSteady = decltype(steady)::value;
+    if (mma) {
+      const unsigned char* slot = ring[s & (kWsRing - 1)];
+      const unsigned char* t = tile[s & 1];
+      half8 b[2];
 #pragma unroll
-    for (int i = 0; i < kBlocks; ++i) {
-      const unsigned char* p = t + (32 * i + (lane & 31)) * kRowBytes + 2 * khalf;
-      const uint2 lo = *reinterpret_cast<const uint2*>(p);
-      const uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
-      av[i] = __builtin_bit_cast(half8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-    }
+      for (int j = 0; j < 2; ++j) {
+        b[j] = *reinterpret_cast<const half8*>(slot + kValBytes + (64 * th + 32 * j + (lane & 31)) * 32 + 2 * khalf);
+        if constexpr (!kSteady)
+          if ((c0 + s) * kKStep + khalf >= a.cols) b[j] = none;
+      }
+      half8 av[2];
 #pragma unroll
-    for (int i = 0; i < kBlocks; ++i) acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], b, acc[i], 0, 0, 0);
-    // the slot's X rows have been read (the operands are in registers); its
-    // values and metadata were decoded before the last barrier
-    if (s + kRing < steps) issue(s + kRing);
-    if (s + 1 < steps) decode(s + 1, meta, tile[(s + 1) & 1]);
-    // step s + 2 (decoded in the next iteration) has landed: the steps
-    // requested after it are s + 3 .. min(s + kRing, steps - 1)
-    if (s + 2 < steps) {
-      wait_landed(min(kRing - 2, steps - 1 - (s + 2)));
-      meta_of(s + 2, meta);
+      for (int i = 0; i < 2; ++i) {
+        const unsigned char* p = t + (64 * rq + 32 * i + (lane & 31)) * kRowBytes + 2 * khalf;
+        const uint2 lo = *reinterpret_cast<const uint2*>(p);
+        const uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
+        av[i] = __builtin_bit_cast(half8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], b[j], acc[i][j], 0, 0, 0);
+      if (kSteady || s + kWsRing - 1 < steps) issue(s + kWsRing - 1);
+      if constexpr (kSteady)
+        wait_vmcnt<kWsDma * (kWsRing - 3)>();
+      else if (s + 2 < steps)
+        wait_steps<kWsRing - 3>(min(kWsRing - 3, steps - 1 - (s + 2)));
+    } else {
+      if (kSteady || s + 2 < steps) load_meta(s + 2, next);
+      if (kSteady || s + 1 < steps) decode(s + 1, cur);
     }
     __syncthreads();
+  };
+
+  // prologue: steps 0 .. kWsRing - 2 requested; step 0 expanded; step 1 landed
+  Meta ma, mb;
+  if (mma) {
+    for (int s = 0; s < kWsRing - 1 && s < steps; ++s) issue(s);
+    wait_steps<kWsRing - 2>(min(kWsRing - 2, steps - 1));
+  } else {
+    load_meta(0, ma);
+    if (steps > 1) load_meta(1, mb);
+  }
+  __syncthreads();
+  if (mma) {
+    if (steps > 1) wait_steps<kWsRing - 3>(min(kWsRing - 3, steps - 2));
+  } else {
+    decode(0, ma);
+  }
+  __syncthreads();
+
+  // step s expands s + 1 from the set loaded two steps before: step 0 uses
+  // mb (step 1) and loads step 2 into ma, step 1 the other way round
+  int s = 0;
+  const int steady_end = steps - kWsRing;
+  for (; s + 1 < steady_end; s += 2) {
+    step(s, mb, ma, std::integral_constant<bool, true>{});
+    step(s + 1, ma, mb, std::integral_constant<bool, true>{});
+  }
+  for (; s < steps; s += 2) {
+    step(s, mb, ma, std::integral_constant<bool, false>{});
+    if (s + 1 < steps) step(s + 1, ma, mb, std::integral_constant<bool, false>{});
   }
 
-  const long long n = nb0 + 32 * wave + (lane & 31);
-  if (n >= a.n_tokens) return;
-  uint16_t* const yrow = a.y + n * (long long)a.rows;
+  if (!mma) return;
+  // accumulator register e of block (i, j) holds row 32 i + 8 (e / 4) +
+  // 4 (lane / 32) + e % 4 of the wave's 64 rows and token 32 j + lane % 32
+  float* const part = wa.k_splits > 1 ? wa.part + (size_t)blockIdx.z * (size_t)a.n_tokens * (size_t)a.rows : nullptr;
 #pragma unroll
-  for (int i = 0; i < kBlocks; ++i) {
+  for (int j = 0; j < 2; ++j) {
+    const long long n = nb0 + 64 * th + 32 * j + (lane & 31);
+    if (n >= a.n_tokens) continue;
 #pragma unroll
-    for (int grp = 0; grp < 4; ++grp) {
-      const int m = r * kTM + 32 * i + 8 * grp + 4 * (lane >> 5);
-      uint16_t hh[4];
+    for (int i = 0; i < 2; ++i) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) hh[e] = __half_as_ushort(__float2half_rn(acc[i][4 * grp + e]));
-      if (a.y_vec && m + 3 < a.rows) {
-        *reinterpret_cast<uint2*>(yrow + m) =
-            make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
-      } else {
+      for (int grp = 0; grp < 4; ++grp) {
+        const int m = r * kTM + 64 * rq + 32 * i + 8 * grp + 4 * (lane >> 5);
+        if (part) {
+          float* const prow = part + n * (long long)a.rows;
+          if (a.y_vec && m + 3 < a.rows) {
+            *reinterpret_cast<float4*>(prow + m) = make_float4(acc[i][j][4 * grp], acc[i][j][4 * grp + 1],
+                                                               acc[i][j][4 * grp + 2], acc[i][j][4 * grp + 3]);
+          } else {
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (m + e < a.rows) yrow[m + e] = hh[e];
+            for (int e = 0; e < 4; ++e)
+              if (m + e < a.rows) prow[m + e] = acc[i][j][4 * grp + e];
+          }
+          continue;
+        }
+        uint16_t* const yrow = a.y + n * (long long)a.rows;
+        uint16_t hh[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hh[e] = __half_as_ushort(__float2half_rn(acc[i][j][4 * grp + e]));
+        if (a.y_vec && m + 3 < a.rows) {
+          *reinterpret_cast<uint2*>(yrow + m) =
+              make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (m + e < a.rows) yrow[m + e] = hh[e];
+        }
       }
+    }
+  }
+}
+
+// Y = fp16(sum over the splits of part[z]), the splits added in order
+// (z = 0, 1, ...), so the result does not depend on timing. Four outputs
+// per lane when the element count is a multiple of 4.
+__global__ __launch_bounds__(256) void spmm_reduce_kernel(const float* __restrict__ part, int k_splits, long long count,
+                                                          uint16_t* __restrict__ y) {
+  const long long stride = (long long)gridDim.x * 256;
+  if ((count & 3) == 0) {
+    const long long n4 = count >> 2;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n4; i += stride) {
+      float4 s = reinterpret_cast<const float4*>(part)[i];
+      for (int z = 1; z < k_splits; ++z) {
+        const float4 p = reinterpret_cast<const float4*>(part + (size_t)z * (size_t)count)[i];
+        s.x += p.x;
+        s.y += p.y;
+        s.z += p.z;
+        s.w += p.w;
+      }
+      const uint32_t lo = __half_as_ushort(__float2half_rn(s.x)) | ((uint32_t)__half_as_ushort(__float2half_rn(s.y)) << 16);
+      const uint32_t hi = __half_as_ushort(__float2half_rn(s.z)) | ((uint32_t)__half_as_ushort(__float2half_rn(s.w)) << 16);
+      reinterpret_cast<uint2*>(y)[i] = make_uint2(lo, hi);
+    }
+  } else {
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < count; i += stride) {
+      float s = part[i];
+      for (int z = 1; z < k_splits; ++z) s += part[(size_t)z * (size_t)count + i];
+      y[i] = __half_as_ushort(__float2half_rn(s));
     }
   }
 }
 
 int hip_fail(hipError_t e, const char* what) {
   return spdp::fail(SPDP_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// The split-K partial sums of the prefill product: grown on demand, the
+// old buffer kept until the handle is freed (a captured graph may still
+// name it); no allocation while the stream is being captured.
+int ensure_spmm_part(spdp_matrix* h, size_t bytes, hipStream_t stream) {
+  if (bytes <= h->spmm_part_bytes) return SPDP_OK;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cs);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+  if (cs != hipStreamCaptureStatusNone)
+    return spdp::fail(SPDP_ERR_INVALID_ARG,
+                      "the prefill split-K workspace is too small for this token count and the stream is "
+                      "capturing; call spdp_spmm once with at least as many tokens before the capture");
+  void* p = nullptr;
+  e = hipMalloc(&p, bytes);
+  if (e != hipSuccess)
+    return e == hipErrorOutOfMemory ? spdp::fail(SPDP_ERR_OOM, "hipMalloc of the prefill workspace failed")
+                                    : hip_fail(e, "hipMalloc");
+  if (h->d_spmm_part) h->retired.push_back(h->d_spmm_part);
+  h->d_spmm_part = p;
+  h->spmm_part_bytes = bytes;
+  return SPDP_OK;
 }
 
 }  // namespace
@@ -444,12 +603,52 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
   a.steps = (int)(h->n_colblocks * h->tile_k / kKStep);
   a.x_vec = h->cols % 8 == 0;
   a.y_vec = h->rows % 4 == 0;
-  const dim3 grid((unsigned)h->n_stripes, (unsigned)((n_tokens + kBN - 1) / kBN));
-  // the pipelined form for 256 x 16 GTiles and 16-byte X rows; the plain one otherwise
-  if (h->tile_k == kKStep && a.x_vec)
-    hipLaunchKernelGGL(spmm_ring_kernel, grid, dim3(kWaves * 64), 0, static_cast<hipStream_t>(stream), a);
-  else
-    hipLaunchKernelGGL(spmm_kernel, grid, dim3(kWaves * 64), 0, static_cast<hipStream_t>(stream), a);
+  const long long tok_tiles = (n_tokens + kBN - 1) / kBN;
+  auto st = static_cast<hipStream_t>(stream);
+  // SPDP_SPMM_FORM=1 forces the plain form (a testing aid)
+  int form = 0;
+  if (const char* env = std::getenv("SPDP_SPMM_FORM")) form = std::atoi(env);
+  if (h->tile_k == kKStep && a.x_vec && form != 1) {
+    // split K when the (stripe, 128-token tile) grid leaves CUs idle, at
+    // least 8 GTiles per split, and so that a split's TileOffsets fit the
+    // LDS table
+    const int ncb = (int)h->n_colblocks;
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    const long long wgs = h->n_stripes * tok_tiles;
+    long long k = wgs < cus ? std::min<long long>(8, (cus + wgs - 1) / wgs) : 1;
+    k = std::min<long long>(k, std::max(1, ncb / 8));
+    if (const char* env = std::getenv("SPDP_SPMM_SPLITS")) k = std::max(1, std::atoi(env));
+    k = std::max<long long>(k, (ncb + kToCap - 2) / (kToCap - 1));
+    k = std::min<long long>(k, ncb);
+    const int sps = (int)((ncb + k - 1) / k);
+    k = (ncb + sps - 1) / sps;  // every split non-empty
+    if (k > 65535) return fail(SPDP_ERR_UNSUPPORTED, "the width needs more than 65535 splits");
+    WsArgs wa;
+    wa.s = a;
+    wa.k_splits = (int)k;
+    wa.sps = sps;
+    wa.part = nullptr;
+    if (k > 1) {
+      const size_t bytes = (size_t)k * (size_t)n_tokens * (size_t)h->rows * sizeof(float);
+      const int st_ok = ensure_spmm_part(h, bytes, st);
+      if (st_ok != SPDP_OK) return st_ok;
+      wa.part = static_cast<float*>(h->d_spmm_part);
+    }
+    hipLaunchKernelGGL(spmm_ws_kernel, dim3((unsigned)h->n_stripes, (unsigned)tok_tiles, (unsigned)k),
+                       dim3(kWsWaves * 64), 0, st, wa);
+    if (k > 1) {
+      e = hipGetLastError();
+      if (e != hipSuccess) return hip_fail(e, "kernel launch");
+      const long long count = n_tokens * h->rows;
+      const long long per = (count & 3) == 0 ? count / 4 : count;
+      const unsigned blocks = (unsigned)std::min<long long>(8192, (per + 255) / 256);
+      hipLaunchKernelGGL(spmm_reduce_kernel, dim3(blocks), dim3(256), 0, st, wa.part, (int)k, count, Y);
+    }
+  } else {
+    hipLaunchKernelGGL(spmm_kernel, dim3((unsigned)h->n_stripes, (unsigned)tok_tiles), dim3(kWaves * 64), 0, st, a);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;

@@ -9,7 +9,12 @@ cores from the same Tiled-CBC handle the decode path uses. Checked against
 * dyadic inputs (weights k 2^-9, tokens j / 4) on which every fp32 sum is
   exact in any order, so Y must equal fp16(y64) bit for bit on every row;
 * ragged rows, columns that are not a multiple of 8, token counts that are
-  not a multiple of the 128-token workgroup tile, tile_k 16/32/64.
+  not a multiple of the 128-token workgroup tile, tile_k 16/32/64;
+* both kernel forms (the plain one forced with SPDP_SPMM_FORM=1) and the
+  split-K path of the warp-specialized form (forced split counts with
+  SPDP_SPMM_SPLITS, and a width whose TileOffsets need several splits),
+  bit for bit; graph capture with the split-K workspace, and its refusal
+  to grow the workspace inside a capture.
 """
 
 import ctypes
@@ -141,6 +146,77 @@ def test_spmm_full_size_realistic(rows, cols, sw, n):
     label = f"spmm {rows}x{cols} sw={sw} N={n}"
     print(f"[gpu] {label}", flush=True)
     _assert_close(_run(m, x), w, x, label)
+    m.close()
+
+
+FORCED = [
+    ({"SPDP_SPMM_FORM": "1"}, (1000, 1536, 0.5, 200)),
+    ({"SPDP_SPMM_FORM": "1"}, (4096, 4096, 0.5, 300)),
+    ({"SPDP_SPMM_SPLITS": "1"}, (1024, 1024, 0.5, 256)),
+    ({"SPDP_SPMM_SPLITS": "3"}, (700, 1000, 0.6, 129)),
+    ({"SPDP_SPMM_SPLITS": "5"}, (4096, 4096, 0.5, 512)),
+    ({"SPDP_SPMM_SPLITS": "1000"}, (333, 520, 0.5, 40)),  # clamped to one GTile per split
+]
+
+
+@pytest.mark.parametrize("env,shape", FORCED, ids=[f"{list(e.items())[0][0]}={list(e.items())[0][1]}-{s[0]}x{s[1]}"
+                                                   for e, s in FORCED])
+def test_spmm_forced_forms_exact(env, shape, monkeypatch):
+    rows, cols, sw, n = shape
+    for k, v in env.items():
+        monkeypatch.setenv(k, v)
+    w, x = _dyadic(rows, cols, n, rows + 5 * cols + n, sw)
+    m = spdp.encode(w, (256, 16))
+    label = f"spmm exact {rows}x{cols} N={n} {env}"
+    print(f"[gpu] {label}", flush=True)
+    _assert_bits(_run(m, x), w, x, label)
+    m.close()
+
+
+def test_spmm_wide_needs_several_splits():
+    # 40000 columns: 2500 GTiles per stripe, more than one split's LDS table
+    # of TileOffsets holds, so the product is split over K whatever the grid
+    # (every partial sum < 2^12 in multiples of 2^-11: exact in fp32)
+    w, x = _dyadic(300, 40000, 70, 17, 0.5)
+    m = spdp.encode(w, (256, 16))
+    print("[gpu] spmm exact 300x40000 N=70", flush=True)
+    _assert_bits(_run(m, x), w, x, "spmm 300x40000")
+    m.close()
+
+
+def test_spmm_split_workspace_not_grown_in_capture():
+    dev = _dev()
+    w, x = _dyadic(512, 2048, 64, 23, 0.5)
+    m = spdp.encode(w, (256, 16))
+    X = _to_dev(x)
+    Y = torch.zeros((64, 512), dtype=torch.float16, device=dev)
+    s = torch.cuda.Stream(device=dev)
+    s.wait_stream(torch.cuda.current_stream(dev))
+    g = torch.cuda.CUDAGraph()
+    err = None
+    with torch.cuda.graph(g, stream=s):
+        try:
+            m.spmm_into(X, Y)  # a fresh handle: the split-K workspace would have to grow here
+        except spdp.SpdpError as e:
+            err = e
+        Y.add_(0)
+    assert err is not None and err.status == -1, "growing the workspace inside a capture must be refused"
+    g.replay()
+    torch.cuda.synchronize()
+    # eager first, then the same call captured: no growth, the graph replays it
+    m.spmm_into(X, Y)
+    torch.cuda.synchronize()
+    ref = Y.clone()
+    _assert_bits(ref, w, x, "eager after refusal")
+    g2 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g2, stream=s):
+        m.spmm_into(X, Y)
+    for _ in range(3):
+        Y.fill_(float("nan"))
+        g2.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(Y, ref)
+    del g, g2
     m.close()
 
 
