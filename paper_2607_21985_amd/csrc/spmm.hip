@@ -505,6 +505,219 @@ __global__ __launch_bounds__(kWsWaves * 64) void spmm_ws_kernel(WsArgs wa) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// 256-token form of the warp-specialized kernel: the expansion of a GTile
+// is an instruction stream of fixed length whatever the token count, so a
+// workgroup of 256 tokens pays it once for twice the MFMA work. Twelve
+// waves (three per SIMD: two multiplying, one expanding):
+//   * multiplying wave m (0-7): rows 64 (m & 3) .., tokens 128 (m >> 2) ..
+//     of the 256 x 256 output tile (2 x 4 blocks of 32 x 32, 128
+//     accumulators); per step one 16-byte DMA of values (8 x 64 lanes x 16
+//     bytes: a dense GTile) and one of X (tokens 32 m .. 32 m + 31);
+//   * expanding wave d (8-11): columns 4d .. 4d + 3 (sixteen bitmap words,
+//     scalar loads two steps ahead); it also warms L2 for its own scalar
+//     loads (a DMA of the words it will load, into a scratch area, never
+//     waited for).
+// The two roles run separate loops with the same number of barriers, so
+// neither role's registers are held across the other's code.
+
+constexpr int kW256Waves = 12;
+constexpr int kW256Ring = 8;
+constexpr int kBN256 = 256;
+constexpr int kX256Bytes = kBN256 * kKStep * 2;
+constexpr int kG256Bytes = kValBytes + kX256Bytes;
+
+__global__ __launch_bounds__(kW256Waves * 64) void spmm_ws256_kernel(WsArgs wa) {
+  const SpmmArgs& a = wa.s;
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kW256Ring][kG256Bytes];
+  __shared__ __attribute__((aligned(16))) unsigned char tile[2][kTileBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char warm[1024];
+  __shared__ uint32_t toff[kToCap];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int r = blockIdx.x;
+  const long long nb0 = (long long)blockIdx.y * kBN256;
+  const int c0 = (int)blockIdx.z * wa.sps;
+  const int steps = min(wa.sps, a.n_colblocks - c0);
+  const uint32_t g0 = (uint32_t)r * (uint32_t)a.n_colblocks;
+  for (int i = threadIdx.x; i <= steps; i += kW256Waves * 64) toff[i] = a.tile_offset[g0 + (uint32_t)(c0 + i)];
+  __syncthreads();
+  constexpr int R = kW256Ring;
+  const int steady_end = steps - R;
+
+  if (wave < 8) {
+    // ---- multiplying waves
+    const int mw = wave;
+    const int khalf = (lane >> 5) * 8;
+    const int rq = mw & 3, th = mw >> 2;
+    const long long left = a.n_tokens - nb0;
+    const int xt = 32 * mw + (lane >> 1);
+    const uint16_t* const xsrc = a.x + nb0 * (long long)a.cols;
+    const uint32_t x_off = (uint32_t)((xt < left ? xt : left - 1) * (long long)a.cols * 2) + 16u * (uint32_t)(lane & 1);
+    const uint32_t q16 = 16u * (uint32_t)(mw * 64 + lane);
+    auto issue = [&](int s) __attribute__((always_inline)) {
+      const uint32_t c = (uint32_t)(c0 + s);
+      const uint32_t slot = lds_addr(ring[s & (R - 1)]);
+      const uint32_t t0 = toff[s], t1 = toff[s + 1];
+      const int span = 2 * (int)(t1 - t0) - 16;
+      const uint32_t voff = 2u * t0 + min(q16, (uint32_t)max(span, 0));
+      asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" ::"v"(voff), "s"(a.values),
+                   "{m0}"((uint32_t)__builtin_amdgcn_readfirstlane((int)(slot + 1024u * (uint32_t)mw)))
+                   : "memory");
+      uint32_t off = x_off + c * (2u * kKStep);
+      if (c * kKStep + 8u * (uint32_t)(lane & 1) >= (uint32_t)a.cols) off = x_off - 16u * (uint32_t)(lane & 1);
+      dma16(xsrc, off, (uint32_t)__builtin_amdgcn_readfirstlane((int)(slot + kValBytes + 1024u * (uint32_t)mw)));
+    };
+    float16v acc[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = float16v{};
+    const half8 none = half8{0, 0, 0, 0, 0, 0, 0, 0};
+    auto step = [&](int s, auto steady) __attribute__((always_inline)) {
+      constexpr bool kSteady = decltype(steady)::value;
+      const unsigned char* slot = ring[s & (R - 1)];
+      const unsigned char* t = tile[s & 1];
+      half8 av[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const unsigned char* p = t + (64 * rq + 32 * i + (lane & 31)) * kRowBytes + 2 * khalf;
+        const uint2 lo = *reinterpret_cast<const uint2*>(p);
+        const uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
+        av[i] = __builtin_bit_cast(half8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      }
+      const bool zero_b = !kSteady && (c0 + s) * kKStep + khalf >= a.cols;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        half8 b = *reinterpret_cast<const half8*>(slot + kValBytes + (128 * th + 32 * j + (lane & 31)) * 32 + 2 * khalf);
+        if (zero_b) b = none;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(av[i], b, acc[i][j], 0, 0, 0);
+      }
+      if (kSteady || s + R - 1 < steps) issue(s + R - 1);
+      if constexpr (kSteady)
+        wait_vmcnt<kWsDma * (R - 3)>();
+      else if (s + 2 < steps)
+        wait_steps<R - 3>(min(R - 3, steps - 1 - (s + 2)));
+      __syncthreads();
+    };
+    for (int s = 0; s < R - 1 && s < steps; ++s) issue(s);
+    wait_steps<R - 2>(min(R - 2, steps - 1));
+    __syncthreads();
+    if (steps > 1) wait_steps<R - 3>(min(R - 3, steps - 2));
+    __syncthreads();
+    int s = 0;
+    for (; s < steady_end; ++s) step(s, std::integral_constant<bool, true>{});
+    for (; s < steps; ++s) step(s, std::integral_constant<bool, false>{});
+
+    float* const part = wa.k_splits > 1 ? wa.part + (size_t)blockIdx.z * (size_t)a.n_tokens * (size_t)a.rows : nullptr;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const long long n = nb0 + 128 * th + 32 * j + (lane & 31);
+      if (n >= a.n_tokens) continue;
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int m = r * kTM + 64 * rq + 32 * i + 8 * grp + 4 * (lane >> 5);
+          if (part) {
+            float* const prow = part + n * (long long)a.rows;
+            if (a.y_vec && m + 3 < a.rows) {
+              *reinterpret_cast<float4*>(prow + m) = make_float4(acc[i][j][4 * grp], acc[i][j][4 * grp + 1],
+                                                                 acc[i][j][4 * grp + 2], acc[i][j][4 * grp + 3]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                if (m + e < a.rows) prow[m + e] = acc[i][j][4 * grp + e];
+            }
+            continue;
+          }
+          uint16_t* const yrow = a.y + n * (long long)a.rows;
+          uint16_t hh[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) hh[e] = __half_as_ushort(__float2half_rn(acc[i][j][4 * grp + e]));
+          if (a.y_vec && m + 3 < a.rows) {
+            *reinterpret_cast<uint2*>(yrow + m) =
+                make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (m + e < a.rows) yrow[m + e] = hh[e];
+          }
+        }
+      }
+    }
+  } else {
+    // ---- expanding waves
+    const int d = wave - 8;
+    struct Meta {
+      uint64_t w[16];  // column 4d + jj: words 4 jj .. 4 jj + 3
+      uint32_t ci[4];
+    };
+    const const_ptr<uint64_t> bm_s = (const_ptr<uint64_t>)a.bitmap;
+    const const_ptr<uint32_t> ci_s = (const_ptr<uint32_t>)a.col_info;
+    auto load_meta = [&](int s, Meta& m) __attribute__((always_inline)) {
+      const uint32_t col0 = (g0 + (uint32_t)(c0 + s)) * (uint32_t)kKStep + 4u * (uint32_t)d;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) m.w[i] = bm_s[(size_t)col0 * 4 + i];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) m.ci[i] = ci_s[col0 + i];
+    };
+    // the words (128 bytes: two lanes of 64) and ColInfo (16 bytes) of step
+    // s into L2, landing in a scratch area nobody reads
+    auto warm_up = [&](int s) __attribute__((always_inline)) {
+      const uint32_t col0 = (g0 + (uint32_t)(c0 + s)) * (uint32_t)kKStep + 4u * (uint32_t)d;
+      dma4(a.bitmap, col0 * 32u + 4u * (uint32_t)(lane & 31), lds_addr(warm) + 256u * (uint32_t)d);
+      dma4(a.col_info, col0 * 4u + 4u * (uint32_t)(lane & 3), lds_addr(warm) + 256u * (uint32_t)d);
+    };
+    auto decode = [&](int s, const Meta& m) __attribute__((always_inline)) {
+      const uint32_t vb = lds_addr(ring[s & (R - 1)]);
+      unsigned char* t = tile[s & 1];
+      uint32_t hv[4][4];  // [column][word]
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) {
+        uint32_t sb = vb + 2u * (m.ci[jj] >> 16);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          hv[jj][v] = *(const __attribute__((address_space(3))) uint16_t*)(uintptr_t)(sb + 2u * mbcnt64(m.w[4 * jj + v]));
+          if (v < 3) {
+            const uint32_t pop = (uint32_t)__builtin_popcountll(m.w[4 * jj + v]);
+            asm("s_lshl1_add_u32 %0, %1, %0" : "+s"(sb) : "s"(pop) : "scc");
+          }
+        }
+      }
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        *reinterpret_cast<uint2*>(t + (64 * v + lane) * kRowBytes + 8 * d) =
+            make_uint2(pair_select(hv[0][v], hv[1][v], m.w[v], m.w[4 + v]),
+                       pair_select(hv[2][v], hv[3][v], m.w[8 + v], m.w[12 + v]));
+    };
+    auto step = [&](int s, Meta& cur, Meta& next, auto steady) __attribute__((always_inline)) {
+      constexpr bool kSteady = decltype(steady)::value;
+      if (kSteady || s + 4 < steps) warm_up(s + 4);
+      if (kSteady || s + 2 < steps) load_meta(s + 2, next);
+      if (kSteady || s + 1 < steps) decode(s + 1, cur);
+      __syncthreads();
+    };
+    Meta ma, mb;
+    for (int s = 0; s < 4 && s < steps; ++s) warm_up(s);
+    load_meta(0, ma);
+    if (steps > 1) load_meta(1, mb);
+    __syncthreads();
+    decode(0, ma);
+    __syncthreads();
+    int s = 0;
+    for (; s + 1 < steady_end; s += 2) {
+      step(s, mb, ma, std::integral_constant<bool, true>{});
+      step(s + 1, ma, mb, std::integral_constant<bool, true>{});
+    }
+    for (; s < steps; s += 2) {
+      step(s, mb, ma, std::integral_constant<bool, false>{});
+      if (s + 1 < steps) step(s + 1, ma, mb, std::integral_constant<bool, false>{});
+    }
+  }
+}
+
 // Y = fp16(sum over the splits of part[z]), the splits added in order
 // (z = 0, 1, ...), so the result does not depend on timing. Four outputs
 // per lane when the element count is a multiple of 4.
@@ -605,18 +818,24 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
   a.y_vec = h->rows % 4 == 0;
   const long long tok_tiles = (n_tokens + kBN - 1) / kBN;
   auto st = static_cast<hipStream_t>(stream);
-  // SPDP_SPMM_FORM=1 forces the plain form (a testing aid)
+  // SPDP_SPMM_FORM (a testing aid): 1 the plain form, 2 the 128-token
+  // warp-specialized form, 3 the 256-token one
   int form = 0;
   if (const char* env = std::getenv("SPDP_SPMM_FORM")) form = std::atoi(env);
   if (h->tile_k == kKStep && a.x_vec && form != 1) {
-    // split K when the (stripe, 128-token tile) grid leaves CUs idle, at
-    // least 8 GTiles per split, and so that a split's TileOffsets fit the
-    // LDS table
+    // 256-token workgroups when their grid still covers half the CUs (the
+    // expansion of a GTile is paid once per workgroup; with fewer, the
+    // deeper split costs more than the expansion saves); split K when the
+    // (stripe, token tile) grid leaves CUs idle, at least 8 GTiles per
+    // split, and so that a split's TileOffsets fit the LDS table
     const int ncb = (int)h->n_colblocks;
     int cus = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
-    const long long wgs = h->n_stripes * tok_tiles;
+    const long long tiles256 = (n_tokens + kBN256 - 1) / kBN256;
+    const bool wide = form == 3 || (form != 2 && n_tokens > kBN && 2 * h->n_stripes * tiles256 >= cus);
+    const long long tiles = wide ? tiles256 : tok_tiles;
+    const long long wgs = h->n_stripes * tiles;
     long long k = wgs < cus ? std::min<long long>(8, (cus + wgs - 1) / wgs) : 1;
     k = std::min<long long>(k, std::max(1, ncb / 8));
     if (const char* env = std::getenv("SPDP_SPMM_SPLITS")) k = std::max(1, std::atoi(env));
@@ -636,8 +855,11 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
       if (st_ok != SPDP_OK) return st_ok;
       wa.part = static_cast<float*>(h->d_spmm_part);
     }
-    hipLaunchKernelGGL(spmm_ws_kernel, dim3((unsigned)h->n_stripes, (unsigned)tok_tiles, (unsigned)k),
-                       dim3(kWsWaves * 64), 0, st, wa);
+    const dim3 grid((unsigned)h->n_stripes, (unsigned)tiles, (unsigned)k);
+    if (wide)
+      hipLaunchKernelGGL(spmm_ws256_kernel, grid, dim3(kW256Waves * 64), 0, st, wa);
+    else
+      hipLaunchKernelGGL(spmm_ws_kernel, grid, dim3(kWsWaves * 64), 0, st, wa);
     if (k > 1) {
       e = hipGetLastError();
       if (e != hipSuccess) return hip_fail(e, "kernel launch");

@@ -10,7 +10,8 @@ cores from the same Tiled-CBC handle the decode path uses. Checked against
   exact in any order, so Y must equal fp16(y64) bit for bit on every row;
 * ragged rows, columns that are not a multiple of 8, token counts that are
   not a multiple of the 128-token workgroup tile, tile_k 16/32/64;
-* both kernel forms (the plain one forced with SPDP_SPMM_FORM=1) and the
+* every kernel form (SPDP_SPMM_FORM=1 the plain one, 2 and 3 the 128- and
+  256-token warp-specialized ones; the default picks by token count) and the
   split-K path of the warp-specialized form (forced split counts with
   SPDP_SPMM_SPLITS, and a width whose TileOffsets need several splits),
   bit for bit; graph capture with the split-K workspace, and its refusal
@@ -150,6 +151,10 @@ def test_spmm_full_size_realistic(rows, cols, sw, n):
 
 
 FORCED = [
+    ({"SPDP_SPMM_FORM": "2"}, (1000, 1536, 0.5, 300)),
+    ({"SPDP_SPMM_FORM": "2"}, (4096, 4096, 0.6, 512)),
+    ({"SPDP_SPMM_FORM": "3"}, (700, 1000, 0.5, 100)),
+    ({"SPDP_SPMM_FORM": "3"}, (4096, 4096, 0.5, 700)),
     ({"SPDP_SPMM_FORM": "1"}, (1000, 1536, 0.5, 200)),
     ({"SPDP_SPMM_FORM": "1"}, (4096, 4096, 0.5, 300)),
     ({"SPDP_SPMM_SPLITS": "1"}, (1024, 1024, 0.5, 256)),
