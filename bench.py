@@ -80,6 +80,8 @@ def parse(argv=None):
                     help="skip the other workloads (single layer, 7B MLP, 13B layer, 70B slice)")
     ap.add_argument("--secondary-steps", type=int, default=12)
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefill products (spdp_spmm)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="run only the prefill products and print them as one JSON line")
     ap.add_argument("--profile-only", action="store_true",
                     help="run warmup + timed steps only (for rocprofv3 runs)")
     ap.add_argument("--calib-read-mib", type=int, default=0,
@@ -709,6 +711,7 @@ SECONDARY = [
     ("llama70b-layer", 0.7, 0.5, [1, 8, 32]),
     ("llama70b-layer", 0.5, 0.0, [1, 8, 32]),
     ("llama70b-layer", 0.8, 0.7, [1]),
+    ("llama70b-tp8", 0.7, 0.5, [1, 8]),
 ]
 
 
@@ -775,15 +778,18 @@ def prefill(B, args, steps=10):
         mats = [spdp.encode(w, (256, 16)) for _ in range(2)]
         X = B.to_dev(proj.activations(n, draw=2))
         Ys = [torch.empty((n, proj.rows), dtype=torch.float16, device=B.dev) for _ in range(2)]
+        Wd = [B.to_dev(w16) for _ in range(2)]
         for i in range(2):
+            # eager calls first: the split-K workspace and the dense library's
+            # state are set up outside the captures
             mats[i].spmm_into(X, Ys[i])
+            F.linear(X, Wd[i])
         B.sync()
         g = B.capture(lambda: [mats[i % 2].spmm_into(X, Ys[i % 2]) for i in range(steps)])
         g.replay()
         B.sync()
         ms = B.timed(lambda _: g.replay(), 3) / (3 * steps)
         del g
-        Wd = [B.to_dev(w16) for _ in range(2)]
         gd = B.capture(lambda: [F.linear(X, Wd[i % 2]) for i in range(steps)])
         gd.replay()
         B.sync()
@@ -827,6 +833,9 @@ def main():
         sys.exit(2)
     B = Bench(args.launch)
     spdp, synth = B.spdp, B.synth
+    if args.prefill_only:
+        print(json.dumps({"prefill_only": True, "prefill": prefill(B, args)}), flush=True)
+        return
     wl = synth.workload(args.workload)
     tile = wl["tile"]
     batch = args.batch if args.batch is not None else wl["batch"][0]
@@ -1024,11 +1033,38 @@ def _cmd(kind, d, tag, pj, extra=""):
             + " ".join(pj["argv"]) + f" > {d}/{kind}_{tag}.log")
 
 
+def summarize_prefill(d, prof_dir):
+    """profiles/spmm_prefill_kernel_trace.txt: the prefill kernels' durations
+    under rocprofv3 next to what bench.py --prefill-only timed in the same run."""
+    with open(os.path.join(d, "trace_prefill.log")) as fh:
+        pj = next(json.loads(l) for l in fh if l.startswith("{") and "prefill_only" in l)
+    rows = list(csv.DictReader(open(os.path.join(d, "trace_prefill", "run_kernel_stats.csv"))))
+    out = ["# spdp_spmm (prefill) kernels", "", "command (GPU box, repository root, TMPDIR=/tmp):",
+           f"  rocprofv3 --kernel-trace --stats --output-format csv -d {d}/trace_prefill -o run -- "
+           f"python3 bench.py --prefill-only > {d}/trace_prefill.log", "",
+           "kernel_stats (durations in ns):", "Name | Calls | AverageNs | MinNs | MaxNs"]
+    for r in rows:
+        out.append(f"{r['Name'].replace('(anonymous namespace)::', '')[:70]} | {r['Calls']} | "
+                   f"{float(r['AverageNs']):.1f} | {r['MinNs']} | {r['MaxNs']}")
+    out += ["", "bench.py --prefill-only (same run; graph replays, two encoded copies alternating):",
+            "projection | tokens | us per call | MFMA TFLOP/s executed | frac of 2500 | dense us | vs dense"]
+    for e in pj["prefill"]:
+        out.append(f"{e['projection']} | {e['tokens']} | {e['us_per_call']} | {e['mfma_tflops']} | "
+                   f"{e['roofline']['frac']} | {e['dense_us_per_call']} | {e['speedup_vs_dense']}")
+    out += [f"spmm_sha: {kernel_source_sha(open(os.path.join(ROOT, 'paper_2607_21985_amd', 'csrc', 'spmm.hip')).read())}",
+            ""]
+    with open(os.path.join(prof_dir, "spmm_prefill_kernel_trace.txt"), "w") as fh:
+        fh.write("\n".join(out))
+    print("\n".join(out))
+
+
 def summarize_profiles(d, prof_dir=None):
     sha = kernel_source_sha()
     prof_dir = prof_dir or os.path.join(ROOT, "profiles")
+    if os.path.isdir(os.path.join(d, "trace_prefill")):
+        summarize_prefill(d, prof_dir)
     tags = sorted(n[len("trace_"):] for n in os.listdir(d)
-                  if n.startswith("trace_") and os.path.isdir(os.path.join(d, n)))
+                  if n.startswith("trace_") and os.path.isdir(os.path.join(d, n)) and n != "trace_prefill")
     for tag in tags:
         pj = _profile_line(os.path.join(d, f"trace_{tag}.log"))
         rows = list(csv.DictReader(open(os.path.join(d, f"trace_{tag}", "run_kernel_stats.csv"))))

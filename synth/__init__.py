@@ -98,7 +98,7 @@ def _proj(name, rows, cols, ws, xs, kind="laplace"):
     return Projection(name, rows, cols, ws, xs, kind)
 
 
-# The five workloads: shapes, sweeps and seeds. Tile shapes are the paper's
+# The five workloads and one tensor-parallel shard: shapes, sweeps and seeds. Tile shapes are the paper's
 # 256 x 16 GTile (Sec. 4.1, 4.2.3) except the small single-layer case.
 WORKLOADS = {
     "single-1024": dict(
@@ -138,6 +138,21 @@ WORKLOADS = {
         weight_sparsity=[0.5, 0.6, 0.7, 0.8],
         act_sparsity=[0.0, 0.1, 0.2, 0.3, 0.4, 0.5, 0.6, 0.7],
         batch=[1, 2, 4, 8, 16, 32], tile=(256, 16)),
+    # one GPU's share of the Llama-70B layer under 8-way tensor parallelism:
+    # q/k/v and gate/up split their output rows (64 query heads and 8 key /
+    # value heads of 128 over 8 GPUs), o and down their input columns; x is
+    # the full layer input, o and down read the local attention output and
+    # the local SwiGLU activations
+    "llama70b-tp8": dict(
+        projections=[_proj("q", 1024, 8192, 601, 611),
+                     _proj("k", 128, 8192, 602, 611),
+                     _proj("v", 128, 8192, 603, 611),
+                     _proj("o", 8192, 1024, 604, 612),
+                     _proj("gate", 3584, 8192, 605, 613),
+                     _proj("up", 3584, 8192, 606, 613),
+                     _proj("down", 8192, 3584, 607, 614, "swiglu")],
+        weight_sparsity=[0.7], act_sparsity=[0.5],
+        batch=[1, 8, 32], tile=(256, 16)),
 }
 
 

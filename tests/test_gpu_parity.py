@@ -416,7 +416,7 @@ def _check_all_rows(m, w, x, t, label, block=2048):
 
 
 FULL = []
-for name in ("llama7b-attn", "llama7b-mlp", "llama13b-layer", "llama70b-layer"):
+for name in ("llama7b-attn", "llama7b-mlp", "llama13b-layer", "llama70b-layer", "llama70b-tp8"):
     wl = synth.workload(name)
     seen = set()
     for proj in wl["projections"]:
