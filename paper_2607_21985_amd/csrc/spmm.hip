@@ -240,19 +240,12 @@ constexpr int kWsDma = 2;      // loads per step of a multiplying wave
 constexpr int kToCap = 1800;   // TileOffsets of one stripe's split held in LDS
 constexpr int kGBytes = kValBytes + kXBytes;  // one GTile's values and X block in a ring slot
 
-// the lane's value of column a (low half) and of column b (high half) where
-// its bit of the column's word is set, else 0: one select per column (SDWA
-// writes one half and keeps the other)
-__device__ __forceinline__ uint32_t pair_select(uint32_t a, uint32_t b, uint64_t ma, uint64_t mb) {
-  uint32_t p;
-  asm("s_mov_b64 vcc, %[ma]\n\t"
-      "v_cndmask_b32_sdwa %[p], 0, %[a], vcc dst_sel:WORD_0 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0\n\t"
-      "s_mov_b64 vcc, %[mb]\n\t"
-      "v_cndmask_b32_sdwa %[p], 0, %[b], vcc dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0"
-      : [p] "=&v"(p)
-      : [a] "v"(a), [b] "v"(b), [ma] "s"(ma), [mb] "s"(mb)
-      : "vcc");
-  return p;
+// the lane's value where its bit of the word is set, else 0 (the word as
+// the select mask of a VOP3 select: no move through vcc)
+__device__ __forceinline__ uint32_t select_word(uint32_t v, uint64_t mask) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, 0, %1, %2" : "=v"(r) : "v"(v), "s"(mask));
+  return r;
 }
 
 // wait until at most kWsDma x `later` loads are in flight (later < N + 1)
@@ -380,7 +373,7 @@ __global__ __launch_bounds__(kWsWaves * 64) void spmm_ws_kernel(WsArgs wa) {
 #pragma unroll
     for (int v = 0; v < 4; ++v)
       *reinterpret_cast<uint32_t*>(t + (64 * v + lane) * kRowBytes + 4 * mw) =
-          pair_select(hv[0][v], hv[1][v], m.w[v], m.w[4 + v]);
+          select_word(hv[0][v], m.w[v]) | (select_word(hv[1][v], m.w[4 + v]) << 16);
   };
 
   const int rq = mw & 3, th = mw >> 2;
@@ -687,10 +680,13 @@ __global__ __launch_bounds__(kW256Waves * 64) void spmm_ws256_kernel(WsArgs wa) 
         }
       }
 #pragma unroll
-      for (int v = 0; v < 4; ++v)
+      for (int v = 0; v < 4; ++v) {
+        uint32_t sel[4];
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) sel[jj] = select_word(hv[jj][v], m.w[4 * jj + v]);
         *reinterpret_cast<uint2*>(t + (64 * v + lane) * kRowBytes + 8 * d) =
-            make_uint2(pair_select(hv[0][v], hv[1][v], m.w[v], m.w[4 + v]),
-                       pair_select(hv[2][v], hv[3][v], m.w[8 + v], m.w[12 + v]));
+            make_uint2(sel[0] | (sel[1] << 16), sel[2] | (sel[3] << 16));
+      }
     };
     auto step = [&](int s, Meta& cur, Meta& next, auto steady) __attribute__((always_inline)) {
       constexpr bool kSteady = decltype(steady)::value;
