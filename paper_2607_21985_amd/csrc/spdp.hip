@@ -324,7 +324,12 @@ __device__ __forceinline__ void spmspv_body() {
   // last 16-byte chunk}; padded to a whole batch with entries that load
   // nothing of use
   __shared__ uint2 ent_s[kMaxWgCols + kBatch];
-  __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kMaxWgCols + kBatch) * NB];
+  // the entries' masked activations: per pair of entries a row of NB dwords
+  // (token b: entry 2j in the low half, 2j + 1 in the high), from four
+  // tokens on padded by one dword so that consecutive pairs start in
+  // different banks; the MFMA form keeps each entry's NB values together
+  constexpr int kXRow = (MM || NB < 4) ? NB : NB + 1;
+  __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kMaxWgCols + kBatch) * kXRow];
   __shared__ int cnt_s[kWaves];
 
   const int lane = threadIdx.x & 63;
@@ -418,13 +423,38 @@ __device__ __forceinline__ void spmspv_body() {
     uint32_t phase_lane = 0;
     if (pass == 0)
       phase_lane = __hip_atomic_load(phase_p + r * A->phase_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-    // activity: the union of the tokens' sets, or the batch's shared set
+    // activity: the union of the tokens' sets, or the batch's shared set.
+    // From four tokens on the activations are also masked here, once per
+    // column (one compare per token gives both the token's bit and its
+    // masked value, so no per-token mask stays live in scalar registers): xm
+    // holds them two tokens to a dword (zero outside the token's set and past
+    // the batch), the registers the list entry is written from.
     uint64_t actm[kChunks];
+    constexpr bool kXm = MM || NB >= 4;
+    uint32_t xm[kChunks][kXm ? NB / 2 : 1];
     int n_w = 0;
   #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
       const bool in = 64 * c + lane < range;
       uint64_t act = 0;
+      if constexpr (kXm) {
+        // mag in (code, 0x7C00] is one unsigned compare for code in [-1, 0x7C00]
+        const uint32_t lo = (uint32_t)(code + 1), span = (uint32_t)(0x7C00 - code);
+        uint64_t any = 0;
+  #pragma unroll
+        for (int j = 0; j < NB / 2; ++j) {
+          uint32_t h[2];
+  #pragma unroll
+          for (int s = 0; s < 2; ++s) {
+            const int b = 2 * j + s;
+            const bool on = b < batch && (BMASK || (xb[c][b] & 0x7FFFu) - lo < span);
+            if constexpr (!BMASK) any |= __builtin_amdgcn_ballot_w64(on);
+            h[s] = on ? xb[c][b] : 0u;
+          }
+          xm[c][j] = h[0] | (h[1] << 16);
+        }
+        act = any & __builtin_amdgcn_ballot_w64(in);
+      }
       if constexpr (BMASK) {
         // fp32 running sum of |x| over the tokens in ascending order (NaN
         // makes it NaN, never active)
@@ -433,7 +463,7 @@ __device__ __forceinline__ void spmspv_body() {
         for (int b = 0; b < NB; ++b)
           if (b < batch) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
         act = __builtin_amdgcn_ballot_w64(in && score > batch_thr);
-      } else {
+      } else if constexpr (!kXm) {
   #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const int mag = (int)(xb[c][b] & 0x7FFFu);
@@ -463,21 +493,47 @@ __device__ __forceinline__ void spmspv_body() {
     auto ent_bitmap = [&](uint32_t y) __attribute__((always_inline)) {
       return kPow2 ? y & ~kLow : (y >> 6) * (WPC * 8u);
     };
+    // The MFMA form keeps an entry's NB activations together (NB / 8 pieces
+    // of 16 bytes, one wide store each); piece k sits at k ^ mm_swz(p), so
+    // that the eight lanes of a 16-byte store phase (consecutive entries)
+    // cover all 32 banks.
+    constexpr int kPieces = MM ? NB / 8 : 1;
+    auto mm_swz = [&](uint32_t p) __attribute__((always_inline)) {
+      return (p / (8u / kPieces)) & (uint32_t)(kPieces - 1);
+    };
     auto put = [&](int c, int p) __attribute__((always_inline)) {
       // 16-byte chunks of the column's padded values (8 fp16 or 16 codes each)
       const uint32_t chunks = Q ? ((ci[c] & 0xFFFFu) + 15u) >> 4 : ((ci[c] & 0xFFFFu) + 7u) >> 3;
       ent_s[p] = make_uint2((Q ? 1u : 2u) * (to[c] + (ci[c] >> 16)), ent_col(colx[c], chunks ? chunks - 1u : 0u));
+      if constexpr (MM) {
+        const uint32_t swz = mm_swz((uint32_t)p);
   #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const int mag = (int)(xb[c][b] & 0x7FFFu);
-        const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
-        xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+        for (int k = 0; k < kPieces; ++k)
+          *reinterpret_cast<uint4*>(&xs_s[p * NB + 8 * (k ^ swz)]) =
+              make_uint4(xm[c][4 * k], xm[c][4 * k + 1], xm[c][4 * k + 2], xm[c][4 * k + 3]);
+      } else {
+  #pragma unroll
+        for (int b = 0; b < NB; ++b) {
+          if constexpr (kXm) {
+            const uint32_t v = xm[c][b >> 1];
+            xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = (b & 1) ? (uint16_t)(v >> 16) : (uint16_t)v;
+          } else {
+            const int mag = (int)(xb[c][b] & 0x7FFFu);
+            const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
+            xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+          }
+        }
       }
     };
     auto put_zero = [&](int p) __attribute__((always_inline)) {
       ent_s[p] = make_uint2(0u, ent_col(zero_col, 0u));
+      if constexpr (MM) {
   #pragma unroll
-      for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * NB + b) * 2 + (p & 1)] = 0;
+        for (int k = 0; k < kPieces; ++k) *reinterpret_cast<uint4*>(&xs_s[p * NB + 8 * k]) = make_uint4(0u, 0u, 0u, 0u);
+      } else {
+  #pragma unroll
+        for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = 0;
+      }
     };
 
     // A batch = kBatch list entries, streamed through the wave's ring of kSlots
@@ -662,7 +718,7 @@ __device__ __forceinline__ void spmspv_body() {
           uint32_t pv[WPC];
   #pragma unroll
           for (int w = 0; w < WPC; ++w) pv[w] = pair_under_words(vb[2 * pr][w], vb[2 * pr + 1][w], m[2 * pr][w], m[2 * pr + 1][w]);
-          const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * NB * 2]);
+          const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * kXRow * 2]);
   #pragma unroll
           for (int b = 0; b < NB; ++b) {
             const uint32_t x2 = xp[b];
@@ -727,8 +783,13 @@ __device__ __forceinline__ void spmspv_body() {
           const int t = lane & 31;
           uint2 bx = make_uint2(0u, 0u);
           if (t < NB && (hl == 0 || (i & 1))) {
-            const uint32_t* xp = reinterpret_cast<const uint32_t*>(xs_s);
-            bx = make_uint2(xp[(e / 2 + 2 * hl) * NB + t], xp[(e / 2 + 2 * hl + 1) * NB + t]);
+            uint32_t h[4];
+  #pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const uint32_t p = (uint32_t)(e + 4 * hl + j);
+              h[j] = xs_s[p * NB + 8 * ((uint32_t)(t >> 3) ^ mm_swz(p)) + (t & 7)];
+            }
+            bx = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
           }
           const half4_t bop = __builtin_bit_cast(half4_t, bx);
   #pragma unroll
@@ -763,9 +824,14 @@ __device__ __forceinline__ void spmspv_body() {
   if constexpr (MM) {
     // per 32-row block: each wave's 32 x 32 accumulators to LDS as
     // [wave][token][row], then thread (row, 4 tokens) adds the waves in
-    // order 0..3 and publishes (consecutive threads, consecutive rows)
+    // order 0..3 and publishes (consecutive threads, consecutive rows). A
+    // stripe of one segment has nothing to gather: its sums are the rows'
+    // results (0 + sum, the value the gather would produce) and go straight
+    // to Y, and no partial, reducer or tag is involved.
     const int prow = threadIdx.x & 31;
     const int ptg = threadIdx.x >> 5;
+    const bool direct = n_seg == 1;
+    const int rows_d = ka->rows;
 #pragma unroll
     for (int blk = 0; blk < kMBlocks; ++blk) {
       __syncthreads();
@@ -780,11 +846,16 @@ __device__ __forceinline__ void spmspv_body() {
           float sum = 0.0f;
 #pragma unroll
           for (int wv = 0; wv < kWaves; ++wv) sum += red[(wv * 32 + b) * 32 + prow];
-          __hip_atomic_store(dst - row + 32 * blk + prow + (size_t)b * mpad, tag | __float_as_uint(sum),
-                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const int m = r * ka->tile_m + 32 * blk + prow;
+          if (!direct)
+            __hip_atomic_store(dst - row + 32 * blk + prow + (size_t)b * mpad, tag | __float_as_uint(sum),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else if (m < rows_d)
+            ka->y[(size_t)b * rows_d + m] = __half_as_ushort(__float2half_rn(0.0f + sum));
         }
       }
     }
+    if (direct) return;
   }
 #pragma unroll
   for (int b0 = 0; b0 < (MM ? 0 : NB); b0 += kSlice) {
@@ -975,8 +1046,12 @@ bool use_mfma(int batch) {
 
 // Passes per workgroup: one K range each up to 16 tokens; above, several
 // consecutive ranges per workgroup, so that the split-K partials (segments
-// x batch x rows x 8 bytes, written and read back) shrink. SPDP_PASSES
-// overrides (for tuning). A property of the batch, like the split.
+// x batch x rows x 8 bytes, written and read back) shrink. Measured per
+// product at 32 tokens, 70/50, with 1 / 2 / 4 / 8 passes: 28672x8192 185 /
+// 172 / 160 / 262 us, 8192x8192 103 / 91 / 84 / 125 us, 1024x8192 32 / 42
+// / 69 / 125 us; one pass for the narrow products alone made the Llama-70B
+// layer's grouped launches 1-2 % slower. SPDP_PASSES overrides (for
+// tuning). A property of the batch, like the split.
 int passes_for(int batch, bool codes) {
   // only the matrix-core form (fp16 values) walks several ranges
   if (codes || !use_mfma(batch)) return 1;
@@ -992,12 +1067,13 @@ void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols
   const int64_t stripes = std::max<int64_t>(1, m->n_stripes);
   auto segs = [&](int64_t wc) { return (cols + kWaves * wc - 1) / (kWaves * wc); };
   int64_t wc = kWaveCols;
-  *passes = passes_for(batch, m->value_bits < 16);
+  const bool codes = m->value_bits < 16;
   if (const char* env = std::getenv("SPDP_SPLITK")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1) {
       wc = std::min<int64_t>(kMaxWaveCols, ((cols + v * kWaves - 1) / (v * kWaves) + 15) / 16 * 16);
       *wave_cols = (int)wc;
+      *passes = passes_for(batch, codes);
       *segments = (int)((segs(wc) + *passes - 1) / *passes);
       return;
     }
@@ -1005,6 +1081,7 @@ void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols
   while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kOneRoundSegments) && wc < kMaxWaveCols) wc += 16;
   while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kOneRoundSegments) wc -= 16;
   *wave_cols = (int)wc;
+  *passes = passes_for(batch, codes);
   *segments = (int)((segs(wc) + *passes - 1) / *passes);
 }
 

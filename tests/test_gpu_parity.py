@@ -505,7 +505,7 @@ def test_batch_mask_edge_cases():
     m.close()
 
 
-@pytest.mark.parametrize("passes", ["1", "2", "3", "5"])
+@pytest.mark.parametrize("passes", ["1", "2", "3", "5", "64"])
 @pytest.mark.parametrize("batch", [8, 17, 32])
 def test_forced_passes_and_matrix_core_form(monkeypatch, passes, batch):
     """Several K ranges per workgroup (the matrix-core form at large
