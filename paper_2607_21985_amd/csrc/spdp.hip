@@ -548,15 +548,18 @@ __device__ __forceinline__ void spmspv_body() {
     auto issue_at = [&](int e0, int si) __attribute__((always_inline)) {
       const uint32_t slot = (uint32_t)__builtin_amdgcn_readfirstlane(
           (int)lds_addr(my_ring + si * kBatchBytes));
+      // the batch's entries are read before the first load is issued, so
+      // that they take one LDS round trip (a load's asm orders every later
+      // LDS read behind it: one round trip per load otherwise)
+      uint2 ev[kBatch / 2];
   #pragma unroll
-      for (int pr = 0; pr < kBatch / 2; ++pr) {
-        const uint2 e = ent_s[e0 + 2 * pr + hsel];
-        dma16(values, e.x + (min((uint32_t)q, ent_chunk(e.y)) << 4), slot + pr * 2 * kSlotBytes);
-      }
-      if (lane < 2 * WPC * kBatch) {
-        const uint2 e = ent_s[e0 + lane / (2 * WPC)];
-        dma4(bitmap, ent_bitmap(e.y) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
-      }
+      for (int pr = 0; pr < kBatch / 2; ++pr) ev[pr] = ent_s[e0 + 2 * pr + hsel];
+      const uint32_t eb = ent_s[e0 + min(lane / (2 * WPC), kBatch - 1)].y;
+  #pragma unroll
+      for (int pr = 0; pr < kBatch / 2; ++pr)
+        dma16(values, ev[pr].x + (min((uint32_t)q, ent_chunk(ev[pr].y)) << 4), slot + pr * 2 * kSlotBytes);
+      if (lane < 2 * WPC * kBatch)
+        dma4(bitmap, ent_bitmap(eb) + 4u * (uint32_t)(lane % (2 * WPC)), slot + kBatch * kSlotBytes);
     };
 
     // ---- 2a. (when the launch asks for it) the wave's first batch: its own
@@ -792,11 +795,18 @@ __device__ __forceinline__ void spmspv_body() {
             bx = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
           }
           const half4_t bop = __builtin_bit_cast(half4_t, bx);
+          // the A operands are read together (one LDS round trip; the empty
+          // asm keeps the compiler from interleaving each read with its
+          // multiply)
+          uint2 av[kMBlocks];
   #pragma unroll
-          for (int blk = 0; blk < kMBlocks; ++blk) {
-            const uint2 av = *reinterpret_cast<const uint2*>(mt + (32 * blk + t) * kMRowBytes + 8 * hl);
-            macc[blk] = __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(half4_t, av), bop, macc[blk], 0, 0, 0);
-          }
+          for (int blk = 0; blk < kMBlocks; ++blk)
+            av[blk] = *reinterpret_cast<const uint2*>(mt + (32 * blk + t) * kMRowBytes + 8 * hl);
+  #pragma unroll
+          for (int blk = 0; blk < kMBlocks; ++blk) asm volatile("" ::"v"(av[blk]));
+  #pragma unroll
+          for (int blk = 0; blk < kMBlocks; ++blk)
+            macc[blk] = __builtin_amdgcn_mfma_f32_32x32x8f16(__builtin_bit_cast(half4_t, av[blk]), bop, macc[blk], 0, 0, 0);
         }
       }
       if (i + kSlots < n_mine) {
