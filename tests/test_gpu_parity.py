@@ -205,6 +205,60 @@ def test_negative_zero_threshold_and_ties():
         _check_full(w, x, t, (256, 16), f"ties t={t}")
 
 
+# Activations at the threshold code's edges for every kernel form: the
+# one-token and two-token forms test each token's magnitude per column; from
+# four tokens on (and in the matrix-core form above 16 tokens) the masks are
+# taken from one unsigned compare per token, which must agree with
+# (code, 0x7C00] at code = -1 (t < 0: every non-NaN value, +-0 included),
+# 0 (t = +-0), a subnormal, ties at 0.5 / 1 / 2, 65504 (nothing finite
+# above it) and +inf (nothing at all). x holds +-0, a subnormal, ties, NaN
+# and +-65504 (two columns per token, so the sums stay finite).
+_EDGE_VALUES = np.array([1.0, -1.0, 0.5, 0.0, -0.0, 2.0, -2.0, np.nan, 6e-8, -6e-8, 1.9990234375, 0.25, -0.5],
+                        dtype=np.float16)
+_EDGE_THRESHOLDS = (1.0, 0.5, 0.0, -0.0, -1.0, 1.9999, 2.0, 65504.0, float("inf"), 5.9604645e-08)
+
+
+def _edge_x(batch, cols):
+    k = np.arange(cols)
+    x = np.stack([_EDGE_VALUES[(k * 7 + b * 3) % _EDGE_VALUES.size] for b in range(batch)])
+    for b in range(batch):
+        x[b, (b * 37) % cols] = np.float16(65504.0)
+        x[b, (b * 53 + 11) % cols] = np.float16(-65504.0)
+    return x
+
+
+@pytest.mark.parametrize("batch,mask,mfma,codes", [
+    (1, "token", None, False), (2, "token", None, False), (4, "token", None, False),
+    (5, "token", None, False), (8, "token", None, False), (8, "token", "1", False),
+    (12, "token", None, False), (16, "token", None, False), (20, "token", None, False),
+    (32, "token", None, False), (2, "batch", None, False), (8, "batch", None, False),
+    (20, "batch", None, False), (32, "batch", None, False),
+    (1, "token", None, True), (4, "token", None, True), (16, "token", None, True), (32, "token", None, True)])
+def test_threshold_edges_every_form(monkeypatch, batch, mask, mfma, codes):
+    if mfma is not None:
+        monkeypatch.setenv("SPDP_MFMA", mfma)
+    w = oracle.magnitude_prune(synth.weights(300, 512, 23), 0.5)
+    x = _edge_x(batch, 512)
+    if mask == "batch":
+        # a NaN in any token drops its column for the batch: keep a few, so
+        # that the other columns' batch scores decide
+        x = np.where(np.isnan(x), np.float16(0.75), x)
+        x[0, ::29] = np.float16(np.nan)
+    if codes:
+        # one-byte 4-bit codes, one scale per row (the low-bit Values form)
+        q, scales, _ = oracle.rtn_quantize(w, 4)
+        m = spdp.encode_rtn(w, (256, 16), 4)
+    else:
+        m = spdp.encode(w, (256, 16))
+    for t in _EDGE_THRESHOLDS:
+        label = f"B={batch} mask={mask} mfma={mfma} codes={codes} t={t}"
+        print(f"[gpu] edges {label}", flush=True)
+        y = _run_gpu(m, x, t, mask=mask)
+        y64, s64, _ = oracle.spmspv_rtn(q, scales, x, t, mask) if codes else oracle.spmspv(w, x, t, mask)
+        _assert_close(y, y64, s64, label)
+    m.close()
+
+
 def test_output_fully_overwritten_and_repeatable():
     w, x, t = _case(600, 1500, (256, 16), 0.5, 0.5, 4, 17, 18)
     m = spdp.encode(w, (256, 16))
