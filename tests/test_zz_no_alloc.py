@@ -107,6 +107,25 @@ def test_noalloc_interleaved_handles_share_the_workspace():
         m.close()
 
 
+def test_noalloc_one_segment_between_split_calls(monkeypatch):
+    # above 16 tokens a stripe that one workgroup covers whole writes Y
+    # directly and leaves the static workspace's epoch as it was; the calls
+    # around it (split, tagged) must still see only their own partials
+    w, x, t = _problem(512, 1111, 0.6, 0.4, 32, 7300)
+    m = spdp.encode(w, (256, 16))
+    w2, x2, t2 = _problem(300, 2048, 0.5, 0.5, 17, 7310)
+    m2 = spdp.encode(w2, (128, 16))
+    for rep in range(2):
+        _compare(m, w, x, t, f"512x1111 B=32 split rep {rep}")
+        monkeypatch.setenv("SPDP_PASSES", "64")
+        _compare(m, w, x, t, f"512x1111 B=32 one segment rep {rep}")
+        _compare(m2, w2, x2, t2, f"300x2048 B=17 one segment rep {rep}")
+        monkeypatch.delenv("SPDP_PASSES")
+        _compare(m2, w2, x2, t2, f"300x2048 B=17 split rep {rep}")
+    m.close()
+    m2.close()
+
+
 def test_noalloc_graph_replay():
     dev = _dev()
     w, x, t = _problem(4096, 4096, 0.6, 0.5, 1, 7201)
