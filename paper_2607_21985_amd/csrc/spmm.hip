@@ -824,13 +824,14 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
     // workgroup; below that the 128-token form's larger grid wins); split K
     // when the (stripe, token tile) grid leaves CUs idle, so that a split's
     // TileOffsets fit the LDS table, and with at least 8 GTiles per split
-    // (40 for the 256-token form). A 256-token workgroup holds its CU, so
-    // its split never asks for more workgroups than there are CUs: a second
-    // round for a few of them doubles the time. Measured (us; the previous
-    // rule, 256-token workgroups only when two of them per CU were left
-    // unsplit -> this one): 11008x4096 at 256 / 512 tokens 108 / 148 -> 57 /
-    // 93, 8192x8192 at 512 149 -> 113, 28672x8192 at 512 334 -> 297,
-    // 4096x4096 at 1024 90 -> 78.
+    // (40 for the 256-token form). A workgroup of either form holds its CU,
+    // so the split never asks for more workgroups than there are CUs: a
+    // second round for a few of them doubles the time. Measured (us; the
+    // previous rule, 256-token workgroups only when two of them per CU were
+    // left unsplit and the split rounded up -> this one): 11008x4096 at 128
+    // / 256 / 512 tokens 66 / 108 / 148 -> 42 / 57 / 95, 8192x8192 at 512
+    // 149 -> 105, 28672x8192 at 128 / 512 199 / 334 -> 145 / 294, 4096x4096
+    // at 1024 90 -> 77.
     const int ncb = (int)h->n_colblocks;
     int cus = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
@@ -842,7 +843,7 @@ extern "C" int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens, u
     const bool wide = form == 3 || (form != 2 && n_tokens > kBN && 2 * wgs256 * k256 >= cus);
     const long long tiles = wide ? tiles256 : tok_tiles;
     const long long wgs = h->n_stripes * tiles;
-    long long k = wide ? k256 : wgs < cus ? std::min<long long>(8, (cus + wgs - 1) / wgs) : 1;
+    long long k = wide ? k256 : wgs < cus ? std::max<long long>(1, std::min<long long>(8, cus / wgs)) : 1;
     if (!wide) k = std::min<long long>(k, std::max(1, ncb / 8));
     if (const char* env = std::getenv("SPDP_SPMM_SPLITS")) k = std::max(1, std::atoi(env));
     k = std::max<long long>(k, (ncb + kToCap - 2) / (kToCap - 1));
