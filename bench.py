@@ -758,6 +758,7 @@ PREFILL = [
     ("llama7b-mlp", "gate", 0.6, 2048),
     ("llama7b-mlp", "down", 0.6, 2048),
     ("llama70b-layer", "gate", 0.7, 1024),
+    ("llama70b-layer", "gate", 0.7, 256),   # a serving-size prefill chunk
 ]
 
 
