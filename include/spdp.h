@@ -214,10 +214,10 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count,
  *              fully overwritten; must not overlap X.
  *   stream     hipStream_t to enqueue on.
  *
- * Asynchronous. When the grid of (256-row stripe, 128-token tile) pairs
+ * Asynchronous. When the grid of (256-row stripe, token tile) pairs
  * leaves compute units idle (few tokens), or when a stripe has more than
  * 1799 GTiles, the columns are split into k <= 8 ranges (more for very wide
- * matrices): one kernel writes k fp32 partial products into a workspace of
+ * matrices; never more workgroups than the device has compute units): one kernel writes k fp32 partial products into a workspace of
  * the handle (k * n_tokens * rows * 4 bytes) and a second adds them in
  * range order and rounds once to fp16. That workspace grows on the first
  * call that needs more (hipMalloc; the old one is kept until spdp_free,
@@ -226,7 +226,8 @@ int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count,
  * at least as many tokens before the capture). SPDP_ERR_OOM if it cannot
  * be allocated. Calls on one handle that overlap in time on different
  * streams share the workspace and race. The fp32 summation order is fixed
- * by the matrix and the token count, so equal inputs give equal bits.
+ * by the matrix, the token count and the device's compute-unit count, so
+ * equal inputs give equal bits on one device.
  */
 int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens,
               uint16_t* Y, void* stream);
