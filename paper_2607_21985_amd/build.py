@@ -41,7 +41,9 @@ def build(verbose: bool = False) -> str:
     jobs = [
         ([cc, "-x", "c++"] + common + ["-c", os.path.join(CSRC, "host.cpp"),
                                        "-o", os.path.join(objdir, "host.o")]),
-        ([cc] + common + device + ["-c", os.path.join(CSRC, "spdp.hip"),
+        # the 4x4x4 MFMA accumulators of the batched decode stay in VGPRs
+        # (the AGPR form would add registers and moves and cost occupancy)
+        ([cc] + common + device + ["-mllvm", "-amdgpu-mfma-vgpr-form=true", "-c", os.path.join(CSRC, "spdp.hip"),
                                    "-o", os.path.join(objdir, "spdp.o")]),
         ([cc] + common + device + ["-c", os.path.join(CSRC, "spmm.hip"),
                                    "-o", os.path.join(objdir, "spmm.o")]),

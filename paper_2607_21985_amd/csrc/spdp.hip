@@ -244,7 +244,6 @@ __device__ __forceinline__ void masked_fma_column2(float (&acc)[WPC][2], const u
 #undef SPDP_FMA2
 
 
-typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
 // {a where word ma has the lane's bit, else 0} | {b likewise under mb} << 16,
 // for a and b zero-extended fp16 bits: two selects that each write one half
@@ -261,10 +260,24 @@ __device__ __forceinline__ uint32_t pair_under_words(uint32_t a, uint32_t b, uin
   return p;
 }
 
-// acc + lo(v) * lo(x) + hi(v) * hi(x) in fp32 (fp16 products are exact in fp32)
-__device__ __forceinline__ float dot2(uint32_t v, uint32_t x, float acc) {
-  return __builtin_amdgcn_fdot2(__builtin_bit_cast(half2_t, v), __builtin_bit_cast(half2_t, x), acc, false);
+// The same pair for a matrix-core operand. The compiler's hazard checks do
+// not look inside the assembly: an MFMA that reads a VGPR a VALU
+// instruction has just written needs wait states between them, so two
+// follow the selects (a GPU test failed on the rows of a batch's last word,
+// whose MFMA came one wait state after its select).
+__device__ __forceinline__ uint32_t pair_under_words_mfma(uint32_t a, uint32_t b, uint64_t ma, uint64_t mb) {
+  uint32_t p;
+  asm("s_mov_b64 vcc, %[ma]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[a], vcc dst_sel:WORD_0 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0\n\t"
+      "s_mov_b64 vcc, %[mb]\n\t"
+      "v_cndmask_b32_sdwa %[p], 0, %[b], vcc dst_sel:WORD_1 dst_unused:UNUSED_PRESERVE src0_sel:DWORD src1_sel:WORD_0\n\t"
+      "s_nop 1"
+      : [p] "=&v"(p)
+      : [a] "v"(a), [b] "v"(b), [ma] "s"(ma), [mb] "s"(mb)
+      : "vcc");
+  return p;
 }
+
 
 // The kernel's argument block, read again from the kernel-argument segment
 // through a pointer the compiler cannot see through: fields used only after
@@ -303,6 +316,7 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float16_t __attribute__((ext_vector_type(16)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
 // MFMA form: a wave's dense tile of decoded weights, one row per matrix row
 // of the stripe, 8 columns (two batches) per row, padded to 24 bytes
 constexpr int kMRowBytes = 24;
@@ -372,6 +386,14 @@ __device__ __forceinline__ void spmspv_body() {
   for (int w = 0; w < WPC; ++w)
 #pragma unroll
     for (int b = 0; b < NB; ++b) acc[w][b] = 0.0f;
+  // from four tokens on (vector-ALU kernels): word w's rows x tokens 4g ..
+  // 4g + 3, lane = row, in the 4x4x4 MFMA's accumulator layout
+  constexpr bool kM4 = !MM && NB >= 4;
+  float4_t acc4[kM4 ? WPC : 1][kM4 ? NB / 4 : 1];
+#pragma unroll
+  for (int w = 0; w < (kM4 ? WPC : 1); ++w)
+#pragma unroll
+    for (int g = 0; g < (kM4 ? NB / 4 : 1); ++g) acc4[w][g] = float4_t{0.0f, 0.0f, 0.0f, 0.0f};
   // MFMA form: the stripe's 32-row blocks x 32 tokens (tokens past the
   // batch stay 0), in the 32x32 accumulator layout
   constexpr int kMBlocks = 2 * WPC;
@@ -680,11 +702,12 @@ __device__ __forceinline__ void spmspv_body() {
       }
       // 4. accumulate in fp32. One or two tokens: the words become EXEC around
       // single FMAs (v_fma_mix, fp16 operands; no branch, no select), NB per
-      // word. More tokens: the two columns of a pair are selected into the
-      // halves of one register (zero where the bit is clear: one SDWA select
-      // per column word) and one dot product per token (v_dot2_f32_f16 against
-      // the pair's two activations) adds both columns: 1 + NB/2 instructions
-      // per word instead of NB, fewer from four tokens on.
+      // word. From four tokens on the quad's four columns times four tokens
+      // are a small dense contraction per 64-row word: the two columns of a
+      // pair are selected into the halves of one register (zero where the bit
+      // is clear: one SDWA select per column word), and one
+      // v_mfma_f32_4x4x4_16b_f16 per word and four tokens adds the four
+      // columns, in place of NB dot products (v_dot2) per column pair.
       if constexpr (MM) {
         // 4 (MFMA form). The batch's four columns, zero where the bit is
         // clear, into the wave's dense tile: row 64 w + lane, columns 4 h ..
@@ -716,18 +739,25 @@ __device__ __forceinline__ void spmspv_body() {
             masked_fma_column<WPC, false>(acc, vb[c], xpair, m[c]);
         }
       } else {
+        // four columns x four tokens per v_mfma_f32_4x4x4_16b_f16: B = the
+        // quad's masked values of the lane's row (the two column pairs), A =
+        // the quad's activations of token 4g + (lane & 3), so that lane r
+        // gets rows r of tokens 4g .. 4g + 3 (D[4b + i][e] = sum_k A[4b + e][k]
+        // B[4b + i][k])
+        uint2 wv[WPC];
   #pragma unroll
-        for (int pr = 0; pr < 2; ++pr) {
-          uint32_t pv[WPC];
+        for (int w = 0; w < WPC; ++w)
+          wv[w] = make_uint2(pair_under_words_mfma(vb[0][w], vb[1][w], m[0][w], m[1][w]),
+                             pair_under_words_mfma(vb[2][w], vb[3][w], m[2][w], m[3][w]));
+        const uint32_t* xp0 = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2) * kXRow * 2]);
+        const uint32_t* xp1 = xp0 + kXRow;
   #pragma unroll
-          for (int w = 0; w < WPC; ++w) pv[w] = pair_under_words(vb[2 * pr][w], vb[2 * pr + 1][w], m[2 * pr][w], m[2 * pr + 1][w]);
-          const uint32_t* xp = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2 + pr) * kXRow * 2]);
+        for (int g = 0; g < NB / 4; ++g) {
+          const int t = 4 * g + (lane & 3);
+          const half4_t xa = __builtin_bit_cast(half4_t, make_uint2(xp0[t], xp1[t]));
   #pragma unroll
-          for (int b = 0; b < NB; ++b) {
-            const uint32_t x2 = xp[b];
-  #pragma unroll
-            for (int w = 0; w < WPC; ++w) acc[w][b] = dot2(pv[w], x2, acc[w][b]);
-          }
+          for (int w = 0; w < WPC; ++w)
+            acc4[w][g] = __builtin_amdgcn_mfma_f32_4x4x4f16(xa, __builtin_bit_cast(half4_t, wv[w]), acc4[w][g], 0, 0, 0);
         }
       }
     };
@@ -873,7 +903,8 @@ __device__ __forceinline__ void spmspv_body() {
 #pragma unroll
     for (int w = 0; w < WPC; ++w)
 #pragma unroll
-      for (int bb = 0; bb < kSlice; ++bb) red[(wave * kSlice + bb) * 256 + 64 * w + lane] = acc[w][b0 + bb];
+      for (int bb = 0; bb < kSlice; ++bb)
+        red[(wave * kSlice + bb) * 256 + 64 * w + lane] = kM4 ? acc4[w][(b0 + bb) / 4][(b0 + bb) % 4] : acc[w][b0 + bb];
     __syncthreads();
 #pragma unroll
     for (int bb = 0; bb < kSlice; ++bb) {
