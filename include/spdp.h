@@ -112,9 +112,9 @@ int spdp_encode_host(const uint16_t* W, int64_t rows, int64_t cols,
  *
  * Deterministic: the fp32 summation order depends only on the matrix, the
  * batch and which columns are active (and on the tuning variables
- * SPDP_SPLITK and SPDP_EARLY_FIRST, when set), so equal inputs give equal
- * bits on every call, and a product gives the same bits alone and inside
- * spdp_spmspv_many.
+ * SPDP_SPLITK, SPDP_PASSES, SPDP_MFMA and SPDP_EARLY_FIRST, when set), so
+ * equal inputs give equal bits on every call, and a product gives the same
+ * bits alone and inside spdp_spmspv_many.
  */
 int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
                 float threshold, uint16_t* Y, void* stream);
@@ -130,8 +130,9 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
  *   A product needing more than SPDP_NOALLOC_PARTIAL_BYTES of partials
  *   (8 bytes x K segments x batch x rows rounded up to tile_m) returns
  *   SPDP_ERR_UNSUPPORTED and launches nothing: a 4096 x 4096 product fits
- *   at every batch up to 32, the largest Llama-70B projections (28672 x
- *   8192, 8192 x 28672) up to batch 9.
+ *   at every batch up to 32, and so does every Llama-7B, -13B and -70B
+ *   projection (the most any needs is 39.9 MiB: 8192 x 8192 at batch
+ *   29, two K ranges per workgroup).
  *   The workspace is shared by every call on one GPU and keeps the last
  *   call's contents (tagged with a device-wide call epoch, so a call never
  *   reads another's partials): calls that overlap on one GPU (two streams,
@@ -139,7 +140,7 @@ int spdp_spmspv(spdp_handle_t h, const uint16_t* X, int32_t batch,
  *   The first call on a device looks up the workspace's address
  *   (hipGetSymbolAddress); no call allocates, frees or waits for the device.
  */
-#define SPDP_NOALLOC_PARTIAL_BYTES ((size_t)32 << 20)
+#define SPDP_NOALLOC_PARTIAL_BYTES ((size_t)40 << 20)
 int spdp_spmspv_noalloc(spdp_handle_t h, const uint16_t* X, int32_t batch,
                         float threshold, uint16_t* Y, void* stream);
 

@@ -402,11 +402,12 @@ __device__ __forceinline__ void spmspv_body() {
   for (int i = 0; i < (MM ? kMBlocks : 1); ++i) macc[i] = float16_t{};
 
   // The workgroup walks `passes` consecutive K ranges (one unless the batch
-  // is large: fewer segments then mean fewer split-K partials, whose bytes
-  // grow with the batch), accumulating into the same registers; each pass
-  // tests its range, builds its list and streams it. The stripe's phase is
-  // read in the first pass.
-  const int passes = MM ? A->passes : 1;  // the vector-ALU forms walk one range
+  // and the product are large: fewer segments then mean fewer split-K
+  // partials, whose bytes grow with the batch), accumulating into the same
+  // registers; each pass tests its range, builds its list and streams it.
+  // The stripe's phase is read in the first pass. The one- and two-token
+  // forms and the code forms walk one range.
+  const int passes = (MM || (NB >= 4 && !Q)) ? A->passes : 1;
   uint32_t phase = 0;
   for (int pass = 0; pass < passes; ++pass) {
     if (pass > 0) __syncthreads();  // the last pass's list, activations and ring are free
@@ -897,6 +898,14 @@ __device__ __forceinline__ void spmspv_body() {
     }
     if (direct) return;
   }
+  // the vector-ALU forms: per token slice, the waves' accumulators to LDS,
+  // then thread `row` adds them in wave order and publishes; a stripe of one
+  // segment writes Y as the MFMA form does (the row scale applied as the
+  // gather applies it)
+  const bool direct_v = !MM && n_seg == 1;
+  const int m_v = r * ka->tile_m + row;
+  const bool live_v = row < 64 * WPC && m_v < ka->rows;
+  const float scale_v = (Q && direct_v && live_v) ? ka->scales[m_v] : 1.0f;
 #pragma unroll
   for (int b0 = 0; b0 < (MM ? 0 : NB); b0 += kSlice) {
     __syncthreads();
@@ -912,11 +921,18 @@ __device__ __forceinline__ void spmspv_body() {
         float s = 0.0f;
 #pragma unroll
         for (int wv = 0; wv < kWaves; ++wv) s += red[(wv * kSlice + bb) * 256 + row];
-        __hip_atomic_store(dst + (size_t)(b0 + bb) * mpad, tag | __float_as_uint(s), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        if (!direct_v) {
+          __hip_atomic_store(dst + (size_t)(b0 + bb) * mpad, tag | __float_as_uint(s), __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+        } else if (live_v) {
+          float t = 0.0f + s;
+          if constexpr (Q) t *= scale_v;
+          ka->y[(size_t)(b0 + bb) * ka->rows + m_v] = __half_as_ushort(__float2half_rn(t));
+        }
       }
     }
   }
+  if (direct_v) return;
 
   // ---- the stripe's last n_red segments gather: reducer j owns the 64-row
   // blocks w = j, j + n_red, ...; its four waves split the segments (wave g
@@ -1066,41 +1082,45 @@ int hip_fail(hipError_t e, const char* what) {
 // faster but three of them (q, k, v) in one launch 5 % slower.
 // SPDP_SPLITK overrides the number of segments (for tuning).
 constexpr int kWaveCols = 48;
-// K ranges per workgroup above 16 tokens (the matrix-core form): measured on
-// the Llama-70B layer at 32 tokens, 118 / 109 / 104 us per product with 1 /
-// 2 / 4 (70/50), latency floor 94 / 68 / 54 us per launch
-constexpr int kLargeBatchPasses = 4;
 constexpr int64_t kOneRoundSegments = 48;
 constexpr int64_t kMinWorkgroups = 512;
 constexpr int64_t kMaxWorkgroups = 1792;
-// The matrix-core accumulate pays above 16 tokens: measured on the Llama-70B
-// layer at 32 tokens 115 against 142 us per product (70/50 and 50/0), while
-// at 8 and 16 tokens the vector-ALU form (NB / 2 dot products per 64-row
-// word) is faster (56 against 90 us at 8 tokens, 39 against 53 at 16).
-// SPDP_MFMA=0 or 1 overrides from 5 tokens on (for tuning). A property of
-// the batch only, so a product gives the same bits alone and grouped.
+// The 32x32 matrix-core form (a 32-row block x 32 tokens per instruction)
+// runs only when SPDP_MFMA=1 asks for it, from 5 tokens on: the vector forms
+// (one 4x4x4 product per 64-row word and four tokens from 3 tokens on) are
+// as fast or faster at every measured size, at 32 tokens per product on the
+// Llama-70B layer 90 against 92 us (70/50) and 94 against 93 (50/0), the
+// Llama-13B layer 49 against 58, the Llama-7B MLP 51 against 76. A property
+// of the batch only, so a product gives the same bits alone and grouped.
 bool use_mfma(int batch) {
   if (batch < 5) return false;
   if (const char* env = std::getenv("SPDP_MFMA")) return std::atoi(env) != 0;
-  return batch > 16;
+  return false;
 }
 
-// Passes per workgroup: one K range each up to 16 tokens; above, several
-// consecutive ranges per workgroup, so that the split-K partials (segments
-// x batch x rows x 8 bytes, written and read back) shrink. Measured per
-// product at 32 tokens, 70/50, with 1 / 2 / 4 / 8 passes: 28672x8192 185 /
-// 172 / 160 / 262 us, 8192x8192 103 / 91 / 84 / 125 us, 1024x8192 32 / 42
-// / 69 / 125 us; one pass for the narrow products alone made the Llama-70B
-// layer's grouped launches 1-2 % slower. SPDP_PASSES overrides (for
-// tuning). A property of the batch, like the split.
-int passes_for(int batch, bool codes) {
-  // only the matrix-core form (fp16 values) walks several ranges
-  if (codes || !use_mfma(batch)) return 1;
+// Passes per workgroup: more passes mean fewer segments, so fewer split-K
+// partials (segments x batch x rows x 8 bytes, written and read back), and
+// fewer, longer workgroups. The rule takes the largest P of 4, 2, 1 whose
+// workgroups W_P (stripes x segments / P, rounded up) satisfy
+// W_P x batch >= 2560 P: the partials' bytes grow with the batch, the cost of
+// too few workgroups with P. Measured per product at 8 / 16 tokens with 1, 2
+// or 4 passes everywhere: Llama-70B layer 46.7 / 43.1 / 50.2 and 58.4 / 51.6 /
+// 58.0 us, Llama-13B 23.4 / 24.1 / 30.6 and 31.9 / 29.9 / 36.1, Llama-7B MLP
+// (8 tokens) 24.9 / 25.7 / 37.3; at 32 tokens the rule (4 passes on the
+// Llama-70B products but k and v, 2 on most others) is within 1 % of the best
+// uniform count on each layer (the Llama-7B MLP at 4 passes everywhere: 46 %
+// slower). One or two tokens and the code forms walk one range. SPDP_PASSES
+// overrides (for tuning). A property of the matrix and the batch, like the
+// split, so a product gives the same bits alone and grouped.
+int passes_for(int batch, bool codes, int64_t stripes, int64_t segs) {
+  if (codes || batch < 3) return 1;
   if (const char* env = std::getenv("SPDP_PASSES")) {
     const long v = std::strtol(env, nullptr, 10);
     if (v >= 1 && v <= 64) return (int)v;
   }
-  return batch > 16 ? kLargeBatchPasses : 1;
+  for (int p = 4; p > 1; p /= 2)
+    if (stripes * ((segs + p - 1) / p) * batch >= int64_t(2560) * p) return p;
+  return 1;
 }
 
 void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols, int* passes) {
@@ -1114,7 +1134,7 @@ void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols
     if (v >= 1) {
       wc = std::min<int64_t>(kMaxWaveCols, ((cols + v * kWaves - 1) / (v * kWaves) + 15) / 16 * 16);
       *wave_cols = (int)wc;
-      *passes = passes_for(batch, codes);
+      *passes = passes_for(batch, codes, stripes, segs(wc));
       *segments = (int)((segs(wc) + *passes - 1) / *passes);
       return;
     }
@@ -1122,7 +1142,7 @@ void choose_split(const spdp_matrix* m, int batch, int* segments, int* wave_cols
   while ((stripes * segs(wc) > kMaxWorkgroups || segs(wc) > kOneRoundSegments) && wc < kMaxWaveCols) wc += 16;
   while (stripes * segs(wc) < kMinWorkgroups && wc > 16 && segs(wc - 16) <= kOneRoundSegments) wc -= 16;
   *wave_cols = (int)wc;
-  *passes = passes_for(batch, codes);
+  *passes = passes_for(batch, codes, stripes, segs(wc));
   *segments = (int)((segs(wc) + *passes - 1) / *passes);
 }
 

@@ -155,15 +155,17 @@ def test_exact_every_row(label, rows, cols, tile, points, batches, seed):
 # one segment per stripe: SPDP_PASSES covers the whole K, so each stripe's
 # workgroup adds every column and writes Y itself (no split-K partials);
 # a 70B gate/up shape and a ragged one (rows and columns past a tile edge)
+@pytest.mark.parametrize("mfma", ["0", "1"], ids=["vector", "mfma32"])
 @pytest.mark.parametrize("rows,cols,batch,seed", [(28672, 8192, 32, 20), (1000, 3000, 17, 51)],
                          ids=["28672x8192 B=32", "1000x3000 B=17"])
-def test_exact_one_segment(monkeypatch, rows, cols, batch, seed):
+def test_exact_one_segment(monkeypatch, rows, cols, batch, seed, mfma):
     monkeypatch.setenv("SPDP_PASSES", "64")
+    monkeypatch.setenv("SPDP_MFMA", mfma)
     w = _pruned(rows, cols, seed, 0.7)
     m = spdp.encode(w, (256, 16))
     x = _dyadic_x(batch, cols, seed * 100 + batch)
     t = float(oracle.threshold_for(x, 0.5))
-    lab = f"{rows}x{cols} B={batch} one segment"
+    lab = f"{rows}x{cols} B={batch} mfma={mfma} one segment"
     print(f"[gpu-exact] {lab} token mask", flush=True)
     _assert_bits(_run(m, x, t, "token"), _expected_bits(w, x, t, "token"), lab + " token mask")
     tb = _batch_t(x, 0.5)

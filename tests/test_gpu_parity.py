@@ -559,20 +559,45 @@ def test_batch_mask_edge_cases():
     m.close()
 
 
+@pytest.mark.parametrize("mfma", ["0", "1"])
 @pytest.mark.parametrize("passes", ["1", "2", "3", "5", "64"])
-@pytest.mark.parametrize("batch", [8, 17, 32])
-def test_forced_passes_and_matrix_core_form(monkeypatch, passes, batch):
-    """Several K ranges per workgroup (the matrix-core form at large
-    batches) and the matrix-core form itself, forced on from 5 tokens: fp16
-    values and one-byte codes (which keep the vector-ALU form and one range)
-    must both match the oracle."""
+@pytest.mark.parametrize("batch", [4, 8, 17, 32])
+def test_forced_passes_and_matrix_core_form(monkeypatch, passes, batch, mfma):
+    """Several K ranges per workgroup, forced, in the vector forms (from 3
+    tokens) and in the 32x32 matrix-core form (forced on from 5 tokens): fp16
+    values and one-byte codes (which keep one range) must both match the
+    oracle. 64 passes cover the whole K: one segment per stripe, Y written
+    without partials."""
+    if mfma == "1" and batch < 5:
+        pytest.skip("the 32x32 matrix-core form starts at 5 tokens")
     monkeypatch.setenv("SPDP_PASSES", passes)
-    monkeypatch.setenv("SPDP_MFMA", "1")
+    monkeypatch.setenv("SPDP_MFMA", mfma)
     w, x, t = _case(700, 3000, (256, 16), 0.6, 0.4, batch, 123, 456)
-    _check_full(w, x, t, (256, 16), f"passes={passes} B={batch} fp16")
+    _check_full(w, x, t, (256, 16), f"passes={passes} mfma={mfma} B={batch} fp16")
     codes, scales, _ = oracle.rtn_quantize(w, 4)
     m = spdp.encode_rtn(w, (256, 16), 4)
     y = _run_gpu(m, x, t)
     y64, s64, _ = oracle.spmspv_rtn(codes, scales, x, t)
-    _assert_close(y, y64, s64, f"passes={passes} B={batch} codes")
+    _assert_close(y, y64, s64, f"passes={passes} mfma={mfma} B={batch} codes")
+    m.close()
+
+
+@pytest.mark.parametrize("codes", [False, True], ids=["fp16", "codes"])
+@pytest.mark.parametrize("batch", [1, 2, 3, 8, 16, 32])
+def test_one_segment_every_vector_form(batch, codes):
+    """40 columns fit one segment (64 columns at the narrowest split), so
+    every stripe's workgroup writes Y itself, also in the one- and two-token
+    forms and the code forms (row scale applied at the write)."""
+    w, x, t = _case(600, 40, (256, 16), 0.5, 0.3, batch, 131, 457)
+    label = f"600x40 B={batch} {'codes' if codes else 'fp16'} one segment"
+    print(f"[gpu] {label}", flush=True)
+    if codes:
+        q, scales, _ = oracle.rtn_quantize(w, 4)
+        m = spdp.encode_rtn(w, (256, 16), 4)
+        y64, s64, _ = oracle.spmspv_rtn(q, scales, x, t)
+    else:
+        m = spdp.encode(w, (256, 16))
+        y64, s64, _ = oracle.spmspv(w, x, t)
+    for rep in range(2):
+        _assert_close(_run_gpu(m, x, t), y64, s64, f"{label} rep {rep}")
     m.close()

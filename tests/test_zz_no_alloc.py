@@ -108,7 +108,7 @@ def test_noalloc_interleaved_handles_share_the_workspace():
 
 
 def test_noalloc_one_segment_between_split_calls(monkeypatch):
-    # above 16 tokens a stripe that one workgroup covers whole writes Y
+    # a stripe that one workgroup covers whole writes Y
     # directly and leaves the static workspace's epoch as it was; the calls
     # around it (split, tagged) must still see only their own partials
     w, x, t = _problem(512, 1111, 0.6, 0.4, 32, 7300)
