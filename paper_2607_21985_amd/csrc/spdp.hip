@@ -326,9 +326,10 @@ constexpr int kMRowBytes = 24;
 // scale per row (else fp16); MM: accumulate on the matrix cores (8 or more
 // tokens: the product of a batch of 8 active columns with up to 32 tokens
 // is a small dense contraction; see step 4).
-template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MM>
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MM, bool MP>
 __device__ __forceinline__ void spmspv_body() {
   static_assert(!MM || (NB >= 8 && !Q && !EARLY), "the MFMA form serves 8 or more tokens of fp16 values");
+  static_assert(!MP || (NB >= 4 && !Q && !EARLY), "several K ranges: 3 or more tokens of fp16 values");
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[S::kRingBytes];
@@ -405,9 +406,9 @@ __device__ __forceinline__ void spmspv_body() {
   // and the product are large: fewer segments then mean fewer split-K
   // partials, whose bytes grow with the batch), accumulating into the same
   // registers; each pass tests its range, builds its list and streams it.
-  // The stripe's phase is read in the first pass. The one- and two-token
-  // forms and the code forms walk one range.
-  const int passes = (MM || (NB >= 4 && !Q)) ? A->passes : 1;
+  // The stripe's phase is read in the first pass. Only the MP kernels have
+  // the loop (in the others it costs 3-6 % at one pass).
+  const int passes = MP ? A->passes : 1;
   uint32_t phase = 0;
   for (int pass = 0; pass < passes; ++pass) {
     if (pass > 0) __syncthreads();  // the last pass's list, activations and ring are free
@@ -1051,13 +1052,13 @@ __device__ __forceinline__ void spmspv_body() {
 
 // The kernels: the vector-ALU forms, and the matrix-core form, whose 32 x 32
 // accumulator blocks live in AGPRs; two waves per SIMD are asked of it.
-template <int NB, int WPC, bool EARLY, bool BMASK, bool Q>
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MP>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
-  spmspv_body<NB, WPC, EARLY, BMASK, Q, false>();
+  spmspv_body<NB, WPC, EARLY, BMASK, Q, false, MP>();
 }
 template <int NB, int WPC, bool BMASK>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void spmspv_mm_kernel(LaunchArgs) {
-  spmspv_body<NB, WPC, false, BMASK, false, true>();
+  spmspv_body<NB, WPC, false, BMASK, false, true, true>();
 }
 
 using spdp::fail;
@@ -1228,15 +1229,19 @@ int upload(const std::vector<T>& v, void** dst) {
 }
 
 template <int NB, int WPC, bool Q>
-hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, dim3 grid, hipStream_t stream) {
+hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, dim3 grid,
+                       hipStream_t stream) {
   // the one-token kernel has the early-first-batch form (no product with
   // more tokens asks for it); the kernels for more tokens have the shared
   // batch mask form (at one token the two masks are the same rule, and the
   // host sends such calls to the per-token kernel); from 8 tokens on, fp16
-  // values accumulate on the matrix cores unless mm is false
+  // values accumulate in 32x32 blocks when mm is set; from 4, the kernels
+  // for fp16 values have a several-range form (multi: some product of the
+  // launch walks more than one K range; one range in it gives the bits of
+  // the one-range kernel)
   if constexpr (NB == 1) {
     if (early) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q, false>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   } else {
@@ -1249,29 +1254,39 @@ hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, 
         return hipGetLastError();
       }
     }
+    if constexpr (NB >= 4 && !Q) {
+      if (multi) {
+        if (bmask)
+          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, true>), grid, dim3(kThreads), 0, stream, args);
+        else
+          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, true>), grid, dim3(kThreads), 0, stream, args);
+        return hipGetLastError();
+      }
+    }
     if (bmask) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, false>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q>), grid, dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, false>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
 template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool mm, bool q, dim3 grid, hipStream_t stream) {
-  return q ? launch_form<NB, WPC, true>(args, early, bmask, mm, grid, stream)
-           : launch_form<NB, WPC, false>(args, early, bmask, mm, grid, stream);
+hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, bool q, dim3 grid,
+                      hipStream_t stream) {
+  return q ? launch_form<NB, WPC, true>(args, early, bmask, mm, multi, grid, stream)
+           : launch_form<NB, WPC, false>(args, early, bmask, mm, multi, grid, stream);
 }
 
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool mm, bool q, dim3 grid,
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool mm, bool multi, bool q, dim3 grid,
                   hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, early, bmask, mm, q, grid, stream);
-    case 2: return launch_one<NB, 2>(args, early, bmask, mm, q, grid, stream);
-    case 3: return launch_one<NB, 3>(args, early, bmask, mm, q, grid, stream);
-    default: return launch_one<NB, 4>(args, early, bmask, mm, q, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, bmask, mm, multi, q, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, bmask, mm, multi, q, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, bmask, mm, multi, q, grid, stream);
+    default: return launch_one<NB, 4>(args, early, bmask, mm, multi, q, grid, stream);
   }
 }
 
@@ -1456,7 +1471,7 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
   std::memset(&la, 0, sizeof(la));
   la.batch = batch;
   int64_t widest = 0;
-  bool early = false;
+  bool early = false, multi = false;
   const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
   for (int i = 0; i < count; ++i) {
     int64_t n_wg = 0;
@@ -1470,6 +1485,7 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
     if (n_wg >= (int64_t(1) << 31)) return fail(SPDP_ERR_UNSUPPORTED, "more than 2^31 - 1 workgroups");
     widest = std::max(widest, n_wg);
     early = early || la.m[i].early_first;
+    multi = multi || la.m[i].passes > 1;
   }
 
   const int wpc = handles[0]->tile_m / 64;
@@ -1478,17 +1494,17 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool mm = use_mfma(batch);
   if (batch <= 1)
-    e = launch<1>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<1>(la, wpc, early, bmask, mm, multi, q, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<2>(la, wpc, early, bmask, mm, multi, q, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<4>(la, wpc, early, bmask, mm, multi, q, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<8>(la, wpc, early, bmask, mm, multi, q, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<16>(la, wpc, early, bmask, mm, multi, q, grid, s);
   else
-    e = launch<32>(la, wpc, early, bmask, mm, q, grid, s);
+    e = launch<32>(la, wpc, early, bmask, mm, multi, q, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }
