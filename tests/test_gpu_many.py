@@ -40,6 +40,10 @@ def _products(shapes, sw, p, batch, seed, share_x=False):
     ([(1100, 4096), (1100, 4096)], (256, 16), 0.6, 0.5, 3, True),                 # gate, up
     ([(130, 200), (64, 64), (257, 1000), (90, 33), (700, 300)], (64, 8), 0.5, 0.3, 2, False),
     ([(256, 256)] * 8, (128, 16), 0.7, 0.25, 1, False),
+    # at 20 tokens the 4096x4096 product walks two K ranges per workgroup and
+    # the 300x1024 one a single range: the launch runs the several-range
+    # kernel, whose one-range products must keep their single-call bits
+    ([(4096, 4096), (300, 1024)], (256, 16), 0.6, 0.5, 20, False),
 ])
 def test_many_matches_oracle_and_single_calls(shapes, tile, sw, p, batch, share_x):
     dev = _dev()
