@@ -412,6 +412,14 @@ __device__ __forceinline__ void spmspv_body() {
   uint32_t phase = 0;
   for (int pass = 0; pass < passes; ++pass) {
     if (pass > 0) __syncthreads();  // the last pass's list, activations and ring are free
+    // in the several-range kernels the batch, the column count, X's address
+    // and the threshold code pass through an empty asm per pass, so that what
+    // the prologue derives from them per token (row offsets, lane masks) is
+    // computed where it is used instead of being hoisted out of the pass
+    // loop, where it would hold scalar registers through every pass
+    int batch_q = batch, cols_q = cols, code_q = code;
+    const uint16_t* x_q = x_p;
+    if constexpr (MP) asm volatile("" : "+s"(batch_q), "+s"(cols_q), "+s"(x_q), "+s"(code_q));
     const int k_begin = ((seg * passes + pass) * kWaves + wave) * wave_cols;
     const int range = max(0, min(wave_cols, cols - k_begin));
 
@@ -435,7 +443,7 @@ __device__ __forceinline__ void spmspv_body() {
       ci[c] = col_info_p[colx[c]];
       to[c] = tile_offset_p[g];
   #pragma unroll
-      for (int b = 0; b < NB; ++b) xb[c][b] = x_p[(size_t)min(b, batch - 1) * cols + k];
+      for (int b = 0; b < NB; ++b) xb[c][b] = x_q[(size_t)min(b, batch_q - 1) * cols_q + k];
     }
     // the stripe's phase: written by the previous call's last segment, read
     // by every workgroup of the stripe before any of them publishes (the
@@ -463,7 +471,7 @@ __device__ __forceinline__ void spmspv_body() {
       uint64_t act = 0;
       if constexpr (kXm) {
         // mag in (code, 0x7C00] is one unsigned compare for code in [-1, 0x7C00]
-        const uint32_t lo = (uint32_t)(code + 1), span = (uint32_t)(0x7C00 - code);
+        const uint32_t lo = (uint32_t)(code_q + 1), span = (uint32_t)(0x7C00 - code_q);
         uint64_t any = 0;
   #pragma unroll
         for (int j = 0; j < NB / 2; ++j) {
@@ -471,7 +479,7 @@ __device__ __forceinline__ void spmspv_body() {
   #pragma unroll
           for (int s = 0; s < 2; ++s) {
             const int b = 2 * j + s;
-            const bool on = b < batch && (BMASK || (xb[c][b] & 0x7FFFu) - lo < span);
+            const bool on = b < batch_q && (BMASK || (xb[c][b] & 0x7FFFu) - lo < span);
             if constexpr (!BMASK) any |= __builtin_amdgcn_ballot_w64(on);
             h[s] = on ? xb[c][b] : 0u;
           }
@@ -485,13 +493,13 @@ __device__ __forceinline__ void spmspv_body() {
         float score = 0.0f;
   #pragma unroll
         for (int b = 0; b < NB; ++b)
-          if (b < batch) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
+          if (b < batch_q) score += __half2float(__ushort_as_half((unsigned short)(xb[c][b] & 0x7FFFu)));
         act = __builtin_amdgcn_ballot_w64(in && score > batch_thr);
       } else if constexpr (!kXm) {
   #pragma unroll
         for (int b = 0; b < NB; ++b) {
           const int mag = (int)(xb[c][b] & 0x7FFFu);
-          act |= __builtin_amdgcn_ballot_w64(in && b < batch && mag > code && mag <= 0x7C00);
+          act |= __builtin_amdgcn_ballot_w64(in && b < batch_q && mag > code_q && mag <= 0x7C00);
         }
       }
       actm[c] = act;
@@ -543,7 +551,7 @@ __device__ __forceinline__ void spmspv_body() {
             xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = (b & 1) ? (uint16_t)(v >> 16) : (uint16_t)v;
           } else {
             const int mag = (int)(xb[c][b] & 0x7FFFu);
-            const bool on = b < batch && (BMASK || (mag > code && mag <= 0x7C00));
+            const bool on = b < batch_q && (BMASK || (mag > code_q && mag <= 0x7C00));
             xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
           }
         }
