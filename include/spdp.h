@@ -237,6 +237,21 @@ int spdp_spmm(spdp_handle_t h, const uint16_t* X, int64_t n_tokens,
 int spdp_reserve(spdp_handle_t h, int32_t max_batch);
 
 /*
+ * spdp_split_plan -- the split-K plan (Sec. 4.2.3) a call with `batch`
+ * tokens uses on this matrix, for inspection and tests: *segments
+ * workgroups per stripe of tile_m rows (the K segments), *wave_cols columns per
+ * wave and range (four waves per workgroup), and *passes consecutive ranges
+ * walked by each workgroup. Segment s covers the columns from
+ * s * passes * 4 * wave_cols on, so every column lies in exactly one range
+ * (segments * passes * 4 * wave_cols >= cols). A property of the matrix and
+ * the batch (and of the tuning variables SPDP_SPLITK and SPDP_PASSES), the
+ * same on host-only handles. SPDP_ERR_INVALID_ARG for a NULL handle or
+ * output, or batch outside [1, 32]; the outputs are then unchanged.
+ */
+int spdp_split_plan(spdp_handle_t h, int32_t batch, int32_t* segments,
+                    int32_t* wave_cols, int32_t* passes);
+
+/*
  * spdp_free -- release a handle. Waits for the device to finish work that
  * may still use it (a device synchronization, so it must not run while a
  * stream capture is in progress). spdp_free(NULL) does nothing. Using h

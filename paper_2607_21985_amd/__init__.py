@@ -44,7 +44,7 @@ _LIB_NAME = "libspdp.so"
 
 EXPORTED_SYMBOLS = (
     "spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_many", "spdp_spmspv_many_mask",
-    "spdp_reserve", "spdp_free",
+    "spdp_reserve", "spdp_split_plan", "spdp_free",
     "spdp_format", "spdp_prune_magnitude", "spdp_calibrate_threshold",
     "spdp_threshold_code", "spdp_strerror", "spdp_last_error",
     "spdp_encode_rtn", "spdp_encode_rtn_host", "spdp_spmspv_noalloc", "spdp_spmm",
@@ -115,6 +115,7 @@ def lib() -> ctypes.CDLL:
                                         ctypes.POINTER(ctypes.c_float), i32, ctypes.POINTER(ctypes.c_void_p),
                                         ctypes.c_void_p]
     L.spdp_reserve.argtypes = [H, i32]
+    L.spdp_split_plan.argtypes = [H, i32, ctypes.POINTER(i32), ctypes.POINTER(i32), ctypes.POINTER(i32)]
     L.spdp_free.argtypes = [H]
     L.spdp_free.restype = None
     L.spdp_format.argtypes = [H, ctypes.POINTER(_Format)]
@@ -128,7 +129,7 @@ def lib() -> ctypes.CDLL:
     for name in ("spdp_encode", "spdp_encode_host", "spdp_spmspv", "spdp_spmspv_noalloc", "spdp_spmm",
                  "spdp_spmspv_many",
                  "spdp_spmspv_many_mask",
-                 "spdp_reserve",
+                 "spdp_reserve", "spdp_split_plan",
                  "spdp_format",
                  "spdp_prune_magnitude", "spdp_calibrate_threshold", "spdp_threshold_code"):
         getattr(L, name).restype = ctypes.c_int
@@ -204,6 +205,12 @@ class Matrix:
 
     def reserve(self, max_batch: int) -> None:
         _check(lib().spdp_reserve(self._h, int(max_batch)))
+
+    def split_plan(self, batch: int) -> tuple:
+        """(segments, wave_cols, passes) of a call with ``batch`` tokens (``spdp_split_plan``)."""
+        sg, wc, ps = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        _check(lib().spdp_split_plan(self._h, int(batch), ctypes.byref(sg), ctypes.byref(wc), ctypes.byref(ps)))
+        return sg.value, wc.value, ps.value
 
     def spmspv_into(self, x, threshold: float, y, stream=None, mask: str = "token") -> None:
         """Enqueue ``y = W_sp . mask(x)`` on ``stream`` (torch stream, or the current one).

@@ -1604,6 +1604,18 @@ int spdp_reserve(spdp_handle_t h, int32_t max_batch) {
   return ensure_workspace(h, (int)need, 1, false, nullptr);
 }
 
+int spdp_split_plan(spdp_handle_t h, int32_t batch, int32_t* segments, int32_t* wave_cols, int32_t* passes) {
+  spdp::clear_error();
+  if (!h || !segments || !wave_cols || !passes) return fail(SPDP_ERR_INVALID_ARG, "handle or an output is NULL");
+  if (batch < 1 || batch > kMaxBatch) return fail(SPDP_ERR_INVALID_ARG, "batch must lie in [1, 32]");
+  int sg = 1, wc = 16, ps = 1;
+  choose_split(h, batch, &sg, &wc, &ps);
+  *segments = sg;
+  *wave_cols = wc;
+  *passes = ps;
+  return SPDP_OK;
+}
+
 int spdp_spmspv_many_mask(const spdp_handle_t* handles, int32_t count, const uint16_t* const* X,
                           int32_t batch, const float* thresholds, int32_t mask, uint16_t* const* Y,
                           void* stream) {
