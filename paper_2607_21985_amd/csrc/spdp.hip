@@ -65,15 +65,16 @@ constexpr int kMaxWords = 4;              // tile_m <= 256: at most 4 bitmap wor
 constexpr int kSlotBytes = 64 * kMaxWords * 2;  // LDS slot: one column of one stripe (fp16)
 constexpr int kBatch = 4;                 // active columns per DMA batch (one decode quad)
 constexpr int kQuad = 4;                  // columns decoded together
-constexpr int kMaxWaveCols = 128;         // columns whose activity one wave tests
-constexpr int kMaxWgCols = kWaves * kMaxWaveCols;
-// With early first batches the workgroup list holds at most kMaxWgCols -
-// kWaves kBatch columns (each wave's first kBatch active columns form its
-// own first batch) plus the last batch's padding, and the waves' first
-// batches follow it at kFirstList; without, the list may use every entry.
-constexpr int kFirstList = kMaxWgCols - kWaves * kBatch + kBatch;
-static_assert(kFirstList % kBatch == 0 && kFirstList + kWaves * kBatch == kMaxWgCols + kBatch,
-              "list layout");
+// Columns whose activity one wave tests per range: up to 128 (the widest
+// products keep few segments). From two tokens on the kernels also come in
+// a 64-column form, launched when no product of the launch has wider
+// ranges: it tests one 64-column chunk per lane instead of two (the second
+// is empty then), and its smaller list and activation arrays in LDS buy an
+// occupancy step at 16 and 32 tokens. A range of at most 64 columns gives
+// the same bits in both forms. The one-token kernel keeps the 128-column
+// form (its 64-column form was 1-3 % slower on the Llama-70B layer).
+constexpr int kMaxWaveCols = 128;
+constexpr int kNarrowWaveCols = 64;
 constexpr int kMaxBatch = 32;
 constexpr int kBmBytes = kBatch * kMaxWords * 8;          // bitmap words of one batch
 constexpr int kBatchBytes = kBatch * kSlotBytes + kBmBytes;  // one ring slot
@@ -326,10 +327,19 @@ constexpr int kMRowBytes = 24;
 // scale per row (else fp16); MM: accumulate on the matrix cores (8 or more
 // tokens: the product of a batch of 8 active columns with up to 32 tokens
 // is a small dense contraction; see step 4).
-template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MM, bool MP>
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MM, bool MP, int MWC>
 __device__ __forceinline__ void spmspv_body() {
   static_assert(!MM || (NB >= 8 && !Q && !EARLY), "the MFMA form serves 8 or more tokens of fp16 values");
   static_assert(!MP || (NB >= 4 && !Q && !EARLY), "several K ranges: 3 or more tokens of fp16 values");
+  static_assert(MWC == kNarrowWaveCols || MWC == kMaxWaveCols, "64- or 128-column ranges");
+  // the workgroup's list capacity; with early first batches the list holds
+  // at most kWgCols - kWaves kBatch columns (each wave's first kBatch active
+  // columns form its own first batch) plus the last batch's padding, and
+  // the waves' first batches follow it at kFirst; without, the list may use
+  // every entry
+  constexpr int kWgCols = kWaves * MWC;
+  constexpr int kFirst = kWgCols - kWaves * kBatch + kBatch;
+  static_assert(kFirst % kBatch == 0 && kFirst + kWaves * kBatch == kWgCols + kBatch, "list layout");
   using S = Smem<NB>;
   constexpr int kSlots = S::kSlots;
   __shared__ __attribute__((aligned(1024))) unsigned char ring[S::kRingBytes];
@@ -338,13 +348,13 @@ __device__ __forceinline__ void spmspv_body() {
   // column's values, the column's bitmap offset and the index of its
   // last 16-byte chunk}; padded to a whole batch with entries that load
   // nothing of use
-  __shared__ uint2 ent_s[kMaxWgCols + kBatch];
+  __shared__ uint2 ent_s[kWgCols + kBatch];
   // the entries' masked activations: per pair of entries a row of NB dwords
   // (token b: entry 2j in the low half, 2j + 1 in the high), from four
   // tokens on padded by one dword so that consecutive pairs start in
   // different banks; the MFMA form keeps each entry's NB values together
   constexpr int kXRow = (MM || NB < 4) ? NB : NB + 1;
-  __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kMaxWgCols + kBatch) * kXRow];
+  __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kWgCols + kBatch) * kXRow];
   __shared__ int cnt_s[kWaves];
 
   const int lane = threadIdx.x & 63;
@@ -431,7 +441,7 @@ __device__ __forceinline__ void spmspv_body() {
     // waited for once: lanes past the range (and waves past the last column)
     // read column k_begin's or column 0's entries, tokens past the batch read
     // the last token; none of those is used below.
-    constexpr int kChunks = kMaxWaveCols / 64;
+    constexpr int kChunks = MWC / 64;
     uint32_t ci[kChunks], to[kChunks], colx[kChunks], xb[kChunks][NB];
     const int k_safe = k_begin < cols ? k_begin : 0;
   #pragma unroll
@@ -611,7 +621,7 @@ __device__ __forceinline__ void spmspv_body() {
     }
     asm volatile("" ::"s"(phase));
     const bool has_first = EARLY && early_first && n_w > 0;
-    const int e_first = kFirstList + kBatch * wave;
+    const int e_first = kFirst + kBatch * wave;
     if (has_first) {
       int rank0 = 0;
   #pragma unroll
@@ -1060,13 +1070,13 @@ __device__ __forceinline__ void spmspv_body() {
 
 // The kernels: the vector-ALU forms, and the matrix-core form, whose 32 x 32
 // accumulator blocks live in AGPRs; two waves per SIMD are asked of it.
-template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MP>
+template <int NB, int WPC, bool EARLY, bool BMASK, bool Q, bool MP, int MWC>
 __global__ __launch_bounds__(kThreads) void spmspv_kernel(LaunchArgs) {
-  spmspv_body<NB, WPC, EARLY, BMASK, Q, false, MP>();
+  spmspv_body<NB, WPC, EARLY, BMASK, Q, false, MP, MWC>();
 }
-template <int NB, int WPC, bool BMASK>
+template <int NB, int WPC, bool BMASK, int MWC>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void spmspv_mm_kernel(LaunchArgs) {
-  spmspv_body<NB, WPC, false, BMASK, false, true, true>();
+  spmspv_body<NB, WPC, false, BMASK, false, true, true, MWC>();
 }
 
 using spdp::fail;
@@ -1236,8 +1246,8 @@ int upload(const std::vector<T>& v, void** dst) {
   return SPDP_OK;
 }
 
-template <int NB, int WPC, bool Q>
-hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, dim3 grid,
+template <int NB, int WPC, bool Q, int MWC>
+hipError_t launch_cols(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, dim3 grid,
                        hipStream_t stream) {
   // the one-token kernel has the early-first-batch form (no product with
   // more tokens asks for it); the kernels for more tokens have the shared
@@ -1249,52 +1259,63 @@ hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, 
   // the one-range kernel)
   if constexpr (NB == 1) {
     if (early) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q, false>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, true, false, Q, false, MWC>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   } else {
     if constexpr (NB >= 8 && !Q) {
       if (mm) {
         if (bmask)
-          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, true>), grid, dim3(kThreads), 0, stream, args);
+          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, true, MWC>), grid, dim3(kThreads), 0, stream, args);
         else
-          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, false>), grid, dim3(kThreads), 0, stream, args);
+          hipLaunchKernelGGL((spmspv_mm_kernel<NB, WPC, false, MWC>), grid, dim3(kThreads), 0, stream, args);
         return hipGetLastError();
       }
     }
     if constexpr (NB >= 4 && !Q) {
       if (multi) {
         if (bmask)
-          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, true>), grid, dim3(kThreads), 0, stream, args);
+          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, true, MWC>), grid, dim3(kThreads), 0, stream,
+                             args);
         else
-          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, true>), grid, dim3(kThreads), 0, stream, args);
+          hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, true, MWC>), grid, dim3(kThreads), 0, stream,
+                             args);
         return hipGetLastError();
       }
     }
     if (bmask) {
-      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, false>), grid, dim3(kThreads), 0, stream, args);
+      hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, true, Q, false, MWC>), grid, dim3(kThreads), 0, stream, args);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, false>), grid, dim3(kThreads), 0, stream, args);
+  hipLaunchKernelGGL((spmspv_kernel<NB, WPC, false, false, Q, false, MWC>), grid, dim3(kThreads), 0, stream, args);
   return hipGetLastError();
 }
 
+// wide: some product of the launch tests more than 64 columns per range
+template <int NB, int WPC, bool Q>
+hipError_t launch_form(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, bool wide, dim3 grid,
+                       hipStream_t stream) {
+  if (NB == 1 || wide) return launch_cols<NB, WPC, Q, kMaxWaveCols>(args, early, bmask, mm, multi, grid, stream);
+  if constexpr (NB > 1) return launch_cols<NB, WPC, Q, kNarrowWaveCols>(args, early, bmask, mm, multi, grid, stream);
+  return hipErrorInvalidValue;
+}
+
 template <int NB, int WPC>
-hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, bool q, dim3 grid,
-                      hipStream_t stream) {
-  return q ? launch_form<NB, WPC, true>(args, early, bmask, mm, multi, grid, stream)
-           : launch_form<NB, WPC, false>(args, early, bmask, mm, multi, grid, stream);
+hipError_t launch_one(const LaunchArgs& args, bool early, bool bmask, bool mm, bool multi, bool wide, bool q,
+                      dim3 grid, hipStream_t stream) {
+  return q ? launch_form<NB, WPC, true>(args, early, bmask, mm, multi, wide, grid, stream)
+           : launch_form<NB, WPC, false>(args, early, bmask, mm, multi, wide, grid, stream);
 }
 
 template <int NB>
-hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool mm, bool multi, bool q, dim3 grid,
-                  hipStream_t stream) {
+hipError_t launch(const LaunchArgs& args, int wpc, bool early, bool bmask, bool mm, bool multi, bool wide, bool q,
+                  dim3 grid, hipStream_t stream) {
   switch (wpc) {
-    case 1: return launch_one<NB, 1>(args, early, bmask, mm, multi, q, grid, stream);
-    case 2: return launch_one<NB, 2>(args, early, bmask, mm, multi, q, grid, stream);
-    case 3: return launch_one<NB, 3>(args, early, bmask, mm, multi, q, grid, stream);
-    default: return launch_one<NB, 4>(args, early, bmask, mm, multi, q, grid, stream);
+    case 1: return launch_one<NB, 1>(args, early, bmask, mm, multi, wide, q, grid, stream);
+    case 2: return launch_one<NB, 2>(args, early, bmask, mm, multi, wide, q, grid, stream);
+    case 3: return launch_one<NB, 3>(args, early, bmask, mm, multi, wide, q, grid, stream);
+    default: return launch_one<NB, 4>(args, early, bmask, mm, multi, wide, q, grid, stream);
   }
 }
 
@@ -1479,7 +1500,7 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
   std::memset(&la, 0, sizeof(la));
   la.batch = batch;
   int64_t widest = 0;
-  bool early = false, multi = false;
+  bool early = false, multi = false, wide = false;
   const bool bmask = mask == SPDP_MASK_BATCH && batch > 1;
   for (int i = 0; i < count; ++i) {
     int64_t n_wg = 0;
@@ -1494,6 +1515,7 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
     widest = std::max(widest, n_wg);
     early = early || la.m[i].early_first;
     multi = multi || la.m[i].passes > 1;
+    wide = wide || la.m[i].wave_cols > kNarrowWaveCols;
   }
 
   const int wpc = handles[0]->tile_m / 64;
@@ -1502,17 +1524,17 @@ int launch_products(const spdp_handle_t* handles, int32_t count, const uint16_t*
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool mm = use_mfma(batch);
   if (batch <= 1)
-    e = launch<1>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<1>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   else if (batch <= 2)
-    e = launch<2>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<2>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   else if (batch <= 4)
-    e = launch<4>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<4>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   else if (batch <= 8)
-    e = launch<8>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<8>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   else if (batch <= 16)
-    e = launch<16>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<16>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   else
-    e = launch<32>(la, wpc, early, bmask, mm, multi, q, grid, s);
+    e = launch<32>(la, wpc, early, bmask, mm, multi, wide, q, grid, s);
   if (e != hipSuccess) return hip_fail(e, "kernel launch");
   return SPDP_OK;
 }
