@@ -48,16 +48,23 @@ def build(verbose: bool = False) -> str:
         ([cc] + common + device + ["-c", os.path.join(CSRC, "spmm.hip"),
                                    "-o", os.path.join(objdir, "spmm.o")]),
     ]
+    # the sources compile concurrently (the decode kernels' instantiations
+    # take most of the time)
+    procs = []
     for cmd in jobs:
         if verbose:
             print(" ".join(cmd), flush=True)
-        res = subprocess.run(cmd, capture_output=True, text=True)
-        out = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
-                        if "packed-fp32-ops" not in l)
-        if res.returncode != 0:
-            raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{out}")
+        procs.append((cmd, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+    failed = None
+    for cmd, proc in procs:
+        text, _ = proc.communicate()
+        out = "\n".join(l for l in text.splitlines() if "packed-fp32-ops" not in l)
+        if proc.returncode != 0 and failed is None:
+            failed = f"compile failed: {' '.join(cmd)}\n{out}"
         if verbose and out.strip():
             print(out, flush=True)
+    if failed:
+        raise RuntimeError(failed)
     tmp = LIB + ".tmp"
     link = [cc, "-shared", f"--offload-arch={ARCH}", "-o", tmp,
             os.path.join(objdir, "host.o"), os.path.join(objdir, "spdp.o"), os.path.join(objdir, "spmm.o"),
