@@ -707,7 +707,7 @@ def roof(step_bytes, step_flops, ms, batch=1):
 SECONDARY = [
     ("single-1024", 0.5, 0.5, [1]),
     ("llama7b-mlp", 0.6, 0.5, [1, 2, 4, 8]),
-    ("llama13b-layer", 0.7, 0.5, [1, 4, 16]),
+    ("llama13b-layer", 0.7, 0.5, [1, 4, 8, 16]),
     ("llama70b-layer", 0.7, 0.5, [1, 8, 32]),
     ("llama70b-layer", 0.5, 0.0, [1, 8, 32]),
     ("llama70b-layer", 0.8, 0.7, [1]),
