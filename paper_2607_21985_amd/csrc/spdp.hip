@@ -1107,10 +1107,11 @@ constexpr int64_t kMaxWorkgroups = 1792;
 // The 32x32 matrix-core form (a 32-row block x 32 tokens per instruction)
 // runs only when SPDP_MFMA=1 asks for it, from 5 tokens on: the vector forms
 // (one 4x4x4 product per 64-row word and four tokens from 3 tokens on) are
-// as fast or faster at every measured size, at 32 tokens per product on the
-// Llama-70B layer 90 against 92 us (70/50) and 94 against 93 (50/0), the
-// Llama-13B layer 49 against 58, the Llama-7B MLP 51 against 76. A property
-// of the batch only, so a product gives the same bits alone and grouped.
+// as fast or faster at every measured size, at 32 tokens per product on one
+// box, both with the passes below, on the Llama-70B layer 92.0 against
+// 93.3 us (70/50) and 91.7 against 95.9 (50/0), the Llama-13B layer 50.4
+// against 53.1, the Llama-7B MLP 51.6 against 55.6. A property of the batch
+// only, so a product gives the same bits alone and grouped.
 bool use_mfma(int batch) {
   if (batch < 5) return false;
   if (const char* env = std::getenv("SPDP_MFMA")) return std::atoi(env) != 0;
@@ -1126,9 +1127,10 @@ bool use_mfma(int batch) {
 // or 4 passes everywhere: Llama-70B layer 46.7 / 43.1 / 50.2 and 58.4 / 51.6 /
 // 58.0 us, Llama-13B 23.4 / 24.1 / 30.6 and 31.9 / 29.9 / 36.1, Llama-7B MLP
 // (8 tokens) 24.9 / 25.7 / 37.3; at 32 tokens the rule (4 passes on the
-// Llama-70B products but k and v, 2 on most others) is within 1 % of the best
-// uniform count on each layer (the Llama-7B MLP at 4 passes everywhere: 46 %
-// slower). One or two tokens and the code forms walk one range. SPDP_PASSES
+// Llama-70B products but k and v, 2 on most others) is within 1-3 % of the
+// best uniform count on each layer (the Llama-7B MLP at 4 passes everywhere:
+// 46 % slower: 516 workgroups in the grouped gate/up launch against 512
+// resident at two per CU). One or two tokens and the code forms walk one range. SPDP_PASSES
 // overrides (for tuning). A property of the matrix and the batch, like the
 // split, so a product gives the same bits alone and grouped.
 int passes_for(int batch, bool codes, int64_t stripes, int64_t segs) {
