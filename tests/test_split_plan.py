@@ -111,3 +111,18 @@ def test_invalid_arguments():
     assert L.spdp_split_plan(m._h, 1, None, refs[1], refs[2]) == ERR_INVALID
     assert [o.value for o in out] == [-7, -7, -7], "a refused call wrote its outputs"
     m.close()
+
+
+def test_noalloc_workspace_holds_every_llama_projection(plans):
+    # the static workspace of spdp_spmspv_noalloc (SPDP_NOALLOC_PARTIAL_BYTES,
+    # 40 MiB) holds the partials of every Llama 7B/13B/70B projection at
+    # every batch up to 32: 8 bytes x segments x batch x rows rounded up to
+    # the 256-row tile
+    limit = 40 << 20
+    worst = 0
+    for (rows, cols), (stripes, by_batch) in plans.items():
+        for b, (segs, _, _) in by_batch.items():
+            need = 8 * segs * b * stripes * 256
+            assert need <= limit, (rows, cols, b, need)
+            worst = max(worst, need)
+    assert worst == 8 * 22 * 29 * 32 * 256  # 8192x8192 at 29 tokens: 39.9 MiB, the most
