@@ -44,6 +44,11 @@ def _products(shapes, sw, p, batch, seed, share_x=False):
     # the 300x1024 one a single range: the launch runs the several-range
     # kernel, whose one-range products must keep their single-call bits
     ([(4096, 4096), (300, 1024)], (256, 16), 0.6, 0.5, 20, False),
+    # 256x16384 tests 96 columns per wave and range, so from two tokens on
+    # the launch runs the 128-column kernels, while the 300x1024 product
+    # alone runs the 64-column ones: the same bits either way
+    ([(256, 16384), (300, 1024)], (256, 16), 0.6, 0.5, 8, False),
+    ([(256, 16384), (300, 1024)], (256, 16), 0.6, 0.5, 20, False),
 ])
 def test_many_matches_oracle_and_single_calls(shapes, tile, sw, p, batch, share_x):
     dev = _dev()
