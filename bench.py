@@ -1020,6 +1020,12 @@ def main():
 
 PASS_R = ["TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum", "TCC_EA0_RDREQ_sum"]
 PASS_W = ["TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum", "TCC_BUBBLE_sum", "TCC_EA0_RDREQ_DRAM_sum"]
+# shader-sequencer passes: where the waves' cycles go, and the instruction mix
+PASS_S = [["SQ_WAVES", "SQ_BUSY_CYCLES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY",
+           "SQ_ACTIVE_INST_ANY", "SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "GRBM_GUI_ACTIVE"],
+          ["SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_VALU", "SQ_ACTIVE_INST_SCA", "SQ_WAIT_INST_LDS",
+           "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_LDS", "SQ_INSTS_VALU", "SQ_INSTS_MFMA", "GRBM_GUI_ACTIVE"],
+          ["SQ_INSTS_SALU", "SQ_INSTS_SMEM", "SQ_INSTS_BRANCH", "SQ_ACTIVE_INST_MISC", "GRBM_GUI_ACTIVE"]]
 
 
 def _profile_line(path):
@@ -1048,7 +1054,9 @@ def _counters(path):
 
 def _cmd(kind, d, tag, pj, extra=""):
     prof = {"trace": "--kernel-trace --stats", "pmcR": "--pmc " + " ".join(PASS_R),
-            "pmcW": "--pmc " + " ".join(PASS_W)}[kind]
+            "pmcW": "--pmc " + " ".join(PASS_W)}
+    prof.update({f"pmcS{i + 1}": "--pmc " + " ".join(p) for i, p in enumerate(PASS_S)})
+    prof = prof[kind]
     return (f"rocprofv3 {prof} --output-format csv -d {d}/{kind}_{tag} -o run -- python3 bench.py "
             + " ".join(pj["argv"]) + f" > {d}/{kind}_{tag}.log")
 
@@ -1074,6 +1082,47 @@ def summarize_prefill(d, prof_dir):
     out += [f"spmm_sha: {kernel_source_sha(open(os.path.join(ROOT, 'paper_2607_21985_amd', 'csrc', 'spmm.hip')).read())}",
             ""]
     with open(os.path.join(prof_dir, "spmm_prefill_kernel_trace.txt"), "w") as fh:
+        fh.write("\n".join(out))
+    print("\n".join(out))
+
+
+def summarize_sq(d, tag, pj, prof_dir, sha):
+    """profiles/sq_spmspv_<tag>.txt from three shader-sequencer counter passes:
+    the mean per spMspV dispatch of each counter, the instruction mix per
+    64-row bitmap word decoded (the algorithmic bitmap bytes / 8), and the
+    fractions of the waves' cycles spent issuing and waiting."""
+    cs, cmds = {}, []
+    for i in range(len(PASS_S)):
+        kind = f"pmcS{i + 1}"
+        cs.update(_counters(os.path.join(d, f"{kind}_{tag}", "run_counter_collection.csv")))
+        cmds.append("  " + _cmd(kind, d, tag, _profile_line(os.path.join(d, f"{kind}_{tag}.log"))))
+
+    def mean(name):
+        v = cs.get(name, ([], []))[0]
+        return sum(v) / len(v) if v else float("nan")
+
+    words = pj["line_model_per_launch"]["bitmap"][0] / 8.0
+    wc = mean("SQ_WAVE_CYCLES")
+    out = [f"# shader-sequencer counters of spmspv_kernel: {tag}", "",
+           "commands (GPU box, repository root, TMPDIR=/tmp), one counter pass per run:"] + cmds + [
+           "", f"mean per spMspV dispatch ({len(cs['SQ_WAVES'][0])} dispatches in the first pass):"]
+    for p in PASS_S:
+        for name in p:
+            if name != "GRBM_GUI_ACTIVE" or p is PASS_S[0]:
+                out.append(f"  {name:26s} {mean(name):16.0f}")
+    out += ["", f"64-row bitmap words decoded per launch (algorithmic bitmap bytes / 8): {words:.0f}",
+            "instructions per word: " + ", ".join(
+                f"{k} {mean(n) / words:.2f}" for k, n in (("VALU", "SQ_INSTS_VALU"), ("SALU", "SQ_INSTS_SALU"),
+                                                          ("LDS", "SQ_INSTS_LDS"), ("MFMA", "SQ_INSTS_MFMA"),
+                                                          ("SMEM", "SQ_INSTS_SMEM"), ("branch", "SQ_INSTS_BRANCH"))),
+            "share of the waves' cycles: " + ", ".join(
+                f"{k} {mean(n) / wc:.3f}" for k, n in (("issuing", "SQ_ACTIVE_INST_ANY"),
+                                                       ("waiting (any)", "SQ_WAIT_ANY"),
+                                                       ("waiting on dependencies", "SQ_WAIT_INST_ANY"))),
+            f"LDS bank conflicts per LDS instruction: "
+            f"{mean('SQ_LDS_BANK_CONFLICT') / max(mean('SQ_INSTS_LDS'), 1):.4f}",
+            f"kernel_sha: {sha}", ""]
+    with open(os.path.join(prof_dir, f"sq_spmspv_{tag}.txt"), "w") as fh:
         fh.write("\n".join(out))
     print("\n".join(out))
 
@@ -1109,6 +1158,9 @@ def summarize_profiles(d, prof_dir=None):
         with open(os.path.join(prof_dir, f"spmspv_{tag}_kernel_trace.txt"), "w") as fh:
             fh.write("\n".join(out))
         print("\n".join(out))
+
+        if all(os.path.isdir(os.path.join(d, f"pmcS{i + 1}_{tag}")) for i in range(len(PASS_S))):
+            summarize_sq(d, tag, pj, prof_dir, sha)
 
         pr, pw = os.path.join(d, f"pmcR_{tag}"), os.path.join(d, f"pmcW_{tag}")
         if not (os.path.isdir(pr) and os.path.isdir(pw)):

@@ -169,3 +169,40 @@ def test_profile_summaries_from_raw_counters(tmp_path):
     assert f"hbm_bytes_per_launch: {rd + wr}" in traffic
     assert "= 4096 = 1.0000 x the bytes read" in traffic
     assert f"kernel_sha: {bench.kernel_source_sha()}" in traffic
+
+
+def test_sq_summary_from_raw_counters(tmp_path):
+    """--summarize-profiles: the shader-sequencer passes give the per-word
+    instruction mix and the waves' cycle shares, on made-up counters."""
+    d = tmp_path / "raw"
+    out = tmp_path / "profiles"
+    out.mkdir()
+    tag = "wl_decoder"
+    pj = {"profile_only": True, "argv": ["--profile-only", "--workload", "wl"], "ms_per_step": 0.02,
+          "launches": 4, "launches_per_step": 2, "algorithmic_bytes_per_launch": 10000.0,
+          "y_bytes_per_launch": 100.0,
+          "line_model_per_launch": {"values": [8000, 8192], "bitmap": [800, 1024], "colinfo": [500, 512],
+                                    "tileoffset": [100, 128], "x": [300, 384], "y": [100, 128],
+                                    "scales": [0, 0]}}
+    (d / f"trace_{tag}").mkdir(parents=True)
+    (d / f"trace_{tag}.log").write_text(json.dumps(pj) + "\n")
+    (d / f"trace_{tag}" / "run_kernel_stats.csv").write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+        '"void spmspv_kernel<8, 4>(LaunchArgs)",4,40000,10000.0,90,9000,11000,1\n')
+    values = {"SQ_WAVES": 64, "SQ_WAVE_CYCLES": 1000, "SQ_WAIT_ANY": 400, "SQ_WAIT_INST_ANY": 150,
+              "SQ_ACTIVE_INST_ANY": 450, "SQ_LDS_BANK_CONFLICT": 3, "SQ_INSTS_LDS": 150, "SQ_INSTS_VALU": 800,
+              "SQ_INSTS_MFMA": 50, "SQ_INSTS_SALU": 600, "SQ_INSTS_SMEM": 20, "SQ_INSTS_BRANCH": 10}
+    hdr = '"Kernel_Name","Counter_Name","Counter_Value"\n'
+    for i, names in enumerate(bench.PASS_S):
+        kind = f"pmcS{i + 1}"
+        (d / f"{kind}_{tag}").mkdir()
+        (d / f"{kind}_{tag}.log").write_text(json.dumps(dict(pj, argv=pj["argv"] + [kind])) + "\n")
+        rows = "".join(f'"spmspv_kernel<8, 4>","{n}",{values.get(n, 7)}\n' for n in names for _ in range(2))
+        (d / f"{kind}_{tag}" / "run_counter_collection.csv").write_text(hdr + rows)
+    bench.summarize_profiles(str(d), str(out))
+    sq = (out / f"sq_spmspv_{tag}.txt").read_text()
+    # 800 bitmap bytes = 100 words
+    assert "instructions per word: VALU 8.00, SALU 6.00, LDS 1.50, MFMA 0.50, SMEM 0.20, branch 0.10" in sq
+    assert "issuing 0.450, waiting (any) 0.400, waiting on dependencies 0.150" in sq
+    assert "LDS bank conflicts per LDS instruction: 0.0200" in sq
+    assert "rocprofv3 --pmc SQ_WAVES" in sq and f"kernel_sha: {bench.kernel_source_sha()}" in sq
