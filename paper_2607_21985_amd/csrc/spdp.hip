@@ -354,6 +354,16 @@ __device__ __forceinline__ void spmspv_body() {
   // tokens on padded by one dword so that consecutive pairs start in
   // different banks; the MFMA form keeps each entry's NB values together
   constexpr int kXRow = (MM || NB < 4) ? NB : NB + 1;
+  // from four tokens (vector forms) the pair rows of a quad are interleaved
+  // by token, so that the 4x4x4 product's A operand (both pair rows of one
+  // token) is one 8-byte read: dword (q kXRow + b) 2 + h holds token b of
+  // entries 4q + 2h (low half) and 4q + 2h + 1 (high half); the row of
+  // kXRow = NB + 1 keeps the quads' stores in different banks
+  constexpr bool kQuadRows = !MM && NB >= 4;
+  auto xs_at = [&](int p, int b) __attribute__((always_inline)) {
+    return kQuadRows ? (((p >> 2) * kXRow + b) * 2 + ((p >> 1) & 1)) * 2 + (p & 1)
+                     : ((p >> 1) * kXRow + b) * 2 + (p & 1);
+  };
   __shared__ __attribute__((aligned(16))) uint16_t xs_s[(kWgCols + kBatch) * kXRow];
   __shared__ int cnt_s[kWaves];
 
@@ -558,11 +568,11 @@ __device__ __forceinline__ void spmspv_body() {
         for (int b = 0; b < NB; ++b) {
           if constexpr (kXm) {
             const uint32_t v = xm[c][b >> 1];
-            xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = (b & 1) ? (uint16_t)(v >> 16) : (uint16_t)v;
+            xs_s[xs_at(p, b)] = (b & 1) ? (uint16_t)(v >> 16) : (uint16_t)v;
           } else {
             const int mag = (int)(xb[c][b] & 0x7FFFu);
             const bool on = b < batch_q && (BMASK || (mag > code_q && mag <= 0x7C00));
-            xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
+            xs_s[xs_at(p, b)] = on ? (uint16_t)xb[c][b] : (uint16_t)0;
           }
         }
       }
@@ -574,7 +584,7 @@ __device__ __forceinline__ void spmspv_body() {
         for (int k = 0; k < kPieces; ++k) *reinterpret_cast<uint4*>(&xs_s[p * NB + 8 * k]) = make_uint4(0u, 0u, 0u, 0u);
       } else {
   #pragma unroll
-        for (int b = 0; b < NB; ++b) xs_s[((p >> 1) * kXRow + b) * 2 + (p & 1)] = 0;
+        for (int b = 0; b < NB; ++b) xs_s[xs_at(p, b)] = 0;
       }
     };
 
@@ -769,12 +779,11 @@ __device__ __forceinline__ void spmspv_body() {
         for (int w = 0; w < WPC; ++w)
           wv[w] = make_uint2(pair_under_words_mfma(vb[0][w], vb[1][w], m[0][w], m[1][w]),
                              pair_under_words_mfma(vb[2][w], vb[3][w], m[2][w], m[3][w]));
-        const uint32_t* xp0 = reinterpret_cast<const uint32_t*>(&xs_s[((e0 + u0) / 2) * kXRow * 2]);
-        const uint32_t* xp1 = xp0 + kXRow;
+        const uint2* xq = reinterpret_cast<const uint2*>(&xs_s[((e0 + u0) / 4) * kXRow * 4]);
   #pragma unroll
         for (int g = 0; g < NB / 4; ++g) {
           const int t = 4 * g + (lane & 3);
-          const half4_t xa = __builtin_bit_cast(half4_t, make_uint2(xp0[t], xp1[t]));
+          const half4_t xa = __builtin_bit_cast(half4_t, xq[t]);
   #pragma unroll
           for (int w = 0; w < WPC; ++w)
             acc4[w][g] = __builtin_amdgcn_mfma_f32_4x4x4f16(xa, __builtin_bit_cast(half4_t, wv[w]), acc4[w][g], 0, 0, 0);
